@@ -1,0 +1,206 @@
+/*
+ * kafila_stage.h -- one pipeline stage of a decoder-only LLM on one MI355X (gfx950).
+ *
+ * In Kafila (arxiv 2609.34045) a model's contiguous chain of transformer blocks
+ * is divided among the members of a ring; each member runs a *stage*: the
+ * hidden state of every token passes through its block range, and the member
+ * holding the *head* also embeds tokens before its blocks and unembeds and
+ * samples after the model's last block (Section III and Fig. 1).  A stage's
+ * decode cost is dominated by reading its weights once per token (Section V-A,
+ * eq. (2)); the session reserves cache for a declared context and concurrency
+ * and refuses a plan that would exhaust a device (Sections V-C, V-D).
+ *
+ * The block is a pre-norm decoder layer: RMSNorm, grouped-query attention with
+ * rotate-half RoPE over a per-user KV cache, SwiGLU MLP, no biases.  The head is
+ * an embedding gather, a final RMSNorm, the vocabulary projection and a greedy
+ * argmax (lowest index on ties).
+ *
+ * Conventions
+ *  - "_dev" pointers are device pointers on the stage's device; other pointers
+ *    are host pointers.  The caller owns every I/O buffer.
+ *  - bf16 tensors are passed as uint16_t bit patterns.  Matrices are row-major
+ *    [out, in] (the layout of a linear layer's weight).
+ *  - Compute calls only enqueue work on the stage's stream and return; argument
+ *    checks run on the host before anything is enqueued, and a call that fails
+ *    them changes no state.  Errors of enqueued work are sticky and surface from
+ *    kf_stage_sync() or the next call as KF_EDEVICE.
+ *  - A stage and its KV caches are not thread-safe; distinct stages are
+ *    independent.  kf_last_error() returns a thread-local message for the last
+ *    failure on the calling thread.
+ *  - Requirements checked at init: head_dim in {64, 128}; n_q_heads a multiple
+ *    of n_kv_heads with at most 8 query heads per KV head; hidden and ffn
+ *    multiples of 64.  Anything else is KF_EUNSUPPORTED.
+ */
+#ifndef KAFILA_STAGE_H
+#define KAFILA_STAGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KF_ABI_VERSION 1
+#define KF_MAX_BATCH 4
+
+typedef struct kf_stage kf_stage;
+typedef struct kf_kv kf_kv;
+
+typedef enum {
+  KF_OK = 0,
+  KF_EINVAL = 1,       /* malformed argument (NULL, size mismatch, position gap, bad range) */
+  KF_ENOMEM = 2,       /* a device or host allocation failed */
+  KF_ERANGE = 3,       /* a position or length beyond the declared capacity */
+  KF_ESTATE = 4,       /* call not allowed in this state (e.g. head call on a stage without the head) */
+  KF_EDEVICE = 5,      /* a HIP error, including a sticky error from earlier enqueued work */
+  KF_EUNSUPPORTED = 6  /* a model shape the kernels are not built for */
+} kf_status;
+
+typedef enum { KF_F32 = 0, KF_BF16 = 1 } kf_dtype; /* element type of hidden-state I/O */
+
+typedef struct {
+  int32_t n_layers;   /* layers in the whole model (the stage holds a sub-range) */
+  int32_t hidden;     /* H */
+  int32_t n_q_heads;  /* nq */
+  int32_t n_kv_heads; /* nkv; query head h reads KV head h / (nq / nkv) */
+  int32_t head_dim;   /* hd */
+  int32_t ffn;        /* F */
+  int32_t vocab;      /* V (used only with the head) */
+  float rms_eps;      /* RMSNorm epsilon, added to mean(x^2) inside the square root */
+  float rope_theta;   /* RoPE base: pair (i, i + hd/2) turns by pos * theta^(-2i/hd) */
+} kf_model_config;
+
+typedef enum {
+  KF_W_ATTN_NORM = 0, /* [H]            gain of the attention RMSNorm */
+  KF_W_Q = 1,         /* [nq*hd, H] */
+  KF_W_K = 2,         /* [nkv*hd, H] */
+  KF_W_V = 3,         /* [nkv*hd, H] */
+  KF_W_O = 4,         /* [H, nq*hd] */
+  KF_W_MLP_NORM = 5,  /* [H]            gain of the MLP RMSNorm */
+  KF_W_GATE = 6,      /* [F, H] */
+  KF_W_UP = 7,        /* [F, H] */
+  KF_W_DOWN = 8,      /* [H, F] */
+  KF_W_EMBED = 9,     /* [V, H]         head only */
+  KF_W_FINAL_NORM = 10, /* [H]          head only */
+  KF_W_LM_HEAD = 11   /* [V, H]         head only (not tied to the embedding) */
+} kf_tensor_kind;
+
+typedef struct {
+  int32_t layer;        /* global layer index in [layer_lo, layer_hi); -1 for head tensors */
+  int32_t kind;         /* kf_tensor_kind */
+  const uint16_t* bf16; /* host pointer to row-major bf16 bits */
+  int64_t numel;        /* must equal the element count of the kind's shape */
+} kf_tensor;
+
+typedef struct {
+  const kf_tensor* tensors;
+  int32_t count;
+} kf_weights;
+
+/* ABI version of the loaded library (KF_ABI_VERSION at build time). */
+int32_t kf_abi_version(void);
+
+/* Thread-local message describing the last failed call on this thread ("" if none). */
+const char* kf_last_error(void);
+
+/*
+ * Byte sizes behind the stage-cost model (Section V-A, eq. (2)) and the block
+ * limit at a declared context and concurrency (Section V-C).
+ *   beta_block : bytes of one decoder layer's weights (bf16, including both gains)
+ *   beta_head  : bytes of the head's weights (embedding + final gain + LM head), 0 without the head
+ *   resident   : device bytes kf_stage_init + kf_kv_create(max_users, max_ctx) would hold for
+ *                layers [lo, hi): weights, KV cache, RoPE table and decode workspaces
+ * Host only; any output pointer may be NULL.  KF_EINVAL for an invalid config or range.
+ */
+kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t layer_lo, int32_t layer_hi, int32_t has_head,
+                         int32_t max_users, int32_t max_ctx, int64_t* beta_block, int64_t* beta_head,
+                         int64_t* resident);
+
+/*
+ * Create a stage holding layers [layer_lo, layer_hi) of the model and, if has_head,
+ * the head.  Weight tensors are copied to the current HIP device (the stage's
+ * device) before the call returns, so the caller may free them afterwards.  Every
+ * layer tensor of every held layer must be present exactly once, plus the three
+ * head tensors when has_head; anything else is KF_EINVAL.  hip_stream (a
+ * hipStream_t, NULL for the default stream) is where all later work is enqueued.
+ */
+kf_status kf_stage_init(const kf_model_config* cfg, int32_t layer_lo, int32_t layer_hi, int32_t has_head,
+                        const kf_weights* weights, void* hip_stream, kf_stage** out);
+
+/* Waits for the stage's stream, then frees its device memory.  KV caches of the stage must be destroyed first. */
+kf_status kf_stage_destroy(kf_stage* stage);
+
+/* Replace the stream later work is enqueued on (the caller orders it after earlier work). */
+kf_status kf_stage_set_stream(kf_stage* stage, void* hip_stream);
+
+/* Wait for all enqueued work; KF_EDEVICE (with the HIP error text) if any of it failed. */
+kf_status kf_stage_sync(kf_stage* stage);
+
+/*
+ * Reserve a KV cache for max_users concurrent users of context up to max_ctx tokens
+ * each, for every layer the stage holds (the declared concurrency x context of
+ * Section V-C).  Layout on the device: bf16 K and V, [layer][user][kv_head][pos][hd].
+ * All user lengths start at 0.  KF_ENOMEM if the device cannot hold it.
+ */
+kf_status kf_kv_create(kf_stage* stage, int32_t max_users, int32_t max_ctx, kf_kv** out);
+kf_status kf_kv_destroy(kf_kv* kv);
+
+/* Number of cached positions of a user (a host-side value; no device sync). */
+kf_status kf_kv_len(const kf_kv* kv, int32_t user, int32_t* len);
+
+/* Set a user's length to any value in [0, max_ctx]: 0 resets the user; positions below
+ * len are from then on taken as valid in every layer (e.g. after kf_kv_write). */
+kf_status kf_kv_set_len(kf_kv* kv, int32_t user, int32_t len);
+
+/*
+ * Copy n positions of keys (already rotated) and values for one held layer and user,
+ * from k_dev / v_dev laid out [n, nkv, hd] in dtype (KF_BF16 bits or KF_F32, rounded
+ * to bf16 to nearest even), into positions [pos0, pos0 + n).  Does not change lengths.
+ * KF_ERANGE if pos0 + n > max_ctx.  Enqueued on the stage's stream.
+ */
+kf_status kf_kv_write(kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, const void* k_dev,
+                      const void* v_dev, kf_dtype dtype);
+
+/* Copy positions [pos0, pos0 + n) of one layer and user out as bf16 bits, [n, nkv, hd]. */
+kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, uint16_t* k_dev,
+                     uint16_t* v_dev);
+
+/*
+ * Forward one token for each of `batch` (1..KF_MAX_BATCH) users (decode).
+ *   users[b], positions[b] : host arrays; users distinct and < max_users;
+ *                            positions[b] must equal the user's current length
+ *                            (append-only; else KF_EINVAL) and be < max_ctx (else KF_ERANGE).
+ *   tokens_dev  : int32 [batch] token ids (stage with the head only), or NULL
+ *   hidden_in_dev : [batch, H] in `io`, or NULL; exactly one of tokens_dev / hidden_in_dev
+ *   hidden_out_dev : [batch, H] in `io`; may alias hidden_in_dev
+ * Row b's token is at positions[b]: its key and value are written at that slot of
+ * the user's cache in every held layer, and it attends slots 0..positions[b].
+ * On success every user's length advances by one.
+ */
+kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32_t* users,
+                          const int32_t* positions, const int32_t* tokens_dev, const void* hidden_in_dev,
+                          void* hidden_out_dev, kf_dtype io);
+
+/*
+ * Forward a chunk of n_tokens consecutive tokens of one user starting at pos0 (prefill).
+ * pos0 must equal the user's length and pos0 + n_tokens <= max_ctx.  Token i attends
+ * slots 0..pos0+i.  tokens_dev int32 [n] or hidden_in_dev [n, H]; hidden_out_dev [n, H].
+ * Dense products run on the matrix cores with bf16 operands and fp32 accumulation.
+ * On success the user's length advances by n_tokens.
+ */
+kf_status kf_stage_prefill(kf_stage* stage, kf_kv* kv, int32_t user, int32_t pos0, int32_t n_tokens,
+                           const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev,
+                           kf_dtype io);
+
+/* logits_dev fp32 [rows, V] = RMSNorm(hidden; final gain) x LM_head^T.  Head stages only (else KF_ESTATE). */
+kf_status kf_head_logits(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype, float* logits_dev);
+
+/* token_dev int32 [rows] = greedy argmax of the logits (lowest index on ties);
+ * max_logit_dev fp32 [rows] (may be NULL) receives the winning logit.  rows <= KF_MAX_BATCH. */
+kf_status kf_head_argmax(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype,
+                         int32_t* token_dev, float* max_logit_dev);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KAFILA_STAGE_H */

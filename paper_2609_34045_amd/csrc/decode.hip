@@ -1,0 +1,618 @@
+// Decode-path kernels for gfx950 (CDNA4): one token per user, batch 1..4.
+//
+// At this batch size a stage reads each weight once per step and does a
+// handful of FLOPs per weight byte, so every matrix product here is an
+// HBM-bound GEMV (Section V-A of the paper prices a stage by exactly these
+// bytes).  The kernels therefore stream bf16 weights with 16-byte non-temporal
+// loads, keep the (tiny) activations in L1/L2, and fuse everything elementwise
+// into the GEMV that produces or consumes it:
+//   * RMSNorm is folded into the consuming GEMV: the same loop that multiplies
+//     a weight chunk by the input chunk also accumulates sum(x^2), so the
+//     normalisation costs no extra pass;  y = rsqrt(mean(x^2)+eps) * W (x * g).
+//   * RoPE and the KV-cache append run in the QKV GEMV's epilogue: one
+//     workgroup owns rows i and i + hd/2 of a head, the pair RoPE rotates.
+//   * SwiGLU runs in the gate/up GEMV's epilogue; the residual add in the
+//     O and down GEMVs' epilogues.
+//   * The LM-head GEMV reduces (max, lowest index) per workgroup.
+// Attention is split-KV over a bf16 cache, [user][kv_head][pos][hd]; each
+// workgroup serves all query heads of one KV head, and the last workgroup of
+// a (row, KV head) merges the splits (online-softmax rescaling).
+#include "kernels.h"
+
+namespace kf {
+
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4u ld_stream(const v4u* p) { return __builtin_nontemporal_load(p); }
+
+__device__ __forceinline__ void bf16x8(const v4u w, float (&f)[8]) {
+  f[0] = __uint_as_float(w.x << 16);
+  f[1] = __uint_as_float(w.x & 0xffff0000u);
+  f[2] = __uint_as_float(w.y << 16);
+  f[3] = __uint_as_float(w.y & 0xffff0000u);
+  f[4] = __uint_as_float(w.z << 16);
+  f[5] = __uint_as_float(w.z & 0xffff0000u);
+  f[6] = __uint_as_float(w.w << 16);
+  f[7] = __uint_as_float(w.w & 0xffff0000u);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// Round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Reduce-scatter of N per-lane values over a 64-lane wave: after it, v[0] of
+// lane l holds the wave total of value index (l >> (6 - log2 N)).  Each step
+// trades half of the remaining values with the lane O apart, so N values cost
+// N - 1 shuffles (plus the all-reduce of the last one over the lanes that
+// share an index) instead of 6 N.
+template <int N, int O>
+struct Butterfly {
+  static __device__ __forceinline__ void run(float* v, int lane) {
+    const bool up = (lane & O) != 0;
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) {
+      const float keep = up ? v[i + N / 2] : v[i];
+      const float send = up ? v[i] : v[i + N / 2];
+      v[i] = keep + __shfl_xor(send, O);
+    }
+    Butterfly<N / 2, O / 2>::run(v, lane);
+  }
+};
+template <int O>
+struct Butterfly<1, O> {
+  static __device__ __forceinline__ void run(float* v, int lane) {
+    v[0] += __shfl_xor(v[0], O);
+    Butterfly<1, O / 2>::run(v, lane);
+  }
+};
+template <>
+struct Butterfly<1, 0> {
+  static __device__ __forceinline__ void run(float*, int) {}
+};
+
+constexpr int ilog2(int n) { return n <= 1 ? 0 : 1 + ilog2(n / 2); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// ------------------------------------------------------------------ GEMV
+// Workgroup of 256 threads owns R output rows of every batch row; its threads
+// stride over K in 16-byte chunks (thread t takes chunks t, t+256, ...), so
+// each wave's loads of a row are 1 KB contiguous.  U chunks of all R rows are
+// in flight per thread before any is consumed.
+template <int B, int R, int EPI, bool NORM>
+__global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
+  constexpr int T = 256, U = 2;
+  constexpr int NV = R * B + (NORM ? B : 0);
+  constexpr int NVP = NV <= 8 ? 8 : NV <= 16 ? 16 : NV <= 32 ? 32 : 64;
+  static_assert(NV <= 64, "too many partial sums per workgroup");
+  constexpr int LPI = 64 / NVP;  // lanes sharing one reduced value
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wg = blockIdx.x;
+  const int K = p.K, nch = K >> 3;
+
+  // Row pointers of this workgroup.
+  const v4u* wrow[R];
+  bool rok[R];
+  int head = 0, i0 = 0;
+  if (EPI == kEpiQKV) {
+    const int wg_per_head = p.hd / R;
+    head = wg / wg_per_head;
+    i0 = (wg % wg_per_head) * (R / 2);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int row = head * p.hd + (r < R / 2 ? i0 + r : p.hd / 2 + i0 + r - R / 2);
+      wrow[r] = reinterpret_cast<const v4u*>(p.w0 + (int64_t)row * K);
+      rok[r] = true;
+    }
+  } else if (EPI == kEpiSwiGLU) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int row = wg * (R / 2) + (r < R / 2 ? r : r - R / 2);
+      wrow[r] = reinterpret_cast<const v4u*>((r < R / 2 ? p.w0 : p.w1) + (int64_t)row * K);
+      rok[r] = true;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int row = wg * R + r;
+      rok[r] = row < p.N;
+      wrow[r] = reinterpret_cast<const v4u*>(p.w0 + (int64_t)(rok[r] ? row : 0) * K);
+    }
+  }
+
+  float acc[NVP];
+#pragma unroll
+  for (int i = 0; i < NVP; ++i) acc[i] = 0.f;
+
+  for (int c0 = tid; c0 < nch; c0 += T * U) {
+    v4u wv[U][R];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * T;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (c < nch && rok[r]) wv[u][r] = ld_stream(wrow[r] + c);
+        else wv[u][r] = v4u{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * T;
+      if (c < nch) {
+        float xf[B][8];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          const v4f* src = reinterpret_cast<const v4f*>(p.in + (int64_t)b * K + c * 8);
+          const v4f lo = src[0], hi = src[1];
+          xf[b][0] = lo.x; xf[b][1] = lo.y; xf[b][2] = lo.z; xf[b][3] = lo.w;
+          xf[b][4] = hi.x; xf[b][5] = hi.y; xf[b][6] = hi.z; xf[b][7] = hi.w;
+        }
+        if (NORM) {
+          float gf[8];
+          bf16x8(*reinterpret_cast<const v4u*>(p.gain + c * 8), gf);
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              acc[R * B + b] += xf[b][i] * xf[b][i];
+              xf[b][i] *= gf[i];
+            }
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          float wf[8];
+          bf16x8(wv[u][r], wf);
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[r * B + b] += wf[i] * xf[b][i];
+          }
+        }
+      }
+    }
+  }
+
+  Butterfly<NVP, 32>::run(acc, lane);
+  __shared__ float red[4][NVP];
+  __shared__ float fin[NVP];
+  if ((lane & (LPI - 1)) == 0) red[wave][lane / LPI] = acc[0];
+  __syncthreads();
+  if (tid < NVP) fin[tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+  __syncthreads();
+
+  float rs[B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) rs[b] = NORM ? 1.0f / sqrtf(fin[R * B + b] / (float)K + p.eps) : 1.0f;
+
+  if (EPI == kEpiQKV) {
+    if (tid < (R / 2) * B) {
+      const int r = tid / B, b = tid % B;
+      const float y1 = fin[r * B + b] * rs[b];
+      const float y2 = fin[(r + R / 2) * B + b] * rs[b];
+      const int hd = p.hd, half = hd / 2, i = i0 + r, pos = p.pos[b];
+      if (head < p.nq + p.nkv) {
+        const float c = p.rope_cos[(int64_t)pos * half + i], s = p.rope_sin[(int64_t)pos * half + i];
+        const float z1 = y1 * c - y2 * s, z2 = y2 * c + y1 * s;
+        if (head < p.nq) {
+          float* q = p.q + (int64_t)b * p.nq * hd + head * hd;
+          q[i] = z1;
+          q[i + half] = z2;
+        } else {
+          uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq) * p.max_ctx + pos) * hd;
+          k[i] = f32_to_bf16(z1);
+          k[i + half] = f32_to_bf16(z2);
+        }
+      } else {
+        uint16_t* v = p.vc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq - p.nkv) * p.max_ctx + pos) * hd;
+        v[i] = f32_to_bf16(y1);
+        v[i + half] = f32_to_bf16(y2);
+      }
+    }
+  } else if (EPI == kEpiResid) {
+    if (tid < R * B) {
+      const int r = tid / B, b = tid % B, row = wg * R + r;
+      if (row < p.N) {
+        const int64_t at = (int64_t)b * p.N + row;
+        const float v = p.x[at] + fin[tid];
+        p.x[at] = v;
+        if (p.out2) {
+          if (p.out2_bf16) reinterpret_cast<uint16_t*>(p.out2)[at] = f32_to_bf16(v);
+          else reinterpret_cast<float*>(p.out2)[at] = v;
+        }
+      }
+    }
+  } else if (EPI == kEpiSwiGLU) {
+    if (tid < (R / 2) * B) {
+      const int r = tid / B, b = tid % B;
+      const float gt = fin[r * B + b] * rs[b];
+      const float up = fin[(r + R / 2) * B + b] * rs[b];
+      p.act[(int64_t)b * p.N + wg * (R / 2) + r] = gt / (1.0f + expf(-gt)) * up;
+    }
+  } else {  // kEpiLMHead
+    if (p.logits && tid < R * B) {
+      const int r = tid / B, b = tid % B, row = wg * R + r;
+      if (row < p.N) p.logits[(int64_t)b * p.N + row] = fin[tid] * rs[b];
+    }
+    if (tid < B) {
+      const int b = tid;
+      float best = fin[b] * rs[b];
+      int bidx = wg * R;
+#pragma unroll
+      for (int r = 1; r < R; ++r) {
+        const float v = fin[r * B + b] * rs[b];
+        if (wg * R + r < p.N && v > best) {  // strict: the lower row keeps a tie
+          best = v;
+          bidx = wg * R + r;
+        }
+      }
+      p.part_val[(int64_t)b * p.n_wg + wg] = best;
+      p.part_idx[(int64_t)b * p.n_wg + wg] = bidx;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ attention
+// Workgroup (split s, KV head g, row b) covers keys [s*split, min((s+1)*split, len_b)).
+// A key's hd elements are read by hd/8 lanes, 16 bytes each; all G query heads of
+// the group are scored against it, so each K/V byte is read once per KV head.
+template <int HD, int G>
+__global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
+  constexpr int LPK = HD / 8;
+  constexpr int KPW = 64 / LPK;
+  constexpr int KPP = 4 * KPW;
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int len = p.len[b];
+  const int s0 = split * p.split;
+  const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
+  const int hq0 = g * G;
+
+  __shared__ float sc[G][kAttnMaxSplit];
+  __shared__ float red[4][G][HD];
+  __shared__ float ml[G][2];
+  __shared__ int is_last;
+
+  const int64_t head_off = (int64_t)p.users[b] * p.user_stride + (int64_t)g * p.max_ctx * HD;
+  const uint16_t* kb = p.kc + head_off + (int64_t)s0 * HD;
+  const uint16_t* vb = p.vc + head_off + (int64_t)s0 * HD;
+  const int d0 = (lane % LPK) * 8;
+  const int kslot = wave * KPW + lane / LPK;
+
+  float qv[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const v4f* src = reinterpret_cast<const v4f*>(p.q + (int64_t)b * p.nq * HD + (hq0 + h) * HD + d0);
+    const v4f lo = src[0], hi = src[1];
+    qv[h][0] = lo.x * p.scale_log2; qv[h][1] = lo.y * p.scale_log2;
+    qv[h][2] = lo.z * p.scale_log2; qv[h][3] = lo.w * p.scale_log2;
+    qv[h][4] = hi.x * p.scale_log2; qv[h][5] = hi.y * p.scale_log2;
+    qv[h][6] = hi.z * p.scale_log2; qv[h][7] = hi.w * p.scale_log2;
+  }
+
+  // scores (log2 domain)
+  for (int t = kslot; t < nk; t += KPP) {
+    float kf[8];
+    bf16x8(*reinterpret_cast<const v4u*>(kb + (int64_t)t * HD + d0), kf);
+    float d[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a += qv[h][i] * kf[i];
+      d[h] = a;
+    }
+#pragma unroll
+    for (int o = LPK / 2; o >= 1; o >>= 1) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) d[h] += __shfl_xor(d[h], o);
+    }
+    if ((lane % LPK) == 0) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) sc[h][t] = d[h];
+    }
+  }
+  __syncthreads();
+
+  for (int h = wave; h < G; h += 4) {
+    float m = -INFINITY;
+    for (int t = lane; t < nk; t += 64) m = fmaxf(m, sc[h][t]);
+    m = wave_max(m);
+    float l = 0.f;
+    for (int t = lane; t < nk; t += 64) {
+      const float e = exp2f(sc[h][t] - m);
+      sc[h][t] = e;
+      l += e;
+    }
+    l = wave_sum(l);
+    if (lane == 0) {
+      ml[h][0] = m;
+      ml[h][1] = l;
+    }
+  }
+  __syncthreads();
+
+  float acc[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[h][i] = 0.f;
+  for (int t = kslot; t < nk; t += KPP) {
+    float vf[8];
+    bf16x8(*reinterpret_cast<const v4u*>(vb + (int64_t)t * HD + d0), vf);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float pt = sc[h][t];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[h][i] += pt * vf[i];
+    }
+  }
+#pragma unroll
+  for (int o = LPK; o < 64; o <<= 1) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[h][i] += __shfl_xor(acc[h][i], o);
+  }
+  if (lane < LPK) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) red[wave][h][d0 + i] = acc[h][i];
+  }
+  __syncthreads();
+
+  for (int e = tid; e < G * HD; e += 256) {
+    const int h = e / HD, d = e % HD;
+    const float v = (red[0][h][d] + red[1][h][d]) + (red[2][h][d] + red[3][h][d]);
+    p.part_acc[(((int64_t)b * p.nq + hq0 + h) * p.max_split + split) * HD + d] = v;
+  }
+  if (tid < G) {
+    float* dst = p.part_ml + (((int64_t)b * p.nq + hq0 + tid) * p.max_split + split) * 2;
+    dst[0] = ml[tid][0];
+    dst[1] = ml[tid][1];
+  }
+
+  // The last workgroup of (b, g) to finish merges the splits.
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) is_last = (atomicAdd(&p.counters[b * p.nkv + g], 1) == p.n_split - 1);
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+
+  const int ns = p.n_split;
+  for (int h = wave; h < G; h += 4) {
+    const float* mlh = p.part_ml + ((int64_t)b * p.nq + hq0 + h) * p.max_split * 2;
+    float M = -INFINITY;
+    for (int s = lane; s < ns; s += 64)
+      if (mlh[2 * s + 1] > 0.f) M = fmaxf(M, mlh[2 * s]);
+    M = wave_max(M);
+    float L = 0.f;
+    for (int s = lane; s < ns; s += 64) {
+      const float l = mlh[2 * s + 1];
+      const float w = l > 0.f ? exp2f(mlh[2 * s] - M) : 0.f;
+      sc[h][s] = w;
+      L += w * l;
+    }
+    L = wave_sum(L);
+    if (lane == 0) ml[h][1] = 1.0f / L;
+  }
+  __syncthreads();
+  for (int e = tid; e < G * HD; e += 256) {
+    const int h = e / HD, d = e % HD;
+    const float* acc_h = p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD + d;
+    float o = 0.f;
+    for (int s = 0; s < ns; ++s) o += sc[h][s] * acc_h[(int64_t)s * HD];
+    p.out[(int64_t)b * p.nq * HD + (hq0 + h) * HD + d] = o * ml[h][1];
+  }
+  if (tid == 0) p.counters[b * p.nkv + g] = 0;
+}
+
+// ------------------------------------------------------------------ small kernels
+__global__ void prep_hidden_kernel(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed,
+                                   int vocab, float* x, int H, int* err_flag) {
+  const int row = blockIdx.x;
+  float* xr = x + (int64_t)row * H;
+  if (tokens) {
+    const int tok = tokens[row];
+    if (tok < 0 || tok >= vocab) {
+      if (threadIdx.x == 0) atomicOr(err_flag, 1);
+      for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = __uint_as_float(0x7fc00000u);
+      return;
+    }
+    const uint16_t* e = embed + (int64_t)tok * H;
+    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = bf16_to_f32(e[k]);
+  } else if (in_bf16) {
+    const uint16_t* s = reinterpret_cast<const uint16_t*>(in) + (int64_t)row * H;
+    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = bf16_to_f32(s[k]);
+  } else {
+    const float* s = reinterpret_cast<const float*>(in) + (int64_t)row * H;
+    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = s[k];
+  }
+}
+
+__global__ void argmax_final_kernel(const float* part_val, const int* part_idx, int n_wg, int32_t* token,
+                                    float* max_logit) {
+  const int b = blockIdx.x, tid = threadIdx.x;
+  float best = -INFINITY;
+  int bidx = 0x7fffffff;
+  for (int i = tid; i < n_wg; i += blockDim.x) {
+    const float v = part_val[(int64_t)b * n_wg + i];
+    const int ix = part_idx[(int64_t)b * n_wg + i];
+    if (v > best || (v == best && ix < bidx)) {
+      best = v;
+      bidx = ix;
+    }
+  }
+  __shared__ float sv[256];
+  __shared__ int si[256];
+  sv[tid] = best;
+  si[tid] = bidx;
+  __syncthreads();
+  for (int o = 128; o >= 1; o >>= 1) {
+    if (tid < o) {
+      const float v = sv[tid + o];
+      const int ix = si[tid + o];
+      if (v > sv[tid] || (v == sv[tid] && ix < si[tid])) {
+        sv[tid] = v;
+        si[tid] = ix;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    token[b] = si[0];
+    if (max_logit) max_logit[b] = sv[0];
+  }
+}
+
+__global__ void store_hidden_kernel(const float* x, void* out, int out_bf16, int64_t n) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  if (out_bf16) reinterpret_cast<uint16_t*>(out)[i] = f32_to_bf16(x[i]);
+  else reinterpret_cast<float*>(out)[i] = x[i];
+}
+
+// src [n][nkv][hd] -> dst [kv_head][max_ctx][hd] (dst already offset to the first position)
+__global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const void* sk, const void* sv, int src_bf16, int n,
+                                int nkv, int hd, int max_ctx) {
+  const int64_t total = (int64_t)n * nkv * hd;
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int d = (int)(i % hd);
+  const int g = (int)((i / hd) % nkv);
+  const int t = (int)(i / ((int64_t)hd * nkv));
+  const int64_t at = ((int64_t)g * max_ctx + t) * hd + d;
+  if (src_bf16) {
+    dk[at] = reinterpret_cast<const uint16_t*>(sk)[i];
+    dv[at] = reinterpret_cast<const uint16_t*>(sv)[i];
+  } else {
+    dk[at] = f32_to_bf16(reinterpret_cast<const float*>(sk)[i]);
+    dv[at] = f32_to_bf16(reinterpret_cast<const float*>(sv)[i]);
+  }
+}
+
+__global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, uint16_t* dk, uint16_t* dv, int n, int nkv,
+                               int hd, int max_ctx) {
+  const int64_t total = (int64_t)n * nkv * hd;
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int d = (int)(i % hd);
+  const int g = (int)((i / hd) % nkv);
+  const int t = (int)(i / ((int64_t)hd * nkv));
+  const int64_t at = ((int64_t)g * max_ctx + t) * hd + d;
+  dk[i] = sk[at];
+  dv[i] = sv[at];
+}
+
+// ------------------------------------------------------------------ launchers
+template <int B, int R>
+static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
+  if (epi == kEpiQKV && norm) hipLaunchKernelGGL((gemv_kernel<B, R, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiResid && !norm)
+    hipLaunchKernelGGL((gemv_kernel<B, R, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiSwiGLU && norm)
+    hipLaunchKernelGGL((gemv_kernel<B, R, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiLMHead && norm)
+    hipLaunchKernelGGL((gemv_kernel<B, R, kEpiLMHead, true>), dim3(grid), dim3(256), 0, s, p);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+static int gemv_grid(int epi, int R, const GemvParams& p) {
+  switch (epi) {
+    case kEpiQKV: return (p.nq + 2 * p.nkv) * (p.hd / R);
+    case kEpiSwiGLU: return p.N / (R / 2);
+    default: return (p.N + R - 1) / R;
+  }
+}
+
+hipError_t launch_gemv(int epi, int rows_per_wg, bool norm, const GemvParams& p, hipStream_t s) {
+  if (rows_per_wg != 8) return hipErrorInvalidValue;
+  const int grid = gemv_grid(epi, 8, p);
+  switch (p.batch) {
+    case 1: return gemv_dispatch_epi<1, 8>(epi, norm, p, grid, s);
+    case 2: return gemv_dispatch_epi<2, 8>(epi, norm, p, grid, s);
+    case 3: return gemv_dispatch_epi<3, 8>(epi, norm, p, grid, s);
+    case 4: return gemv_dispatch_epi<4, 8>(epi, norm, p, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int HD>
+static hipError_t attn_dispatch_g(const AttnParams& p, dim3 grid, hipStream_t s) {
+  switch (p.nq / p.nkv) {
+    case 1: hipLaunchKernelGGL((attn_decode_kernel<HD, 1>), grid, dim3(256), 0, s, p); break;
+    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, 2>), grid, dim3(256), 0, s, p); break;
+    case 3: hipLaunchKernelGGL((attn_decode_kernel<HD, 3>), grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, 4>), grid, dim3(256), 0, s, p); break;
+    case 5: hipLaunchKernelGGL((attn_decode_kernel<HD, 5>), grid, dim3(256), 0, s, p); break;
+    case 6: hipLaunchKernelGGL((attn_decode_kernel<HD, 6>), grid, dim3(256), 0, s, p); break;
+    case 7: hipLaunchKernelGGL((attn_decode_kernel<HD, 7>), grid, dim3(256), 0, s, p); break;
+    case 8: hipLaunchKernelGGL((attn_decode_kernel<HD, 8>), grid, dim3(256), 0, s, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s) {
+  const dim3 grid(p.n_split, p.nkv, batch);
+  if (p.hd == 128) return attn_dispatch_g<128>(p, grid, s);
+  if (p.hd == 64) return attn_dispatch_g<64>(p, grid, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
+                              float* x, int rows, int H, int* err_flag, hipStream_t s) {
+  hipLaunchKernelGGL(prep_hidden_kernel, dim3(rows), dim3(256), 0, s, in, in_bf16, tokens, embed, vocab, x, H,
+                     err_flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
+                               float* max_logit, hipStream_t s) {
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(rows), dim3(256), 0, s, part_val, part_idx, n_wg, token, max_logit);
+  return hipGetLastError();
+}
+
+hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t n, hipStream_t s) {
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(store_hidden_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, out, out_bf16, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_bf16,
+                           int n, int nkv, int hd, int max_ctx, hipStream_t s) {
+  const int64_t total = (int64_t)n * nkv * hd;
+  hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, dst_k, dst_v, src_k,
+                     src_v, src_bf16, n, nkv, hd, max_ctx);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k, uint16_t* dst_v, int n,
+                          int nkv, int hd, int max_ctx, hipStream_t s) {
+  const int64_t total = (int64_t)n * nkv * hd;
+  hipLaunchKernelGGL(kv_read_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, src_k, src_v, dst_k,
+                     dst_v, n, nkv, hd, max_ctx);
+  return hipGetLastError();
+}
+
+}  // namespace kf

@@ -1,0 +1,90 @@
+// Internal interface between the stage runtime (stage.hip) and the gfx950 kernels.
+// Nothing here is exported from the shared library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kf {
+
+constexpr int kMaxBatch = 4;
+constexpr int kMaxGroup = 8;     // query heads per KV head
+constexpr int kAttnMinSplit = 64;   // keys per split-KV workgroup, lower bound
+constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound (LDS score buffer)
+
+enum GemvEpi : int {
+  kEpiQKV = 0,     // RoPE on q and k, q -> fp32 workspace, k and v -> bf16 cache at the row's position
+  kEpiResid = 1,   // x[b][row] += y (fp32 residual stream), optional copy to the hidden output
+  kEpiSwiGLU = 2,  // a[b][j] = silu(gate_j) * up_j
+  kEpiLMHead = 3,  // optional fp32 logits, per-workgroup (max, lowest index) partials
+};
+
+// One decode GEMV launch: y[b][n] = sum_k W[n][k] * in[b][k] (* gain[k] * rsqrt(mean(in^2)+eps) if norm).
+struct GemvParams {
+  const uint16_t* w0;  // matrix rows (QKV: [q;k;v] rows; SwiGLU: gate; others: the matrix)
+  const uint16_t* w1;  // SwiGLU: up rows; unused otherwise
+  const uint16_t* gain;  // RMSNorm gain [K] when the launch normalises its input
+  const float* in;     // [B][K] fp32
+  int K;               // reduction length (multiple of 8)
+  int N;               // output rows (logical)
+  float eps;
+  int batch;
+
+  // kEpiResid
+  float* x;            // [B][N] residual stream, updated in place
+  void* out2;          // optional [B][N] copy of the updated rows (hidden output), dtype out2_bf16
+  int out2_bf16;
+
+  // kEpiQKV
+  float* q;            // [B][nq*hd]
+  uint16_t* kc;        // K cache of this layer: [user][kv_head][pos][hd]
+  uint16_t* vc;
+  int64_t user_stride; // elements between users in kc / vc
+  int max_ctx;
+  int nq, nkv, hd;
+  const float* rope_cos;  // [max_ctx][hd/2]
+  const float* rope_sin;
+  int users[kMaxBatch];
+  int pos[kMaxBatch];
+
+  // kEpiSwiGLU
+  float* act;          // [B][N] with N = F
+
+  // kEpiLMHead
+  float* logits;       // optional [B][N]
+  float* part_val;     // [B][n_wg]
+  int* part_idx;       // [B][n_wg]
+  int n_wg;
+};
+
+struct AttnParams {
+  const float* q;      // [B][nq*hd] rotated queries
+  const uint16_t* kc;  // layer base, [user][kv_head][pos][hd]
+  const uint16_t* vc;
+  float* out;          // [B][nq*hd]
+  float* part_acc;     // [B][nq][max_split][hd]
+  float* part_ml;      // [B][nq][max_split][2]
+  int* counters;       // [B][nkv], zero between launches
+  int64_t user_stride;
+  int max_ctx, nq, nkv, hd;
+  int split;           // keys per workgroup
+  int n_split;         // workgroups per (row, kv head)
+  int max_split;       // allocated split capacity
+  float scale_log2;    // log2(e) / sqrt(hd)
+  int users[kMaxBatch];
+  int len[kMaxBatch];  // keys visible to row b: position + 1
+};
+
+// Launchers (return hipGetLastError() of the launch).
+hipError_t launch_gemv(int epi, int rows_per_wg, bool norm, const GemvParams& p, hipStream_t s);
+hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
+hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
+                              float* x, int rows, int H, int* err_flag, hipStream_t s);
+hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
+                               float* max_logit, hipStream_t s);
+hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t n, hipStream_t s);
+hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_bf16,
+                           int n, int nkv, int hd, int max_ctx, hipStream_t s);
+hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k, uint16_t* dst_v, int n,
+                          int nkv, int hd, int max_ctx, hipStream_t s);
+
+}  // namespace kf

@@ -1,0 +1,49 @@
+// Internal interface of the chunked-prefill path (matrix cores).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kf {
+
+struct PrefillArgs {
+  int H, nq, nkv, hd, F;
+  float eps;
+  int T;          // tokens in the chunk
+  int pos0;       // position of the first token
+  int max_ctx;
+  int64_t user_stride;
+  const float* rope_cos;  // [max_ctx][hd/2]
+  const float* rope_sin;
+  hipStream_t stream;
+};
+
+struct PrefillLayer {
+  const uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
+  uint16_t* kc;  // K cache of this layer and user: [kv_head][pos][hd]
+  uint16_t* vc;
+  void* out;     // hidden output after this layer (last layer only), else NULL
+  int out_bf16;
+};
+
+// Device workspace, grown on demand to the largest chunk seen.
+struct PrefillWorkspace {
+  int cap_T = 0;
+  char* mem = nullptr;
+  float* x = nullptr;      // [T][H] residual stream
+  uint16_t* xn = nullptr;  // [T][H] normalised, bf16
+  float* qkv = nullptr;    // [T][(nq+2nkv) hd] raw projections
+  uint16_t* q = nullptr;   // [T][nq][hd] rotated queries, bf16
+  uint16_t* o = nullptr;   // [T][nq hd] attention output, bf16
+  uint16_t* act = nullptr; // [T][F] SwiGLU output, bf16
+};
+
+hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a);
+void prefill_free(PrefillWorkspace& ws);
+hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l);
+
+// Exposed for unit tests of the matrix-core GEMM through the library.
+enum GemmEpi : int { kGemmStoreF32 = 0, kGemmResidF32 = 1, kGemmSwiGLU = 2 };
+hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
+                       float* C, uint16_t* Cb, hipStream_t s);
+
+}  // namespace kf

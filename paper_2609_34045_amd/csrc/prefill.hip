@@ -1,0 +1,497 @@
+// Chunked-prefill kernels for gfx950: a chunk of T tokens of one user.
+//
+// With T in the hundreds the projections are dense contractions,
+// [T, K] x [N, K]^T, and run on the matrix cores (v_mfma_f32_32x32x16_bf16:
+// bf16 operands, fp32 accumulation).  Both operands are K-contiguous in HBM
+// (activations row-major, weights [out, in]), so every MFMA operand fragment
+// is one 16-byte run of a row.  Attention is causal flash attention over the
+// cache [0, pos0) plus the chunk, also on the matrix cores.
+//
+// Operand fragment layout of v_mfma_f32_32x32x16_bf16 (lane l of 64):
+//   A: row l%32, k = 8*(l/32) .. +7      B: column l%32, k = 8*(l/32) .. +7
+//   D: element v (0..15) at row 8*(v/4) + 4*(l/32) + v%4, column l%32
+#include <cmath>
+
+#include "kernels.h"
+#include "prefill.h"
+
+namespace kf {
+
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float from_bf16(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+__device__ __forceinline__ bf16x8 as_bf16x8(v4u v) {
+  bf16x8 r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+__device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+// ------------------------------------------------------------------ GEMM
+// Workgroup tile 128 x 128 x 64, four waves in a 2 x 2 arrangement, each wave
+// 64 x 64 (2 x 2 MFMA blocks).  Global -> registers -> LDS, double-buffered so
+// one barrier per K step separates reading one buffer from refilling the other.
+namespace gemm {
+constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;  // +16 B row pad against LDS bank conflicts
+}
+
+struct GemmParams {
+  const uint16_t* A;   // [M][K]
+  const uint16_t* W;   // [N][K]   (SwiGLU: gate rows)
+  const uint16_t* W2;  // SwiGLU: up rows
+  int M, N, K;         // SwiGLU: N counts gate and up rows together (2F)
+  float* C;            // [M][N] fp32 (store or residual add)
+  uint16_t* Cb;        // SwiGLU: [M][N/2] bf16
+};
+
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
+  using namespace gemm;
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int mt = (p.M + BM - 1) / BM, nt = (p.N + BN - 1) / BN, ntiles = mt * nt;
+  // Tiles that share a weight panel go to the same XCD (workgroups are dealt
+  // round-robin over the 8 XCDs), so the panel is fetched from HBM once per L2.
+  int t = blockIdx.x;
+  if (ntiles % 8 == 0) t = (t % 8) * (ntiles / 8) + t / 8;
+  const int tm = t % mt, tn = t / mt;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int K = p.K;
+
+  // Global load assignment: 4 chunks of 16 B per thread per operand per K step.
+  const v4u* ga[4];
+  const v4u* gw[4];
+  bool oka[4], okw[4];
+  int lrow[4], lcol[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int idx = tid + 256 * i;
+    const int r = idx >> 3, ch = idx & 7;
+    lrow[i] = r;
+    lcol[i] = ch * 8;
+    oka[i] = m0 + r < p.M;
+    ga[i] = reinterpret_cast<const v4u*>(p.A + (int64_t)(oka[i] ? m0 + r : 0) * K + ch * 8);
+    const uint16_t* wbase;
+    int wr;
+    if (EPI == kGemmSwiGLU) {
+      wbase = ((r >> 5) & 1) ? p.W2 : p.W;
+      wr = (n0 >> 1) + (r >> 6) * 32 + (r & 31);
+      okw[i] = wr < (p.N >> 1);
+    } else {
+      wbase = p.W;
+      wr = n0 + r;
+      okw[i] = wr < p.N;
+    }
+    gw[i] = reinterpret_cast<const v4u*>(wbase + (int64_t)(okw[i] ? wr : 0) * K + ch * 8);
+  }
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  v4u ra[4], rw[4];
+  const v4u zero = {0u, 0u, 0u, 0u};
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ra[i] = oka[i] ? ga[i][kt * (BK / 8)] : zero;
+      rw[i] = okw[i] ? __builtin_nontemporal_load(gw[i] + kt * (BK / 8)) : zero;
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<v4u*>(&As[buf][lrow[i] * LDK + lcol[i]]) = ra[i];
+      *reinterpret_cast<v4u*>(&Ws[buf][lrow[i] * LDK + lcol[i]]) = rw[i];
+    }
+  };
+
+  const int nk = K / BK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int arow = wm * 64 + (lane & 31), wrow = wn * 64 + (lane & 31), kof = 8 * (lane >> 5);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload(kt + 1);
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      v4u fa[2], fw[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = *reinterpret_cast<const v4u*>(&As[buf][(arow + 32 * i) * LDK + s * 16 + kof]);
+        fw[i] = *reinterpret_cast<const v4u*>(&Ws[buf][(wrow + 32 * i) * LDK + s * 16 + kof]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(fa[i], fw[j], acc[i][j]);
+    }
+    if (kt + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue.
+  const int col_in = lane & 31, rq = 4 * (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = m0 + wm * 64 + 32 * i + 8 * (v >> 2) + rq + (v & 3);
+      if (row >= p.M) continue;
+      if (EPI == kGemmSwiGLU) {
+        const int j = (n0 >> 1) + wn * 32 + col_in;
+        if (j < (p.N >> 1)) {
+          const float g = acc[i][0][v], u = acc[i][1][v];
+          p.Cb[(int64_t)row * (p.N >> 1) + j] = to_bf16(g / (1.0f + expf(-g)) * u);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int col = n0 + wn * 64 + 32 * j + col_in;
+          if (col >= p.N) continue;
+          float* c = p.C + (int64_t)row * p.N + col;
+          if (EPI == kGemmResidF32) *c += acc[i][j][v];
+          else *c = acc[i][j][v];
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
+                       float* C, uint16_t* Cb, hipStream_t s) {
+  using namespace gemm;
+  if (M <= 0 || N <= 0 || K <= 0 || K % BK) return hipErrorInvalidValue;
+  GemmParams p{A, W, W2, M, N, K, C, Cb};
+  const int grid = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  switch (epi) {
+    case kGemmStoreF32: hipLaunchKernelGGL(gemm_kernel<kGemmStoreF32>, dim3(grid), dim3(256), 0, s, p); break;
+    case kGemmResidF32: hipLaunchKernelGGL(gemm_kernel<kGemmResidF32>, dim3(grid), dim3(256), 0, s, p); break;
+    case kGemmSwiGLU:
+      if (N % 2) return hipErrorInvalidValue;
+      hipLaunchKernelGGL(gemm_kernel<kGemmSwiGLU>, dim3(grid), dim3(256), 0, s, p);
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ row RMSNorm -> bf16
+__global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const float* x, const uint16_t* g, float eps,
+                                                                uint16_t* out, int H) {
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const float* xr = x + (int64_t)row * H;
+  float ss = 0.f;
+  for (int k = tid; k < H; k += 256) ss += xr[k] * xr[k];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  __shared__ float red[4];
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float rs = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)H + eps);
+  uint16_t* o = out + (int64_t)row * H;
+  for (int k = tid; k < H; k += 256) o[k] = to_bf16(xr[k] * rs * from_bf16(g[k]));
+}
+
+// ------------------------------------------------------------------ RoPE + KV append
+// qkv [T][(nq+2nkv) hd] fp32 -> q [T][nq][hd] bf16 (rotated), K/V cache at pos0 + i (bf16).
+__global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, uint16_t* q, uint16_t* kc, uint16_t* vc,
+                                                      const float* cosT, const float* sinT, int nq, int nkv, int hd,
+                                                      int pos0, int max_ctx) {
+  const int i = blockIdx.x, half = hd / 2, pos = pos0 + i;
+  const int nh = nq + 2 * nkv;
+  const float* src = qkv + (int64_t)i * nh * hd;
+  for (int e = threadIdx.x; e < nh * half; e += 256) {
+    const int h = e / half, j = e % half;
+    const float a = src[h * hd + j], b = src[h * hd + j + half];
+    if (h < nq + nkv) {
+      const float c = cosT[(int64_t)pos * half + j], s = sinT[(int64_t)pos * half + j];
+      const float z1 = a * c - b * s, z2 = b * c + a * s;
+      if (h < nq) {
+        uint16_t* dst = q + ((int64_t)i * nq + h) * hd;
+        dst[j] = to_bf16(z1);
+        dst[j + half] = to_bf16(z2);
+      } else {
+        uint16_t* dst = kc + ((int64_t)(h - nq) * max_ctx + pos) * hd;
+        dst[j] = to_bf16(z1);
+        dst[j + half] = to_bf16(z2);
+      }
+    } else {
+      uint16_t* dst = vc + ((int64_t)(h - nq - nkv) * max_ctx + pos) * hd;
+      dst[j] = to_bf16(a);
+      dst[j + half] = to_bf16(b);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ causal flash attention
+// Workgroup = (128 queries, one query head); wave w owns queries 32w .. 32w+31.
+// Per block of 32 keys each wave computes S^T = K Q^T (keys x queries) so that
+// every lane holds one query's column; the online softmax is then per lane, and
+// the lane's probabilities are already a B fragment of O^T += V^T P^T once the
+// MFMA's k index is mapped to the keys the lane holds.  V^T is written to LDS
+// transposed when the block is staged.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
+                                                           const uint16_t* vc, uint16_t* out, int T, int nq, int nkv,
+                                                           int pos0, int max_ctx, float scale_log2) {
+  constexpr int KB = 32;            // keys per block
+  constexpr int LDK = HD + 8;       // K tile row stride (bf16)
+  constexpr int LDV = KB + 4;       // V^T tile row stride (bf16), keeps 8-byte alignment
+  constexpr int DB = HD / 32;       // 32-row d-blocks of O^T
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KB * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = blockIdx.y, g = h / (nq / nkv);
+  const int i0 = blockIdx.x * 128;
+  const int qi = i0 + wave * 32 + (lane & 31);  // this lane's query (chunk index)
+  const int half_sel = lane >> 5;
+  const bool qok = qi < T;
+  const int qpos = pos0 + qi;
+  const int last_q = min(i0 + 127, T - 1);
+  const int nkeys = pos0 + last_q + 1;  // keys visible to the workgroup's last query
+  const int nblk = (nkeys + KB - 1) / KB;
+  const uint16_t* kbase = kc + (int64_t)g * max_ctx * HD;
+  const uint16_t* vbase = vc + (int64_t)g * max_ctx * HD;
+
+  // Q^T fragments: lane holds query qi, d = 16 s + 8 half_sel .. +7.
+  v4u qf[HD / 16];
+  {
+    const uint16_t* qr = q + ((int64_t)(qok ? qi : 0) * nq + h) * HD;
+#pragma unroll
+    for (int s = 0; s < HD / 16; ++s) {
+      v4u v = *reinterpret_cast<const v4u*>(qr + 16 * s + 8 * half_sel);
+      qf[s] = qok ? v : v4u{0u, 0u, 0u, 0u};
+    }
+  }
+
+  f32x16 o[DB];
+#pragma unroll
+  for (int d = 0; d < DB; ++d)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[d][v] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // Staging: 32 keys x HD elements for K and V; a thread moves 16 B of each.
+  // Global loads for the next block are issued before this block's MFMAs and
+  // written to the other LDS buffer after them.
+  constexpr int CH = HD / 8;               // 16-byte chunks per key
+  constexpr int PER = (KB * CH + 255) / 256;
+  v4u rk[PER], rv[PER];
+  auto gload = [&](int blk) {
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int idx = tid + 256 * r;
+      const int key = idx / CH, ch = idx % CH;
+      const int pos = blk * KB + key;
+      rk[r] = v4u{0u, 0u, 0u, 0u};
+      rv[r] = v4u{0u, 0u, 0u, 0u};
+      if (idx < KB * CH && pos < nkeys) {
+        rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)pos * HD + ch * 8);
+        rv[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)pos * HD + ch * 8);
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int idx = tid + 256 * r;
+      if (idx < KB * CH) {
+        const int key = idx / CH, ch = idx % CH;
+        *reinterpret_cast<v4u*>(&Ks[buf][key * LDK + ch * 8]) = rk[r];
+        const uint32_t w[4] = {rv[r].x, rv[r].y, rv[r].z, rv[r].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          Vt[buf][(ch * 8 + 2 * e) * LDV + key] = (uint16_t)(w[e] & 0xffffu);
+          Vt[buf][(ch * 8 + 2 * e + 1) * LDV + key] = (uint16_t)(w[e] >> 16);
+        }
+      }
+    }
+  };
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int blk = 0; blk < nblk; ++blk) {
+    const int buf = blk & 1;
+    if (blk + 1 < nblk) gload(blk + 1);
+
+    // S^T[key][query] for the 32 keys of this block.
+    f32x16 st;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) st[v] = 0.f;
+#pragma unroll
+    for (int s = 0; s < HD / 16; ++s) {
+      const v4u kf = *reinterpret_cast<const v4u*>(&Ks[buf][(lane & 31) * LDK + 16 * s + 8 * half_sel]);
+      st = mfma32(kf, qf[s], st);
+    }
+    // Lane holds keys kk(v) = 8 (v/4) + 4 half_sel + v%4 of its query.
+    float mb = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int key = blk * KB + 8 * (v >> 2) + 4 * half_sel + (v & 3);
+      const float sv = (key <= qpos) ? st[v] * scale_log2 : -INFINITY;
+      st[v] = sv;
+      mb = fmaxf(mb, sv);
+    }
+    mb = fmaxf(mb, __shfl_xor(mb, 32));
+    const float m_new = fmaxf(m_run, mb);
+    const float alpha = exp2f(m_run - m_new);  // 0 on the first block (m_run = -inf, m_new finite)
+    float ls = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float pv = exp2f(st[v] - m_new);
+      st[v] = pv;
+      ls += pv;
+    }
+    ls += __shfl_xor(ls, 32);
+    l_run = l_run * alpha + ls;
+    m_run = m_new;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
+
+    // P^T fragments: step 0 takes v = 0..7, step 1 takes v = 8..15 (the MFMA's
+    // k index runs over the keys this lane holds, in that order).
+    v4u pf[2];
+#pragma unroll
+    for (int sidx = 0; sidx < 2; ++sidx) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)to_bf16(st[8 * sidx + 2 * e]) | ((uint32_t)to_bf16(st[8 * sidx + 2 * e + 1]) << 16);
+      pf[sidx] = v4u{w[0], w[1], w[2], w[3]};
+    }
+    // V^T fragments with the same key order: keys 16 sidx + 4 half_sel + {0..3} and 16 sidx + 8 + 4 half_sel + {0..3}.
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+      const uint16_t* vrow = &Vt[buf][(32 * d + (lane & 31)) * LDV];
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const v2u lo = *reinterpret_cast<const v2u*>(vrow + 16 * sidx + 4 * half_sel);
+        const v2u hi = *reinterpret_cast<const v2u*>(vrow + 16 * sidx + 8 + 4 * half_sel);
+        o[d] = mfma32(v4u{lo.x, lo.y, hi.x, hi.y}, pf[sidx], o[d]);
+      }
+    }
+    if (blk + 1 < nblk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  if (qok) {
+    const float inv = 1.0f / l_run;
+    uint16_t* dst = out + ((int64_t)qi * nq + h) * HD;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = to_bf16(o[d][v] * inv);
+  }
+}
+
+// ------------------------------------------------------------------ final copy
+__global__ void store_rows_kernel(const float* x, void* out, int out_bf16, int64_t n) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  if (out_bf16) reinterpret_cast<uint16_t*>(out)[i] = to_bf16(x[i]);
+  else reinterpret_cast<float*>(out)[i] = x[i];
+}
+
+// ------------------------------------------------------------------ host side
+static int64_t a256(int64_t n) { return (n + 255) & ~(int64_t)255; }
+
+void prefill_free(PrefillWorkspace& ws) {
+  if (ws.mem) hipFree(ws.mem);
+  ws = PrefillWorkspace{};
+}
+
+hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
+  if (a.T <= ws.cap_T && ws.mem) return hipSuccess;
+  const int64_t T = a.T, H = a.H, nqkv = (int64_t)(a.nq + 2 * a.nkv) * a.hd;
+  const int64_t sz_x = a256(T * H * 4), sz_xn = a256(T * H * 2), sz_qkv = a256(T * nqkv * 4),
+                sz_q = a256(T * a.nq * a.hd * 2), sz_o = a256(T * a.nq * a.hd * 2), sz_act = a256(T * a.F * 2);
+  const int64_t total = sz_x + sz_xn + sz_qkv + sz_q + sz_o + sz_act;
+  char* mem = nullptr;
+  // Drain work that may still use the old buffer before freeing it.
+  hipError_t e = hipStreamSynchronize(a.stream);
+  if (e != hipSuccess) return e;
+  e = hipMalloc((void**)&mem, total);
+  if (e != hipSuccess) {
+    hipGetLastError();
+    return hipErrorOutOfMemory;
+  }
+  prefill_free(ws);
+  ws.mem = mem;
+  ws.cap_T = a.T;
+  char* p = mem;
+  ws.x = (float*)p;
+  p += sz_x;
+  ws.xn = (uint16_t*)p;
+  p += sz_xn;
+  ws.qkv = (float*)p;
+  p += sz_qkv;
+  ws.q = (uint16_t*)p;
+  p += sz_q;
+  ws.o = (uint16_t*)p;
+  p += sz_o;
+  ws.act = (uint16_t*)p;
+  return hipSuccess;
+}
+
+hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l) {
+  hipStream_t s = a.stream;
+  const int T = a.T, H = a.H, nqkv = (a.nq + 2 * a.nkv) * a.hd;
+  hipError_t e;
+  hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_attn, a.eps, ws.xn, H);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_gemm(kGemmStoreF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.qkv, nullptr, s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.qkv, ws.q, l.kc, l.vc, a.rope_cos, a.rope_sin, a.nq,
+                     a.nkv, a.hd, a.pos0, a.max_ctx);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));
+  const dim3 ag((T + 127) / 128, a.nq);
+  if (a.hd == 128)
+    hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, T, a.nq, a.nkv, a.pos0,
+                       a.max_ctx, sl2);
+  else if (a.hd == 64)
+    hipLaunchKernelGGL(attn_prefill_kernel<64>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, T, a.nq, a.nkv, a.pos0,
+                       a.max_ctx, sl2);
+  else
+    return hipErrorInvalidValue;
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_gemm(kGemmResidF32, ws.o, l.wo, nullptr, T, H, a.nq * a.hd, ws.x, nullptr, s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_mlp, a.eps, ws.xn, H);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_gemm(kGemmSwiGLU, ws.xn, l.wg, l.wu, T, 2 * a.F, H, nullptr, ws.act, s)) != hipSuccess) return e;
+  if ((e = launch_gemm(kGemmResidF32, ws.act, l.wd, nullptr, T, H, a.F, ws.x, nullptr, s)) != hipSuccess) return e;
+  if (l.out) {
+    const int64_t n = (int64_t)T * H;
+    hipLaunchKernelGGL(store_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, ws.x, l.out, l.out_bf16, n);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace kf

@@ -1,0 +1,712 @@
+// Stage runtime behind the C ABI of include/kafila_stage.h: argument checks,
+// device memory (weights, KV cache, workspaces) and the per-step kernel sequence.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kafila_stage.h"
+#include "kernels.h"
+#include "prefill.h"
+
+using namespace kf;
+
+static thread_local std::string g_err;
+
+static kf_status fail(kf_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define KF_HIP(call, what)                                                                  \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess) return fail(KF_EDEVICE, "%s: %s", (what), hipGetErrorString(e_)); \
+  } while (0)
+
+static int64_t align256(int64_t n) { return (n + 255) & ~(int64_t)255; }
+
+struct LayerW {
+  uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
+};
+
+struct kf_stage {
+  kf_model_config cfg;
+  int lo, hi, has_head;
+  hipStream_t stream;
+  int device;
+  char* arena = nullptr;  // all weights
+  std::vector<LayerW> layers;
+  uint16_t *embed = nullptr, *lm_head = nullptr, *g_final = nullptr;
+  // decode workspace
+  char* ws = nullptr;
+  float *x = nullptr, *q = nullptr, *o = nullptr, *act = nullptr, *hx = nullptr;
+  float* part_val = nullptr;
+  int* part_idx = nullptr;
+  int lm_wg = 0;
+  int* err_flag = nullptr;
+  int live_kv = 0;
+  PrefillWorkspace pf;
+};
+
+struct kf_kv {
+  kf_stage* st;
+  int max_users, max_ctx, max_split;
+  uint16_t *k = nullptr, *v = nullptr;
+  float *rcos = nullptr, *rsin = nullptr;
+  float *part_acc = nullptr, *part_ml = nullptr;
+  int* counters = nullptr;
+  int64_t user_stride, layer_stride;  // elements
+  std::vector<int> len;
+};
+
+// ------------------------------------------------------------------ config checks
+static kf_status check_cfg(const kf_model_config* c, int lo, int hi) {
+  if (!c) return fail(KF_EINVAL, "config is NULL");
+  if (c->n_layers <= 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->ffn <= 0 || c->vocab < 0)
+    return fail(KF_EINVAL, "config sizes must be positive");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) return fail(KF_EINVAL, "rms_eps must be >= 0 and rope_theta > 0");
+  if (!(0 <= lo && lo < hi && hi <= c->n_layers))
+    return fail(KF_EINVAL, "layer range [%d, %d) not inside [0, %d)", lo, hi, c->n_layers);
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(KF_EUNSUPPORTED, "head_dim %d (64 or 128 only)", c->head_dim);
+  if (c->n_q_heads % c->n_kv_heads) return fail(KF_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
+  if (c->n_q_heads / c->n_kv_heads > kMaxGroup)
+    return fail(KF_EUNSUPPORTED, "more than %d query heads per KV head", kMaxGroup);
+  if (c->hidden % 64 || c->ffn % 64) return fail(KF_EUNSUPPORTED, "hidden and ffn must be multiples of 64");
+  return KF_OK;
+}
+
+static int64_t tensor_numel(const kf_model_config& c, int kind) {
+  const int64_t H = c.hidden, hd = c.head_dim, F = c.ffn, V = c.vocab;
+  switch (kind) {
+    case KF_W_ATTN_NORM: case KF_W_MLP_NORM: case KF_W_FINAL_NORM: return H;
+    case KF_W_Q: return c.n_q_heads * hd * H;
+    case KF_W_K: case KF_W_V: return c.n_kv_heads * hd * H;
+    case KF_W_O: return H * c.n_q_heads * hd;
+    case KF_W_GATE: case KF_W_UP: case KF_W_DOWN: return F * H;
+    case KF_W_EMBED: case KF_W_LM_HEAD: return V * H;
+    default: return -1;
+  }
+}
+
+static int64_t block_bytes(const kf_model_config& c) {
+  int64_t n = 0;
+  for (int k = KF_W_ATTN_NORM; k <= KF_W_DOWN; ++k) n += tensor_numel(c, k);
+  return 2 * n;
+}
+
+static int64_t head_bytes(const kf_model_config& c) {
+  return 2 * (tensor_numel(c, KF_W_EMBED) + tensor_numel(c, KF_W_LM_HEAD) + tensor_numel(c, KF_W_FINAL_NORM));
+}
+
+static int max_split_for(int max_ctx) {
+  int ms = (max_ctx + kAttnMinSplit - 1) / kAttnMinSplit;
+  return ms > 1024 ? 1024 : ms;
+}
+
+static int64_t kv_bytes(const kf_model_config& c, int layers, int max_users, int max_ctx) {
+  const int64_t cache = 2LL * layers * max_users * c.n_kv_heads * (int64_t)max_ctx * c.head_dim * 2;
+  const int64_t rope = 2LL * max_ctx * (c.head_dim / 2) * 4;
+  const int64_t ms = max_split_for(max_ctx);
+  const int64_t part = (int64_t)kMaxBatch * c.n_q_heads * ms * (c.head_dim + 2) * 4;
+  return align256(cache / 2) * 2 + align256(rope / 2) * 2 + align256(part) + 256;
+}
+
+static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
+  const int64_t H = c.hidden, B = kMaxBatch;
+  int64_t n = 0;
+  n += align256(B * H * 4);                           // x
+  n += align256(B * c.n_q_heads * c.head_dim * 4);    // q
+  n += align256(B * c.n_q_heads * c.head_dim * 4);    // o
+  n += align256(B * (int64_t)c.ffn * 4);              // act
+  n += align256(B * H * 4);                           // hx
+  if (has_head) {
+    const int64_t wgs = (c.vocab + 7) / 8;
+    n += 2 * align256(B * wgs * 4);
+  }
+  n += 256;  // error flag
+  return n;
+}
+
+extern "C" {
+
+int32_t kf_abi_version(void) { return KF_ABI_VERSION; }
+
+const char* kf_last_error(void) { return g_err.c_str(); }
+
+kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t lo, int32_t hi, int32_t has_head, int32_t max_users,
+                         int32_t max_ctx, int64_t* beta_block, int64_t* beta_head, int64_t* resident) {
+  kf_status st = check_cfg(cfg, lo, hi);
+  if (st != KF_OK && st != KF_EUNSUPPORTED) return st;
+  if (max_users < 0 || max_ctx < 0) return fail(KF_EINVAL, "max_users and max_ctx must be >= 0");
+  const int64_t bb = block_bytes(*cfg), hb = has_head ? head_bytes(*cfg) : 0;
+  if (beta_block) *beta_block = bb;
+  if (beta_head) *beta_head = hb;
+  if (resident)
+    *resident = (int64_t)(hi - lo) * bb + hb + decode_ws_bytes(*cfg, has_head) +
+                (max_users > 0 && max_ctx > 0 ? kv_bytes(*cfg, hi - lo, max_users, max_ctx) : 0);
+  return KF_OK;
+}
+
+kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int32_t has_head,
+                        const kf_weights* weights, void* hip_stream, kf_stage** out) {
+  if (!out) return fail(KF_EINVAL, "out is NULL");
+  *out = nullptr;
+  kf_status st = check_cfg(cfg, lo, hi);
+  if (st != KF_OK) return st;
+  if (has_head && cfg->vocab <= 0) return fail(KF_EINVAL, "a head stage needs vocab > 0");
+  if (!weights || (weights->count > 0 && !weights->tensors)) return fail(KF_EINVAL, "weights is NULL");
+
+  const int nl = hi - lo;
+  // Locate every tensor exactly once.
+  std::vector<const kf_tensor*> slot((size_t)nl * 9, nullptr);
+  const kf_tensor* hslot[3] = {nullptr, nullptr, nullptr};
+  for (int i = 0; i < weights->count; ++i) {
+    const kf_tensor& t = weights->tensors[i];
+    if (t.kind < KF_W_ATTN_NORM || t.kind > KF_W_LM_HEAD) return fail(KF_EINVAL, "tensor %d: unknown kind %d", i, t.kind);
+    if (!t.bf16) return fail(KF_EINVAL, "tensor %d: NULL data", i);
+    if (t.numel != tensor_numel(*cfg, t.kind))
+      return fail(KF_EINVAL, "tensor %d (layer %d kind %d): numel %lld, expected %lld", i, t.layer, t.kind,
+                  (long long)t.numel, (long long)tensor_numel(*cfg, t.kind));
+    const kf_tensor** dst;
+    if (t.kind >= KF_W_EMBED) {
+      if (!has_head) return fail(KF_EINVAL, "tensor %d: head tensor given to a stage without the head", i);
+      if (t.layer != -1) return fail(KF_EINVAL, "tensor %d: head tensors take layer -1", i);
+      dst = &hslot[t.kind - KF_W_EMBED];
+    } else {
+      if (t.layer < lo || t.layer >= hi) return fail(KF_EINVAL, "tensor %d: layer %d outside [%d, %d)", i, t.layer, lo, hi);
+      dst = &slot[(size_t)(t.layer - lo) * 9 + t.kind];
+    }
+    if (*dst) return fail(KF_EINVAL, "tensor %d (layer %d kind %d) given twice", i, t.layer, t.kind);
+    *dst = &t;
+  }
+  for (int l = 0; l < nl; ++l)
+    for (int k = 0; k < 9; ++k)
+      if (!slot[(size_t)l * 9 + k]) return fail(KF_EINVAL, "missing tensor: layer %d kind %d", lo + l, k);
+  if (has_head)
+    for (int k = 0; k < 3; ++k)
+      if (!hslot[k]) return fail(KF_EINVAL, "missing head tensor kind %d", KF_W_EMBED + k);
+
+  kf_stage* s = new (std::nothrow) kf_stage();
+  if (!s) return fail(KF_ENOMEM, "host allocation");
+  s->cfg = *cfg;
+  s->lo = lo;
+  s->hi = hi;
+  s->has_head = has_head ? 1 : 0;
+  s->stream = (hipStream_t)hip_stream;
+  if (hipGetDevice(&s->device) != hipSuccess) {
+    delete s;
+    return fail(KF_EDEVICE, "no HIP device");
+  }
+
+  const kf_model_config& c = *cfg;
+  const int64_t H = c.hidden, hd = c.head_dim, F = c.ffn;
+  const int64_t nqkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * hd;
+  // Per-layer arena: wqkv | wo | wg | wu | wd | g_attn | g_mlp, each 256-byte aligned.
+  const int64_t off_qkv = 0, off_o = align256(off_qkv + nqkv * H * 2), off_g = align256(off_o + H * c.n_q_heads * hd * 2),
+                off_u = align256(off_g + F * H * 2), off_d = align256(off_u + F * H * 2),
+                off_na = align256(off_d + H * F * 2), off_nm = align256(off_na + H * 2), lsz = align256(off_nm + H * 2);
+  const int64_t V = c.vocab;
+  const int64_t off_e = lsz * nl, off_lm = align256(off_e + (has_head ? V * H * 2 : 0)),
+                off_gf = align256(off_lm + (has_head ? V * H * 2 : 0)), total = align256(off_gf + H * 2);
+
+  auto cleanup = [&](kf_status code) {
+    if (s->arena) hipFree(s->arena);
+    if (s->ws) hipFree(s->ws);
+    delete s;
+    return code;
+  };
+  if (hipMalloc((void**)&s->arena, total) != hipSuccess) {
+    hipGetLastError();
+    s->arena = nullptr;
+    return cleanup(fail(KF_ENOMEM, "device allocation of %lld weight bytes", (long long)total));
+  }
+  auto up = [&](char* dst, const kf_tensor* t) {
+    return hipMemcpy(dst, t->bf16, (size_t)t->numel * 2, hipMemcpyHostToDevice);
+  };
+  s->layers.resize(nl);
+  for (int l = 0; l < nl; ++l) {
+    char* base = s->arena + lsz * l;
+    const kf_tensor** w = &slot[(size_t)l * 9];
+    LayerW& L = s->layers[l];
+    L.wqkv = (uint16_t*)(base + off_qkv);
+    L.wo = (uint16_t*)(base + off_o);
+    L.wg = (uint16_t*)(base + off_g);
+    L.wu = (uint16_t*)(base + off_u);
+    L.wd = (uint16_t*)(base + off_d);
+    L.g_attn = (uint16_t*)(base + off_na);
+    L.g_mlp = (uint16_t*)(base + off_nm);
+    const int64_t qb = (int64_t)c.n_q_heads * hd * H * 2, kb = (int64_t)c.n_kv_heads * hd * H * 2;
+    hipError_t e = hipSuccess;
+    if (e == hipSuccess) e = up(base + off_qkv, w[KF_W_Q]);
+    if (e == hipSuccess) e = up(base + off_qkv + qb, w[KF_W_K]);
+    if (e == hipSuccess) e = up(base + off_qkv + qb + kb, w[KF_W_V]);
+    if (e == hipSuccess) e = up(base + off_o, w[KF_W_O]);
+    if (e == hipSuccess) e = up(base + off_g, w[KF_W_GATE]);
+    if (e == hipSuccess) e = up(base + off_u, w[KF_W_UP]);
+    if (e == hipSuccess) e = up(base + off_d, w[KF_W_DOWN]);
+    if (e == hipSuccess) e = up(base + off_na, w[KF_W_ATTN_NORM]);
+    if (e == hipSuccess) e = up(base + off_nm, w[KF_W_MLP_NORM]);
+    if (e != hipSuccess) return cleanup(fail(KF_EDEVICE, "weight upload: %s", hipGetErrorString(e)));
+  }
+  if (has_head) {
+    s->embed = (uint16_t*)(s->arena + off_e);
+    s->lm_head = (uint16_t*)(s->arena + off_lm);
+    s->g_final = (uint16_t*)(s->arena + off_gf);
+    hipError_t e = up((char*)s->embed, hslot[0]);
+    if (e == hipSuccess) e = up((char*)s->g_final, hslot[1]);
+    if (e == hipSuccess) e = up((char*)s->lm_head, hslot[2]);
+    if (e != hipSuccess) return cleanup(fail(KF_EDEVICE, "head upload: %s", hipGetErrorString(e)));
+  }
+
+  const int64_t wsz = decode_ws_bytes(c, s->has_head);
+  if (hipMalloc((void**)&s->ws, wsz) != hipSuccess) {
+    hipGetLastError();
+    s->ws = nullptr;
+    return cleanup(fail(KF_ENOMEM, "device allocation of the decode workspace"));
+  }
+  if (hipMemset(s->ws, 0, wsz) != hipSuccess) return cleanup(fail(KF_EDEVICE, "workspace clear"));
+  char* p = s->ws;
+  auto take = [&](int64_t bytes) {
+    char* r = p;
+    p += align256(bytes);
+    return r;
+  };
+  const int64_t B = kMaxBatch;
+  s->x = (float*)take(B * H * 4);
+  s->q = (float*)take(B * c.n_q_heads * hd * 4);
+  s->o = (float*)take(B * c.n_q_heads * hd * 4);
+  s->act = (float*)take(B * F * 4);
+  s->hx = (float*)take(B * H * 4);
+  if (has_head) {
+    s->lm_wg = (int)((V + 7) / 8);
+    s->part_val = (float*)take(B * s->lm_wg * 4);
+    s->part_idx = (int*)take(B * s->lm_wg * 4);
+  }
+  s->err_flag = (int*)take(4);
+  *out = s;
+  g_err.clear();
+  return KF_OK;
+}
+
+kf_status kf_stage_destroy(kf_stage* s) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  if (s->live_kv) return fail(KF_ESTATE, "%d KV cache(s) of this stage still exist", s->live_kv);
+  hipStreamSynchronize(s->stream);
+  if (s->arena) hipFree(s->arena);
+  if (s->ws) hipFree(s->ws);
+  prefill_free(s->pf);
+  delete s;
+  return KF_OK;
+}
+
+kf_status kf_stage_set_stream(kf_stage* s, void* hip_stream) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  s->stream = (hipStream_t)hip_stream;
+  return KF_OK;
+}
+
+kf_status kf_stage_sync(kf_stage* s) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  KF_HIP(hipStreamSynchronize(s->stream), "stream synchronize");
+  KF_HIP(hipGetLastError(), "earlier enqueued work");
+  int flag = 0;
+  KF_HIP(hipMemcpy(&flag, s->err_flag, 4, hipMemcpyDeviceToHost), "error flag read");
+  if (flag) {
+    int zero = 0;
+    KF_HIP(hipMemcpy(s->err_flag, &zero, 4, hipMemcpyHostToDevice), "error flag clear");
+    return fail(KF_EINVAL, "a token id was outside [0, vocab); its hidden row was set to NaN");
+  }
+  return KF_OK;
+}
+
+// ------------------------------------------------------------------ KV cache
+kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** out) {
+  if (!out) return fail(KF_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  if (max_users <= 0 || max_ctx <= 0) return fail(KF_EINVAL, "max_users and max_ctx must be positive");
+  if ((int64_t)max_ctx > (int64_t)kAttnMaxSplit * 1024) return fail(KF_ERANGE, "max_ctx above %d", kAttnMaxSplit * 1024);
+  const kf_model_config& c = s->cfg;
+  const int nl = s->hi - s->lo;
+  kf_kv* kv = new (std::nothrow) kf_kv();
+  if (!kv) return fail(KF_ENOMEM, "host allocation");
+  kv->st = s;
+  kv->max_users = max_users;
+  kv->max_ctx = max_ctx;
+  kv->max_split = max_split_for(max_ctx);
+  kv->user_stride = (int64_t)c.n_kv_heads * max_ctx * c.head_dim;
+  kv->layer_stride = kv->user_stride * max_users;
+  kv->len.assign(max_users, 0);
+  const int64_t cache = kv->layer_stride * nl * 2;
+  const int64_t half = c.head_dim / 2;
+  const int64_t rope = (int64_t)max_ctx * half * 4;
+  const int64_t pacc = (int64_t)kMaxBatch * c.n_q_heads * kv->max_split * c.head_dim * 4;
+  const int64_t pml = (int64_t)kMaxBatch * c.n_q_heads * kv->max_split * 2 * 4;
+  const int64_t cnt = (int64_t)kMaxBatch * c.n_kv_heads * 4;
+  char* mem[7] = {nullptr};
+  const int64_t sz[7] = {cache, cache, rope, rope, pacc, pml, cnt};
+  for (int i = 0; i < 7; ++i) {
+    if (hipMalloc((void**)&mem[i], sz[i]) != hipSuccess) {
+      hipGetLastError();
+      for (int j = 0; j < i; ++j) hipFree(mem[j]);
+      delete kv;
+      return fail(KF_ENOMEM, "device allocation of %lld KV bytes", (long long)sz[i]);
+    }
+  }
+  kv->k = (uint16_t*)mem[0];
+  kv->v = (uint16_t*)mem[1];
+  kv->rcos = (float*)mem[2];
+  kv->rsin = (float*)mem[3];
+  kv->part_acc = (float*)mem[4];
+  kv->part_ml = (float*)mem[5];
+  kv->counters = (int*)mem[6];
+  // RoPE table from float64 angles: pos * theta^(-2i/hd).
+  std::vector<float> tc((size_t)max_ctx * half), ts((size_t)max_ctx * half);
+  for (int64_t i = 0; i < half; ++i) {
+    const double w = std::pow((double)c.rope_theta, -2.0 * (double)i / (double)c.head_dim);
+    for (int64_t p = 0; p < max_ctx; ++p) {
+      const double a = (double)p * w;
+      tc[p * half + i] = (float)std::cos(a);
+      ts[p * half + i] = (float)std::sin(a);
+    }
+  }
+  hipError_t e = hipMemset(kv->k, 0, cache);
+  if (e == hipSuccess) e = hipMemset(kv->v, 0, cache);
+  if (e == hipSuccess) e = hipMemset(kv->counters, 0, cnt);
+  if (e == hipSuccess) e = hipMemcpy(kv->rcos, tc.data(), rope, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(kv->rsin, ts.data(), rope, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    for (int j = 0; j < 7; ++j) hipFree(mem[j]);
+    delete kv;
+    return fail(KF_EDEVICE, "KV init: %s", hipGetErrorString(e));
+  }
+  s->live_kv++;
+  *out = kv;
+  return KF_OK;
+}
+
+kf_status kf_kv_destroy(kf_kv* kv) {
+  if (!kv) return fail(KF_EINVAL, "kv is NULL");
+  hipStreamSynchronize(kv->st->stream);
+  void* mem[7] = {kv->k, kv->v, kv->rcos, kv->rsin, kv->part_acc, kv->part_ml, kv->counters};
+  for (void* m : mem) hipFree(m);
+  kv->st->live_kv--;
+  delete kv;
+  return KF_OK;
+}
+
+kf_status kf_kv_len(const kf_kv* kv, int32_t user, int32_t* len) {
+  if (!kv || !len) return fail(KF_EINVAL, "NULL argument");
+  if (user < 0 || user >= kv->max_users) return fail(KF_EINVAL, "user %d outside [0, %d)", user, kv->max_users);
+  *len = kv->len[user];
+  return KF_OK;
+}
+
+kf_status kf_kv_set_len(kf_kv* kv, int32_t user, int32_t len) {
+  if (!kv) return fail(KF_EINVAL, "kv is NULL");
+  if (user < 0 || user >= kv->max_users) return fail(KF_EINVAL, "user %d outside [0, %d)", user, kv->max_users);
+  if (len < 0 || len > kv->max_ctx) return fail(KF_ERANGE, "length %d outside [0, %d]", len, kv->max_ctx);
+  kv->len[user] = len;
+  return KF_OK;
+}
+
+static kf_status kv_slice_check(const kf_kv* kv, int layer, int user, int pos0, int n) {
+  const kf_stage* s = kv->st;
+  if (layer < s->lo || layer >= s->hi) return fail(KF_EINVAL, "layer %d not held by the stage [%d, %d)", layer, s->lo, s->hi);
+  if (user < 0 || user >= kv->max_users) return fail(KF_EINVAL, "user %d outside [0, %d)", user, kv->max_users);
+  if (pos0 < 0 || n < 0) return fail(KF_EINVAL, "negative position or count");
+  if ((int64_t)pos0 + n > kv->max_ctx) return fail(KF_ERANGE, "positions [%d, %d) beyond max_ctx %d", pos0, pos0 + n, kv->max_ctx);
+  return KF_OK;
+}
+
+kf_status kf_kv_write(kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, const void* k_dev,
+                      const void* v_dev, kf_dtype dtype) {
+  if (!kv) return fail(KF_EINVAL, "kv is NULL");
+  kf_status st = kv_slice_check(kv, layer, user, pos0, n);
+  if (st != KF_OK) return st;
+  if (n == 0) return KF_OK;
+  if (!k_dev || !v_dev) return fail(KF_EINVAL, "NULL source");
+  if (dtype != KF_F32 && dtype != KF_BF16) return fail(KF_EINVAL, "dtype");
+  const kf_model_config& c = kv->st->cfg;
+  const int64_t off = (layer - kv->st->lo) * kv->layer_stride + user * kv->user_stride + (int64_t)pos0 * c.head_dim;
+  KF_HIP(launch_kv_write(kv->k + off, kv->v + off, k_dev, v_dev, dtype == KF_BF16, n, c.n_kv_heads, c.head_dim,
+                         kv->max_ctx, kv->st->stream),
+         "kv_write launch");
+  return KF_OK;
+}
+
+kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, uint16_t* k_dev,
+                     uint16_t* v_dev) {
+  if (!kv) return fail(KF_EINVAL, "kv is NULL");
+  kf_status st = kv_slice_check(kv, layer, user, pos0, n);
+  if (st != KF_OK) return st;
+  if (n == 0) return KF_OK;
+  if (!k_dev || !v_dev) return fail(KF_EINVAL, "NULL destination");
+  const kf_model_config& c = kv->st->cfg;
+  const int64_t off = (layer - kv->st->lo) * kv->layer_stride + user * kv->user_stride + (int64_t)pos0 * c.head_dim;
+  KF_HIP(launch_kv_read(kv->k + off, kv->v + off, k_dev, v_dev, n, c.n_kv_heads, c.head_dim, kv->max_ctx,
+                        kv->st->stream),
+         "kv_read launch");
+  return KF_OK;
+}
+
+// ------------------------------------------------------------------ decode
+static void attn_split(int batch, int nkv, int max_len, int max_split, int* split, int* n_split) {
+  const int target = (512 + batch * nkv - 1) / (batch * nkv);  // about two workgroups per CU in total
+  auto up64 = [](int v) { return (v + 63) / 64 * 64; };
+  int sp = up64((max_len + target - 1) / target);
+  const int need = up64((max_len + max_split - 1) / max_split);
+  if (sp < need) sp = need;
+  if (sp < kAttnMinSplit) sp = kAttnMinSplit;
+  if (sp > kAttnMaxSplit) sp = kAttnMaxSplit;
+  *split = sp;
+  *n_split = (max_len + sp - 1) / sp;
+}
+
+kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* users, const int32_t* positions,
+                          const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev, kf_dtype io) {
+  if (!s || !kv) return fail(KF_EINVAL, "stage or kv is NULL");
+  if (kv->st != s) return fail(KF_EINVAL, "kv belongs to another stage");
+  if (batch < 1 || batch > kMaxBatch) return fail(KF_EINVAL, "batch %d outside [1, %d]", batch, kMaxBatch);
+  if (!users || !positions) return fail(KF_EINVAL, "users / positions is NULL");
+  if ((tokens_dev == nullptr) == (hidden_in_dev == nullptr))
+    return fail(KF_EINVAL, "exactly one of tokens / hidden input must be given");
+  if (tokens_dev && !s->has_head) return fail(KF_ESTATE, "token input needs the head");
+  if (!hidden_out_dev) return fail(KF_EINVAL, "hidden output is NULL");
+  if (io != KF_F32 && io != KF_BF16) return fail(KF_EINVAL, "io dtype");
+  int max_len = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int u = users[b], p = positions[b];
+    if (u < 0 || u >= kv->max_users) return fail(KF_EINVAL, "users[%d] = %d outside [0, %d)", b, u, kv->max_users);
+    for (int j = 0; j < b; ++j)
+      if (users[j] == u) return fail(KF_EINVAL, "user %d appears twice in the batch", u);
+    if (p != kv->len[u]) return fail(KF_EINVAL, "positions[%d] = %d but user %d holds %d positions", b, p, u, kv->len[u]);
+    if (p >= kv->max_ctx) return fail(KF_ERANGE, "position %d beyond max_ctx %d", p, kv->max_ctx);
+    if (p + 1 > max_len) max_len = p + 1;
+  }
+  const kf_model_config& c = s->cfg;
+  const int H = c.hidden, hd = c.head_dim;
+  hipStream_t st = s->stream;
+
+  KF_HIP(launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->x, batch, H, s->err_flag, st),
+         "prep launch");
+
+  int split, n_split;
+  attn_split(batch, c.n_kv_heads, max_len, kv->max_split, &split, &n_split);
+
+  for (int l = s->lo; l < s->hi; ++l) {
+    const LayerW& L = s->layers[l - s->lo];
+    const int64_t loff = (l - s->lo) * kv->layer_stride;
+
+    GemvParams g{};
+    g.batch = batch;
+    g.eps = c.rms_eps;
+    // attention RMSNorm + QKV + RoPE + KV append
+    g.w0 = L.wqkv;
+    g.gain = L.g_attn;
+    g.in = s->x;
+    g.K = H;
+    g.N = (c.n_q_heads + 2 * c.n_kv_heads) * hd;
+    g.q = s->q;
+    g.kc = kv->k + loff;
+    g.vc = kv->v + loff;
+    g.user_stride = kv->user_stride;
+    g.max_ctx = kv->max_ctx;
+    g.nq = c.n_q_heads;
+    g.nkv = c.n_kv_heads;
+    g.hd = hd;
+    g.rope_cos = kv->rcos;
+    g.rope_sin = kv->rsin;
+    for (int b = 0; b < kMaxBatch; ++b) {
+      g.users[b] = b < batch ? users[b] : 0;
+      g.pos[b] = b < batch ? positions[b] : 0;
+    }
+    KF_HIP(launch_gemv(kEpiQKV, 8, true, g, st), "qkv launch");
+
+    AttnParams a{};
+    a.q = s->q;
+    a.kc = kv->k + loff;
+    a.vc = kv->v + loff;
+    a.out = s->o;
+    a.part_acc = kv->part_acc;
+    a.part_ml = kv->part_ml;
+    a.counters = kv->counters;
+    a.user_stride = kv->user_stride;
+    a.max_ctx = kv->max_ctx;
+    a.nq = c.n_q_heads;
+    a.nkv = c.n_kv_heads;
+    a.hd = hd;
+    a.split = split;
+    a.n_split = n_split;
+    a.max_split = kv->max_split;
+    a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+    for (int b = 0; b < kMaxBatch; ++b) {
+      a.users[b] = b < batch ? users[b] : 0;
+      a.len[b] = b < batch ? positions[b] + 1 : 0;
+    }
+    KF_HIP(launch_attn_decode(a, batch, st), "attention launch");
+
+    GemvParams o{};
+    o.batch = batch;
+    o.w0 = L.wo;
+    o.in = s->o;
+    o.K = c.n_q_heads * hd;
+    o.N = H;
+    o.x = s->x;
+    KF_HIP(launch_gemv(kEpiResid, 8, false, o, st), "o-proj launch");
+
+    GemvParams gu{};
+    gu.batch = batch;
+    gu.eps = c.rms_eps;
+    gu.w0 = L.wg;
+    gu.w1 = L.wu;
+    gu.gain = L.g_mlp;
+    gu.in = s->x;
+    gu.K = H;
+    gu.N = c.ffn;
+    gu.act = s->act;
+    KF_HIP(launch_gemv(kEpiSwiGLU, 8, true, gu, st), "gate/up launch");
+
+    GemvParams d{};
+    d.batch = batch;
+    d.w0 = L.wd;
+    d.in = s->act;
+    d.K = c.ffn;
+    d.N = H;
+    d.x = s->x;
+    if (l == s->hi - 1) {
+      d.out2 = hidden_out_dev;
+      d.out2_bf16 = io == KF_BF16;
+    }
+    KF_HIP(launch_gemv(kEpiResid, 8, false, d, st), "down launch");
+  }
+  for (int b = 0; b < batch; ++b) kv->len[users[b]] += 1;
+  return KF_OK;
+}
+
+// ------------------------------------------------------------------ head
+static kf_status head_common(kf_stage* s, int rows, const void* hidden, kf_dtype dtype) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  if (!s->has_head) return fail(KF_ESTATE, "the stage does not hold the head");
+  if (rows < 1) return fail(KF_EINVAL, "rows must be >= 1");
+  if (!hidden) return fail(KF_EINVAL, "hidden is NULL");
+  if (dtype != KF_F32 && dtype != KF_BF16) return fail(KF_EINVAL, "dtype");
+  return KF_OK;
+}
+
+static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype dtype, float* logits) {
+  const kf_model_config& c = s->cfg;
+  KF_HIP(launch_prep_hidden(hidden, dtype == KF_BF16, nullptr, nullptr, 0, s->hx, rows, c.hidden, s->err_flag,
+                            s->stream),
+         "head prep launch");
+  GemvParams g{};
+  g.batch = rows;
+  g.eps = c.rms_eps;
+  g.w0 = s->lm_head;
+  g.gain = s->g_final;
+  g.in = s->hx;
+  g.K = c.hidden;
+  g.N = c.vocab;
+  g.logits = logits;
+  g.part_val = s->part_val;
+  g.part_idx = s->part_idx;
+  g.n_wg = s->lm_wg;
+  KF_HIP(launch_gemv(kEpiLMHead, 8, true, g, s->stream), "lm-head launch");
+  return KF_OK;
+}
+
+kf_status kf_head_logits(kf_stage* s, int32_t rows, const void* hidden, kf_dtype dtype, float* logits) {
+  kf_status st = head_common(s, rows, hidden, dtype);
+  if (st != KF_OK) return st;
+  if (!logits) return fail(KF_EINVAL, "logits is NULL");
+  const size_t esz = dtype == KF_BF16 ? 2 : 4;
+  for (int r0 = 0; r0 < rows; r0 += kMaxBatch) {
+    const int n = rows - r0 < kMaxBatch ? rows - r0 : kMaxBatch;
+    st = head_launch(s, n, (const char*)hidden + (size_t)r0 * s->cfg.hidden * esz, dtype,
+                     logits + (size_t)r0 * s->cfg.vocab);
+    if (st != KF_OK) return st;
+  }
+  return KF_OK;
+}
+
+kf_status kf_head_argmax(kf_stage* s, int32_t rows, const void* hidden, kf_dtype dtype, int32_t* token,
+                         float* max_logit) {
+  kf_status st = head_common(s, rows, hidden, dtype);
+  if (st != KF_OK) return st;
+  if (rows > kMaxBatch) return fail(KF_EINVAL, "rows %d above %d", rows, kMaxBatch);
+  if (!token) return fail(KF_EINVAL, "token is NULL");
+  st = head_launch(s, rows, hidden, dtype, nullptr);
+  if (st != KF_OK) return st;
+  KF_HIP(launch_argmax_final(s->part_val, s->part_idx, s->lm_wg, rows, token, max_logit, s->stream), "argmax launch");
+  return KF_OK;
+}
+
+// ------------------------------------------------------------------ prefill
+kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, int32_t n, const int32_t* tokens_dev,
+                           const void* hidden_in_dev, void* hidden_out_dev, kf_dtype io) {
+  if (!s || !kv) return fail(KF_EINVAL, "stage or kv is NULL");
+  if (kv->st != s) return fail(KF_EINVAL, "kv belongs to another stage");
+  if (n < 1) return fail(KF_EINVAL, "n_tokens must be >= 1");
+  if (user < 0 || user >= kv->max_users) return fail(KF_EINVAL, "user %d outside [0, %d)", user, kv->max_users);
+  if ((tokens_dev == nullptr) == (hidden_in_dev == nullptr))
+    return fail(KF_EINVAL, "exactly one of tokens / hidden input must be given");
+  if (tokens_dev && !s->has_head) return fail(KF_ESTATE, "token input needs the head");
+  if (!hidden_out_dev) return fail(KF_EINVAL, "hidden output is NULL");
+  if (io != KF_F32 && io != KF_BF16) return fail(KF_EINVAL, "io dtype");
+  if (pos0 != kv->len[user]) return fail(KF_EINVAL, "pos0 = %d but user %d holds %d positions", pos0, user, kv->len[user]);
+  if ((int64_t)pos0 + n > kv->max_ctx) return fail(KF_ERANGE, "positions up to %d beyond max_ctx %d", pos0 + n, kv->max_ctx);
+
+  const kf_model_config& c = s->cfg;
+  PrefillArgs pa{};
+  pa.H = c.hidden;
+  pa.nq = c.n_q_heads;
+  pa.nkv = c.n_kv_heads;
+  pa.hd = c.head_dim;
+  pa.F = c.ffn;
+  pa.eps = c.rms_eps;
+  pa.T = n;
+  pa.pos0 = pos0;
+  pa.max_ctx = kv->max_ctx;
+  pa.user_stride = kv->user_stride;
+  pa.rope_cos = kv->rcos;
+  pa.rope_sin = kv->rsin;
+  pa.stream = s->stream;
+  hipError_t e = prefill_reserve(s->pf, pa);
+  if (e == hipErrorOutOfMemory) return fail(KF_ENOMEM, "device allocation of the prefill workspace");
+  KF_HIP(e, "prefill workspace");
+  KF_HIP(launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->pf.x, n, c.hidden,
+                            s->err_flag, s->stream),
+         "prefill prep launch");
+  for (int l = s->lo; l < s->hi; ++l) {
+    const LayerW& L = s->layers[l - s->lo];
+    const int64_t loff = (l - s->lo) * kv->layer_stride + user * kv->user_stride;
+    PrefillLayer pl{};
+    pl.wqkv = L.wqkv;
+    pl.wo = L.wo;
+    pl.wg = L.wg;
+    pl.wu = L.wu;
+    pl.wd = L.wd;
+    pl.g_attn = L.g_attn;
+    pl.g_mlp = L.g_mlp;
+    pl.kc = kv->k + loff;
+    pl.vc = kv->v + loff;
+    pl.out = l == s->hi - 1 ? hidden_out_dev : nullptr;
+    pl.out_bf16 = io == KF_BF16;
+    KF_HIP(prefill_layer(s->pf, pa, pl), "prefill layer");
+  }
+  kv->len[user] += n;
+  return KF_OK;
+}
+
+}  // extern "C"

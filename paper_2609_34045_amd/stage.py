@@ -1,0 +1,315 @@
+"""Python binding of the stage library (``include/kafila_stage.h``).
+
+Argument marshalling only: every step of the forward pass runs in the HIP
+kernels of ``libkafila_stage.so``.  torch provides device memory (tensors are
+passed by ``data_ptr()``) and the stream.  The library must have been built
+(``python -m paper_2609_34045_amd.build``); importing this module without it
+raises, there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkafila_stage.so")
+
+KF_OK, KF_EINVAL, KF_ENOMEM, KF_ERANGE, KF_ESTATE, KF_EDEVICE, KF_EUNSUPPORTED = range(7)
+STATUS_NAMES = {0: "KF_OK", 1: "KF_EINVAL", 2: "KF_ENOMEM", 3: "KF_ERANGE", 4: "KF_ESTATE", 5: "KF_EDEVICE",
+                6: "KF_EUNSUPPORTED"}
+KF_F32, KF_BF16 = 0, 1
+MAX_BATCH = 4
+
+LAYER_KINDS = {"attn_norm": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "mlp_norm": 5, "wg": 6, "wu": 7, "wd": 8}
+HEAD_KINDS = {"embed": 9, "final_norm": 10, "lm_head": 11}
+
+EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init", "kf_stage_destroy",
+           "kf_stage_set_stream", "kf_stage_sync", "kf_kv_create", "kf_kv_destroy", "kf_kv_len", "kf_kv_set_len",
+           "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax")
+
+
+class KFError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class ModelConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+
+    @classmethod
+    def of(cls, shape) -> "ModelConfig":
+        return cls(shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
+                   shape.vocab, shape.rms_eps, shape.rope_theta)
+
+
+class Tensor(ctypes.Structure):
+    _fields_ = [("layer", ctypes.c_int32), ("kind", ctypes.c_int32), ("bf16", ctypes.c_void_p), ("numel", ctypes.c_int64)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [("tensors", ctypes.POINTER(Tensor)), ("count", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load the built library once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2609_34045_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, VP = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    I32P, I64P = ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64)
+    sig = {
+        "kf_abi_version": (I32, []),
+        "kf_last_error": (ctypes.c_char_p, []),
+        "kf_stage_bytes": (I32, [ctypes.POINTER(ModelConfig), I32, I32, I32, I32, I32, I64P, I64P, I64P]),
+        "kf_stage_init": (I32, [ctypes.POINTER(ModelConfig), I32, I32, I32, ctypes.POINTER(Weights), VP,
+                                ctypes.POINTER(P)]),
+        "kf_stage_destroy": (I32, [P]),
+        "kf_stage_set_stream": (I32, [P, VP]),
+        "kf_stage_sync": (I32, [P]),
+        "kf_kv_create": (I32, [P, I32, I32, ctypes.POINTER(P)]),
+        "kf_kv_destroy": (I32, [P]),
+        "kf_kv_len": (I32, [P, I32, I32P]),
+        "kf_kv_set_len": (I32, [P, I32, I32]),
+        "kf_kv_write": (I32, [P, I32, I32, I32, I32, VP, VP, I32]),
+        "kf_kv_read": (I32, [P, I32, I32, I32, I32, VP, VP]),
+        "kf_stage_decode": (I32, [P, P, I32, I32P, I32P, VP, VP, VP, I32]),
+        "kf_stage_prefill": (I32, [P, P, I32, I32, I32, VP, VP, VP, I32]),
+        "kf_head_logits": (I32, [P, I32, VP, I32, VP]),
+        "kf_head_argmax": (I32, [P, I32, VP, I32, VP, VP]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != KF_OK:
+        raise KFError(status, where, _lib.kf_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _io_dtype(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return KF_F32
+    if t.dtype == torch.bfloat16:
+        return KF_BF16
+    raise TypeError(f"hidden states must be float32 or bfloat16, not {t.dtype}")
+
+
+def _require_device(t, what: str):
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+
+
+def stage_bytes(shape, lo: int, hi: int, has_head: bool, max_users: int, max_ctx: int):
+    """(beta_block, beta_head, resident) bytes of a stage; host-only arithmetic in the library."""
+    lib = load_library()
+    cfg = ModelConfig.of(shape)
+    bb, bh, rs = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib.kf_stage_bytes(ctypes.byref(cfg), lo, hi, int(has_head), max_users, max_ctx, ctypes.byref(bb),
+                              ctypes.byref(bh), ctypes.byref(rs)), "kf_stage_bytes")
+    return bb.value, bh.value, rs.value
+
+
+class Stage:
+    """Layers ``[lo, hi)`` of a model (and the head if ``head_weights`` is given) on the current device.
+
+    ``layer_weights`` maps each held layer index to a dict of bf16 bit arrays
+    (numpy uint16, row-major [out, in]) named attn_norm, wq, wk, wv, wo, mlp_norm,
+    wg, wu, wd; ``head_weights`` holds embed, final_norm and lm_head.
+    """
+
+    def __init__(self, shape, lo: int, hi: int, layer_weights, head_weights=None, stream=None):
+        import torch
+        lib = load_library()
+        self.shape, self.lo, self.hi = shape, lo, hi
+        self.has_head = head_weights is not None
+        self._cfg = ModelConfig.of(shape)
+        keep, items = [], []
+        for l in range(lo, hi):
+            w = layer_weights[l] if not callable(layer_weights) else layer_weights(l)
+            for name, kind in LAYER_KINDS.items():
+                a = np.ascontiguousarray(w[name], dtype=np.uint16)
+                keep.append(a)
+                items.append(Tensor(l, kind, a.ctypes.data, a.size))
+        if self.has_head:
+            for name, kind in HEAD_KINDS.items():
+                a = np.ascontiguousarray(head_weights[name], dtype=np.uint16)
+                keep.append(a)
+                items.append(Tensor(-1, kind, a.ctypes.data, a.size))
+        arr = (Tensor * len(items))(*items)
+        ws = Weights(arr, len(items))
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.stream = stream
+        handle = ctypes.c_void_p()
+        _check(lib.kf_stage_init(ctypes.byref(self._cfg), lo, hi, int(self.has_head), ctypes.byref(ws),
+                                 ctypes.c_void_p(stream.cuda_stream), ctypes.byref(handle)), "kf_stage_init")
+        self.handle = handle
+        self._lib = lib
+
+    # -- lifetime
+    def close(self):
+        if self.handle:
+            _check(self._lib.kf_stage_destroy(self.handle), "kf_stage_destroy")
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def set_stream(self, stream):
+        _check(self._lib.kf_stage_set_stream(self.handle, ctypes.c_void_p(stream.cuda_stream)), "kf_stage_set_stream")
+        self.stream = stream
+
+    def sync(self):
+        _check(self._lib.kf_stage_sync(self.handle), "kf_stage_sync")
+
+    def kv(self, max_users: int, max_ctx: int) -> "KV":
+        return KV(self, max_users, max_ctx)
+
+    # -- compute
+    def decode(self, kv: "KV", users, positions, tokens=None, hidden=None, out=None):
+        import torch
+        B = len(users)
+        u = (ctypes.c_int32 * max(B, 1))(*users)
+        p = (ctypes.c_int32 * max(B, 1))(*positions)
+        if len(positions) != B:
+            raise ValueError("users and positions differ in length")
+        src = hidden if hidden is not None else tokens
+        if hidden is not None:
+            _require_device(hidden, "hidden")
+            io = _io_dtype(hidden)
+            odt = hidden.dtype
+        else:
+            io, odt = KF_F32, torch.float32
+        if tokens is not None:
+            _require_device(tokens, "tokens")
+            if tokens.dtype != torch.int32:
+                raise TypeError("tokens must be int32")
+        if out is None:
+            out = torch.empty((B, self.shape.hidden), dtype=odt, device=src.device if src is not None else "cuda")
+        else:
+            _require_device(out, "out")
+            if _io_dtype(out) != io:
+                raise TypeError("out dtype must match the hidden input dtype")
+        _check(self._lib.kf_stage_decode(self.handle, kv.handle, B, u, p, _ptr(tokens), _ptr(hidden), _ptr(out), io),
+               "kf_stage_decode")
+        return out
+
+    def prefill(self, kv: "KV", user: int, pos0: int, tokens=None, hidden=None, out=None):
+        import torch
+        src = hidden if hidden is not None else tokens
+        n = 0 if src is None else int(src.shape[0])
+        if hidden is not None:
+            _require_device(hidden, "hidden")
+            io, odt = _io_dtype(hidden), hidden.dtype
+        else:
+            io, odt = KF_F32, torch.float32
+        if tokens is not None:
+            _require_device(tokens, "tokens")
+            if tokens.dtype != torch.int32:
+                raise TypeError("tokens must be int32")
+        if out is None:
+            out = torch.empty((max(n, 1), self.shape.hidden), dtype=odt, device=src.device if src is not None else "cuda")
+        _check(self._lib.kf_stage_prefill(self.handle, kv.handle, user, pos0, n, _ptr(tokens), _ptr(hidden),
+                                          _ptr(out), io), "kf_stage_prefill")
+        return out
+
+    def head_logits(self, hidden, out=None):
+        import torch
+        _require_device(hidden, "hidden")
+        rows = int(hidden.shape[0])
+        if out is None:
+            out = torch.empty((rows, self.shape.vocab), dtype=torch.float32, device=hidden.device)
+        _check(self._lib.kf_head_logits(self.handle, rows, _ptr(hidden), _io_dtype(hidden), _ptr(out)),
+               "kf_head_logits")
+        return out
+
+    def head_argmax(self, hidden, with_max: bool = False):
+        import torch
+        _require_device(hidden, "hidden")
+        rows = int(hidden.shape[0])
+        tok = torch.empty((rows,), dtype=torch.int32, device=hidden.device)
+        mx = torch.empty((rows,), dtype=torch.float32, device=hidden.device) if with_max else None
+        _check(self._lib.kf_head_argmax(self.handle, rows, _ptr(hidden), _io_dtype(hidden), _ptr(tok), _ptr(mx)),
+               "kf_head_argmax")
+        return (tok, mx) if with_max else tok
+
+
+class KV:
+    """A KV reservation of ``max_users`` users x ``max_ctx`` positions for every layer of a stage."""
+
+    def __init__(self, stage: Stage, max_users: int, max_ctx: int):
+        self.stage, self.max_users, self.max_ctx = stage, max_users, max_ctx
+        self._lib = stage._lib
+        h = ctypes.c_void_p()
+        _check(self._lib.kf_kv_create(stage.handle, max_users, max_ctx, ctypes.byref(h)), "kf_kv_create")
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            _check(self._lib.kf_kv_destroy(self.handle), "kf_kv_destroy")
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def len(self, user: int) -> int:
+        n = ctypes.c_int32()
+        _check(self._lib.kf_kv_len(self.handle, user, ctypes.byref(n)), "kf_kv_len")
+        return n.value
+
+    def set_len(self, user: int, n: int):
+        _check(self._lib.kf_kv_set_len(self.handle, user, n), "kf_kv_set_len")
+
+    def write(self, layer: int, user: int, pos0: int, k, v):
+        """k, v: device tensors [n, nkv, hd], bfloat16 (or int16/uint16 bf16 bits) or float32."""
+        import torch
+        _require_device(k, "k")
+        _require_device(v, "v")
+        if k.dtype == torch.float32:
+            dt = KF_F32
+        elif k.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+            dt = KF_BF16
+        else:
+            raise TypeError("k/v dtype")
+        _check(self._lib.kf_kv_write(self.handle, layer, user, pos0, int(k.shape[0]), _ptr(k), _ptr(v), dt),
+               "kf_kv_write")
+
+    def read(self, layer: int, user: int, pos0: int, n: int):
+        """Returns (k, v) as bfloat16 device tensors [n, nkv, hd]."""
+        import torch
+        s = self.stage.shape
+        k = torch.empty((n, s.n_kv_heads, s.head_dim), dtype=torch.bfloat16, device="cuda")
+        v = torch.empty_like(k)
+        _check(self._lib.kf_kv_read(self.handle, layer, user, pos0, n, _ptr(k), _ptr(v)), "kf_kv_read")
+        return k, v
