@@ -1,0 +1,278 @@
+#!/usr/bin/env python3
+"""Stage decode benchmark on one MI355X.
+
+Times K decode steps of one pipeline stage (a contiguous range of decoder
+layers, optionally with the head) at the workload's batch and context, and
+prints one JSON line: tokens/s, the step's algorithmic HBM bytes per second
+against the 8 TB/s peak, the dominant kernel's roofline figure (HIP-event
+durations of its launches inside the timed region), and the CPU oracle's
+throughput on a bounded sample of the same workload.
+
+Default workload: layers [8, 16) of a Llama-3-8B-shaped model (H4096,
+32 q / 8 KV heads x 128, F14336), batch 1, KV cache injected for positions
+[0, 2048), decode at positions 2048.. .  All inputs are seeded and synthetic.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+METRIC = "stage decode tokens/s + achieved HBM GB/s (% of peak), batch 1 and 4"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_decode_gateup_8b_mid.json")
+DECODE_SRC = os.path.join(ROOT, "paper_2609_34045_amd", "csrc", "decode.hip")
+
+
+def log(msg: str):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="8b_mid", choices=[k for k in synth.WORKLOADS])
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="CPU oracle sample budget (0 disables)")
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="skip the per-launch HIP-event pass (no roofline figure)")
+    return ap.parse_args()
+
+
+# ------------------------------------------------------------------ algorithmic work
+def step_bytes(wl, positions) -> int:
+    """HBM bytes one decode step must move: every weight once, each user's K/V for keys 0..p, the appends,
+    and with the head the LM head plus the gathered embedding rows."""
+    s = wl.shape
+    L = wl.layer_hi - wl.layer_lo
+    kv_per_key = 4 * s.n_kv_heads * s.head_dim  # K and V, bf16
+    b = L * s.block_bytes()
+    b += sum(L * kv_per_key * (p + 1) for p in positions)  # reads (the new key included)
+    b += len(positions) * L * kv_per_key  # appends
+    if wl.has_head:
+        b += s.vocab * s.hidden * 2 + s.hidden * 2 + len(positions) * s.hidden * 2
+    return int(b)
+
+
+def gateup_bytes(wl, B: int) -> int:
+    """Algorithmic bytes of one gate/up launch: both matrices, the gain, the input rows, the SwiGLU output."""
+    s = wl.shape
+    return 2 * s.ffn * s.hidden * 2 + s.hidden * 2 + B * s.hidden * 4 + B * s.ffn * 4
+
+
+def source_hash(path: str) -> str:
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def traffic_from_counters(wl_name: str):
+    """HBM bytes per gate/up launch from committed rocprofv3 counter runs, or None if absent or stale."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    rec = json.load(open(COUNTERS_FILE))
+    if rec.get("workload") != wl_name or rec.get("decode_hip_sha256_16") != source_hash(DECODE_SRC):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ------------------------------------------------------------------ CPU oracle baseline
+def cpu_baseline(wl, model_layers, kv_inject, hidden_steps, budget_s: float):
+    from threadpoolctl import threadpool_info
+
+    from oracle import OracleStage
+
+    s = wl.shape
+    B = wl.batch
+    ctx = list(wl.contexts)
+    o = OracleStage(s, wl.layer_lo, wl.layer_hi, model_layers, None, max_users=B,
+                    max_ctx=max(ctx) + len(hidden_steps) + 1, cache_weights=True)
+    t0 = time.perf_counter()
+    for l in range(wl.layer_lo, wl.layer_hi):
+        o.weights(l)  # widen to float64 outside the timed region
+    widen_s = time.perf_counter() - t0
+    for (l, u), (kb, vb) in kv_inject.items():
+        o.kv.inject(l, u, 0, kb, vb)
+    for u in range(B):
+        o.kv.set_len(u, ctx[u])
+    done, t0 = 0, time.perf_counter()
+    while done < len(hidden_steps):
+        o.decode(list(range(B)), [ctx[u] + done for u in range(B)], hidden=hidden_steps[done])
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
+    return {
+        "value": round(B * done / el, 3),
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{done} decode step(s) of the same stage, batch {B}, from the injected context "
+                  f"(float64 numpy oracle; {widen_s:.1f} s of weight widening excluded)",
+    }
+
+
+# ------------------------------------------------------------------ main
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU; the stage is one GPU's share of the ring "
+                                   "(multi-GPU pipelining is not built)", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+
+    from paper_2609_34045_amd import stage as kf
+
+    wl = synth.WORKLOADS[args.workload]
+    s, B = wl.shape, wl.batch
+    ctx = list(wl.contexts)
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    layers = {l: synth.layer_weights(s, wl.cfg_id, l, wl.seed) for l in range(wl.layer_lo, wl.layer_hi)}
+    head = synth.head_weights(s, wl.cfg_id, wl.seed) if wl.has_head else None
+    log(f"[bench] generated {wl.name} weights in {time.perf_counter() - t0:.1f} s")
+    t0 = time.perf_counter()
+    g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, head)
+    span = max(args.steps, args.warmup)
+    kv = g.kv(B, max(ctx) + span + 1)
+    inject = {}
+    for l in range(wl.layer_lo, wl.layer_hi):
+        for u in range(B):
+            kb, vb = synth.injected_kv(s, wl.cfg_id, l, u, ctx[u], wl.seed)
+            inject[(l, u)] = (kb, vb)
+            kv.write(l, u, 0, torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+    for u in range(B):
+        kv.set_len(u, ctx[u])
+    torch.cuda.synchronize()
+    log(f"[bench] stage init + KV injection {time.perf_counter() - t0:.1f} s")
+
+    hs = [synth.hidden_states(wl.cfg_id, synth.STREAM_DECODE_HIDDEN, i, B, s.hidden, wl.seed) for i in range(span)]
+    hid = torch.from_numpy(np.stack(hs)).cuda()  # resident before the timed region
+    toks = torch.from_numpy(synth.tokens(wl.cfg_id, 0, B, s.vocab, wl.seed)).cuda() if wl.has_head else None
+    out = torch.empty((B, s.hidden), dtype=torch.float32, device="cuda")
+    users = list(range(B))
+
+    def run(n: int):
+        nonlocal toks
+        for i in range(n):
+            pos = [ctx[u] + i for u in users]
+            if wl.has_head:
+                g.decode(kv, users, pos, tokens=toks, out=out)
+                toks = g.head_argmax(out)  # closed-loop greedy decode
+            else:
+                g.decode(kv, users, pos, hidden=hid[i], out=out)
+
+    def reset():
+        for u in users:
+            kv.set_len(u, ctx[u])
+
+    run(args.warmup)
+    g.sync()
+    reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    run(args.steps)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms_step = ev0.elapsed_time(ev1) / args.steps
+    ms_step = 1e3 * wall / args.steps
+    tok_s = B * args.steps / (wall if wall > 0 else 1e-9)
+    g.sync()
+
+    # Kernel-timing passes: the same K steps again with HIP event pairs around
+    # launches (each pair adds a few microseconds to the stream, so they stay out
+    # of the timed region above).  The roofline pass brackets only the dominant
+    # kernel; the breakdown pass brackets every launch.
+    prof, dom = {}, {}
+    if not args.no_kernel_events:
+        reset()
+        g.profile(True, classes=["gateup"])
+        run(args.steps)
+        g.profile(False)
+        dom = g.profile_read()
+        reset()
+        g.profile(True)
+        run(args.steps)
+        g.profile(False)
+        prof = g.profile_read()
+        g.sync()
+    positions_mid = [ctx[u] + args.steps // 2 for u in users]
+    sb = step_bytes(wl, positions_mid)
+    hbm = sb / (ms_step * 1e-3) / 1e9
+
+    # dominant kernel: the fused RMSNorm + gate/up + SwiGLU GEMV
+    n_gu, t_gu = dom.get("gateup", (0, 0.0))
+    avg_gu_ms = t_gu / max(n_gu, 1)
+    gu_bytes = gateup_bytes(wl, B)
+    achieved = gu_bytes / (avg_gu_ms * 1e-3) / 1e9 if n_gu else None
+    per_kernel = {k: {"launches": n, "avg_us": round(1e3 * t / n, 2), "share": round(t / max(sum(v[1] for v in
+                  prof.values()), 1e-9), 4)} for k, (n, t) in prof.items()}
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(wl, lambda l: layers[l], inject, hs, args.cpu_seconds)
+        log(f"[bench] cpu oracle {cpu['value']} tokens/s on {cpu['cores']} threads")
+
+    traffic = traffic_from_counters(wl.name)
+    line = {
+        "metric": METRIC,
+        "value": round(tok_s, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "gpu_ms_per_step": round(gpu_ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}) of a {s.n_layers}-layer model, H{s.hidden}, "
+                        f"{s.n_q_heads}q/{s.n_kv_heads}kv x {s.head_dim}, F{s.ffn}"
+                        + (f", head V{s.vocab}" if wl.has_head else "") + f"; batch {B}, contexts {ctx}, decode",
+            "batch": B,
+            "contexts": ctx,
+            "layers": wl.layer_hi - wl.layer_lo,
+            "has_head": wl.has_head,
+            "parallelism": "single GPU (one stage)",
+        },
+        "hbm": {"algorithmic_bytes_per_step": sb, "achieved_gbps": round(hbm, 1),
+                "frac_of_peak": round(hbm / PEAK_HBM_GBPS, 4), "peak_gbps": PEAK_HBM_GBPS},
+        "roofline": {
+            "kernel": "gemv gate/up + RMSNorm + SwiGLU (decode)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1) if achieved else None,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4) if achieved else None,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": gu_bytes,
+            "avg_launch_us": round(avg_gu_ms * 1e3, 2),
+            "launches": n_gu,
+        },
+        "per_kernel": per_kernel,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    kv.close()
+    g.close()
+
+
+if __name__ == "__main__":
+    main()

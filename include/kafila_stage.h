@@ -200,6 +200,42 @@ kf_status kf_head_logits(kf_stage* stage, int32_t rows, const void* hidden_dev, 
 kf_status kf_head_argmax(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype,
                          int32_t* token_dev, float* max_logit_dev);
 
+/*
+ * Per-kernel timing (instrumentation).  The paper's sessions record predicted and
+ * measured cost per stage (Section VI); this records, per kernel class, the HIP-event
+ * time of every launch the stage enqueues while recording is on.
+ *   kf_stage_profile(stage, mask) clears the records and starts recording the classes
+ *   whose bit (1 << class) is set in mask; kf_stage_profile(stage, 0) stops recording
+ *   (records are kept).  KF_K_ALL records every class.
+ *   kf_stage_profile_read waits for the stage's stream, then returns the number of
+ *   recorded launches of a class and their summed duration in milliseconds.
+ * Each recorded launch is bracketed by two hipEventRecord calls on the stage's
+ * stream, which adds a few microseconds per launch to the stream's timeline.
+ */
+typedef enum {
+  KF_K_PREP = 0,       /* hidden/token input to the fp32 residual stream */
+  KF_K_QKV = 1,        /* decode: RMSNorm + QKV GEMV + RoPE + KV append */
+  KF_K_ATTN = 2,       /* decode: split-KV attention + merge */
+  KF_K_OPROJ = 3,      /* decode: O GEMV + residual */
+  KF_K_GATEUP = 4,     /* decode: RMSNorm + gate/up GEMV + SwiGLU */
+  KF_K_DOWN = 5,       /* decode: down GEMV + residual */
+  KF_K_LMHEAD = 6,     /* head: final RMSNorm + LM-head GEMV + partial argmax */
+  KF_K_ARGMAX = 7,     /* head: final argmax reduction */
+  KF_K_PF_NORM = 8,    /* prefill: row RMSNorm to bf16 */
+  KF_K_PF_QKV = 9,     /* prefill: QKV GEMM (matrix cores) */
+  KF_K_PF_ROPE = 10,   /* prefill: RoPE + KV append */
+  KF_K_PF_ATTN = 11,   /* prefill: causal flash attention (matrix cores) */
+  KF_K_PF_OPROJ = 12,  /* prefill: O GEMM + residual */
+  KF_K_PF_GATEUP = 13, /* prefill: gate/up GEMM + SwiGLU */
+  KF_K_PF_DOWN = 14,   /* prefill: down GEMM + residual */
+  KF_K_PF_STORE = 15,  /* prefill: hidden output store */
+  KF_K_COUNT = 16
+} kf_kernel_class;
+#define KF_K_ALL 0xffff
+
+kf_status kf_stage_profile(kf_stage* stage, int32_t mask);
+kf_status kf_stage_profile_read(kf_stage* stage, int32_t kernel_class, int64_t* launches, double* total_ms);
+
 #ifdef __cplusplus
 }
 #endif

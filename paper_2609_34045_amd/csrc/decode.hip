@@ -15,8 +15,8 @@
 //     O and down GEMVs' epilogues.
 //   * The LM-head GEMV reduces (max, lowest index) per workgroup.
 // Attention is split-KV over a bf16 cache, [user][kv_head][pos][hd]; each
-// workgroup serves all query heads of one KV head, and the last workgroup of
-// a (row, KV head) merges the splits (online-softmax rescaling).
+// workgroup serves all query heads of one KV head, and a second small kernel
+// merges the splits of each (row, KV head) (online-softmax rescaling).
 #include "kernels.h"
 
 namespace kf {
@@ -95,9 +95,13 @@ __device__ __forceinline__ float wave_max(float v) {
 // stride over K in 16-byte chunks (thread t takes chunks t, t+256, ...), so
 // each wave's loads of a row are 1 KB contiguous.  U chunks of all R rows are
 // in flight per thread before any is consumed.
+#ifndef KF_GEMV_U
+#define KF_GEMV_U 1
+#endif
+
 template <int B, int R, int EPI, bool NORM>
 __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
-  constexpr int T = 256, U = 2;
+  constexpr int T = 256, U = KF_GEMV_U;
   constexpr int NV = R * B + (NORM ? B : 0);
   constexpr int NVP = NV <= 8 ? 8 : NV <= 16 ? 16 : NV <= 32 ? 32 : 64;
   static_assert(NV <= 64, "too many partial sums per workgroup");
@@ -273,11 +277,16 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
 // Workgroup (split s, KV head g, row b) covers keys [s*split, min((s+1)*split, len_b)).
 // A key's hd elements are read by hd/8 lanes, 16 bytes each; all G query heads of
 // the group are scored against it, so each K/V byte is read once per KV head.
+// Each wave runs its own online softmax over chunks of 4 keys per lane group (K
+// and V of a chunk are loaded together, so one memory latency covers both); the
+// four waves' (max, sum, acc) states are merged through LDS and written as the
+// split's partial.
 template <int HD, int G>
 __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
-  constexpr int LPK = HD / 8;
-  constexpr int KPW = 64 / LPK;
-  constexpr int KPP = 4 * KPW;
+  constexpr int LPK = HD / 8;      // lanes per key
+  constexpr int KPW = 64 / LPK;    // keys per wave per pass
+  constexpr int J = 4;             // keys per lane group per chunk
+  constexpr int CH = KPW * J;      // keys per wave chunk
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int len = p.len[b];
@@ -285,16 +294,14 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
   const int hq0 = g * G;
 
-  __shared__ float sc[G][kAttnMaxSplit];
-  __shared__ float red[4][G][HD];
-  __shared__ float ml[G][2];
-  __shared__ int is_last;
+  __shared__ float wacc[4][G][HD];
+  __shared__ float wml[4][G][2];
 
   const int64_t head_off = (int64_t)p.users[b] * p.user_stride + (int64_t)g * p.max_ctx * HD;
   const uint16_t* kb = p.kc + head_off + (int64_t)s0 * HD;
   const uint16_t* vb = p.vc + head_off + (int64_t)s0 * HD;
   const int d0 = (lane % LPK) * 8;
-  const int kslot = wave * KPW + lane / LPK;
+  const int kgrp = lane / LPK;
 
   float qv[G][8];
 #pragma unroll
@@ -306,99 +313,136 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     qv[h][4] = hi.x * p.scale_log2; qv[h][5] = hi.y * p.scale_log2;
     qv[h][6] = hi.z * p.scale_log2; qv[h][7] = hi.w * p.scale_log2;
   }
-
-  // scores (log2 domain)
-  for (int t = kslot; t < nk; t += KPP) {
-    float kf[8];
-    bf16x8(*reinterpret_cast<const v4u*>(kb + (int64_t)t * HD + d0), kf);
-    float d[G];
+  float acc[G][8], m_run[G], l_run[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float a = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) a += qv[h][i] * kf[i];
-      d[h] = a;
-    }
-#pragma unroll
-    for (int o = LPK / 2; o >= 1; o >>= 1) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) d[h] += __shfl_xor(d[h], o);
-    }
-    if ((lane % LPK) == 0) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) sc[h][t] = d[h];
-    }
-  }
-  __syncthreads();
-
-  for (int h = wave; h < G; h += 4) {
-    float m = -INFINITY;
-    for (int t = lane; t < nk; t += 64) m = fmaxf(m, sc[h][t]);
-    m = wave_max(m);
-    float l = 0.f;
-    for (int t = lane; t < nk; t += 64) {
-      const float e = exp2f(sc[h][t] - m);
-      sc[h][t] = e;
-      l += e;
-    }
-    l = wave_sum(l);
-    if (lane == 0) {
-      ml[h][0] = m;
-      ml[h][1] = l;
-    }
-  }
-  __syncthreads();
-
-  float acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h)
+  for (int h = 0; h < G; ++h) {
+    m_run[h] = -INFINITY;
+    l_run[h] = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[h][i] = 0.f;
-  for (int t = kslot; t < nk; t += KPP) {
-    float vf[8];
-    bf16x8(*reinterpret_cast<const v4u*>(vb + (int64_t)t * HD + d0), vf);
+  }
+
+  for (int c0 = wave * CH; c0 < nk; c0 += 4 * CH) {
+    v4u kw[J], vw[J];
+    bool ok[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int t = c0 + j * KPW + kgrp;
+      ok[j] = t < nk;
+      const int tt = ok[j] ? t : 0;
+      kw[j] = *reinterpret_cast<const v4u*>(kb + (int64_t)tt * HD + d0);
+      vw[j] = *reinterpret_cast<const v4u*>(vb + (int64_t)tt * HD + d0);
+    }
+    float sc[J][G];
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      float kf[8];
+      bf16x8(kw[j], kf);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float a = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a += qv[h][i] * kf[i];
+        sc[j][h] = a;
+      }
+    }
+#pragma unroll
+    for (int o = LPK / 2; o >= 1; o >>= 1)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int h = 0; h < G; ++h) sc[j][h] += __shfl_xor(sc[j][h], o);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float pt = sc[h][t];
+      float mc = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[h][i] += pt * vf[i];
+      for (int j = 0; j < J; ++j) mc = ok[j] ? fmaxf(mc, sc[j][h]) : mc;
+#pragma unroll
+      for (int o = LPK; o < 64; o <<= 1) mc = fmaxf(mc, __shfl_xor(mc, o));
+      const float m_new = fmaxf(m_run[h], mc);  // finite: the chunk has at least one valid key
+      const float alpha = exp2f(m_run[h] - m_new);
+      m_run[h] = m_new;
+      l_run[h] *= alpha;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[h][i] *= alpha;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const float pj = ok[j] ? exp2f(sc[j][h] - m_new) : 0.f;
+        sc[j][h] = pj;
+        l_run[h] += pj;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      float vf[8];
+      bf16x8(vw[j], vf);
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[h][i] += sc[j][h] * vf[i];
     }
   }
+  // Sum over the key groups of the wave (same dims, distinct keys, same running max).
 #pragma unroll
   for (int o = LPK; o < 64; o <<= 1) {
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+    for (int h = 0; h < G; ++h) {
+      l_run[h] += __shfl_xor(l_run[h], o);
 #pragma unroll
       for (int i = 0; i < 8; ++i) acc[h][i] += __shfl_xor(acc[h][i], o);
+    }
   }
   if (lane < LPK) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) red[wave][h][d0 + i] = acc[h][i];
+      for (int i = 0; i < 8; ++i) wacc[wave][h][d0 + i] = acc[h][i];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      wml[wave][h][0] = m_run[h];
+      wml[wave][h][1] = l_run[h];
+    }
   }
   __syncthreads();
 
+  // Merge the four waves into this split's partial.
   for (int e = tid; e < G * HD; e += 256) {
     const int h = e / HD, d = e % HD;
-    const float v = (red[0][h][d] + red[1][h][d]) + (red[2][h][d] + red[3][h][d]);
-    p.part_acc[(((int64_t)b * p.nq + hq0 + h) * p.max_split + split) * HD + d] = v;
-  }
-  if (tid < G) {
-    float* dst = p.part_ml + (((int64_t)b * p.nq + hq0 + tid) * p.max_split + split) * 2;
-    dst[0] = ml[tid][0];
-    dst[1] = ml[tid][1];
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (wml[w][h][1] > 0.f) M = fmaxf(M, wml[w][h][0]);
+    float v = 0.f, l = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float sw = wml[w][h][1] > 0.f ? exp2f(wml[w][h][0] - M) : 0.f;
+      v += sw * wacc[w][h][d];
+      l += sw * wml[w][h][1];
+    }
+    const int64_t row = ((int64_t)b * p.nq + hq0 + h) * p.max_split + split;
+    p.part_acc[row * HD + d] = v;
+    if (d == 0) {
+      p.part_ml[row * 2] = M;
+      p.part_ml[row * 2 + 1] = l;
+    }
   }
 
-  // The last workgroup of (b, g) to finish merges the splits.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) is_last = (atomicAdd(&p.counters[b * p.nkv + g], 1) == p.n_split - 1);
-  __syncthreads();
-  if (!is_last) return;
-  __threadfence();
+}
 
-  const int ns = p.n_split;
+// Merge of the split-KV partials of one (row, KV head): all G query heads, all hd dims.
+// Runs as its own launch so that the kernel boundary orders the partials' writes
+// before these reads (a device-scope fence per workgroup costs far more on gfx950).
+// The per-split weights 2^(m_s - M) are computed once into LDS; the weighted sum
+// over splits then has no data-dependent branch, so its loads stay in flight.
+template <int HD, int G>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams p) {
+  const int g = blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hq0 = g * G, ns = p.n_split;
+  __shared__ float wsplit[G][kAttnMaxSplitCount];
+  __shared__ float inv_l[G];
   for (int h = wave; h < G; h += 4) {
     const float* mlh = p.part_ml + ((int64_t)b * p.nq + hq0 + h) * p.max_split * 2;
     float M = -INFINITY;
@@ -409,44 +453,52 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     for (int s = lane; s < ns; s += 64) {
       const float l = mlh[2 * s + 1];
       const float w = l > 0.f ? exp2f(mlh[2 * s] - M) : 0.f;
-      sc[h][s] = w;
+      wsplit[h][s] = w;
       L += w * l;
     }
     L = wave_sum(L);
-    if (lane == 0) ml[h][1] = 1.0f / L;
+    if (lane == 0) inv_l[h] = 1.0f / L;
   }
   __syncthreads();
-  for (int e = tid; e < G * HD; e += 256) {
-    const int h = e / HD, d = e % HD;
-    const float* acc_h = p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD + d;
-    float o = 0.f;
-    for (int s = 0; s < ns; ++s) o += sc[h][s] * acc_h[(int64_t)s * HD];
-    p.out[(int64_t)b * p.nq * HD + (hq0 + h) * HD + d] = o * ml[h][1];
+  for (int e = tid; e < G * HD / 4; e += 256) {
+    const int h = e / (HD / 4), d4 = e % (HD / 4);
+    const v4f* src = reinterpret_cast<const v4f*>(p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD) + d4;
+    v4f o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int s = 0; s < ns; ++s) o += wsplit[h][s] * src[(int64_t)s * (HD / 4)];
+    reinterpret_cast<v4f*>(p.out + (int64_t)b * p.nq * HD + (hq0 + h) * HD)[d4] = o * inv_l[h];
   }
-  if (tid == 0) p.counters[b * p.nkv + g] = 0;
 }
 
 // ------------------------------------------------------------------ small kernels
-__global__ void prep_hidden_kernel(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed,
-                                   int vocab, float* x, int H, int* err_flag) {
-  const int row = blockIdx.x;
-  float* xr = x + (int64_t)row * H;
+// One thread per 4 elements of the [rows][H] input (H is a multiple of 64).
+__global__ void prep_hidden_kernel(const void* __restrict__ in, int in_bf16, const int32_t* __restrict__ tokens,
+                                   const uint16_t* __restrict__ embed, int vocab, float* __restrict__ x, int rows, int H,
+                                   int* err_flag) {
+  const int64_t i4 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;  // index of a group of 4 elements
+  const int64_t n4 = (int64_t)rows * H / 4;
+  if (i4 >= n4) return;
+  const int row = (int)(i4 * 4 / H), k = (int)(i4 * 4 % H);
+  v4f v;
   if (tokens) {
     const int tok = tokens[row];
     if (tok < 0 || tok >= vocab) {
-      if (threadIdx.x == 0) atomicOr(err_flag, 1);
-      for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = __uint_as_float(0x7fc00000u);
-      return;
+      if (k == 0) atomicOr(err_flag, 1);
+      const float qn = __uint_as_float(0x7fc00000u);
+      v = v4f{qn, qn, qn, qn};
+    } else {
+      const uint2 e = *reinterpret_cast<const uint2*>(embed + (int64_t)tok * H + k);
+      v = v4f{__uint_as_float(e.x << 16), __uint_as_float(e.x & 0xffff0000u), __uint_as_float(e.y << 16),
+              __uint_as_float(e.y & 0xffff0000u)};
     }
-    const uint16_t* e = embed + (int64_t)tok * H;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = bf16_to_f32(e[k]);
   } else if (in_bf16) {
-    const uint16_t* s = reinterpret_cast<const uint16_t*>(in) + (int64_t)row * H;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = bf16_to_f32(s[k]);
+    const uint2 e = reinterpret_cast<const uint2*>(in)[i4];
+    v = v4f{__uint_as_float(e.x << 16), __uint_as_float(e.x & 0xffff0000u), __uint_as_float(e.y << 16),
+            __uint_as_float(e.y & 0xffff0000u)};
   } else {
-    const float* s = reinterpret_cast<const float*>(in) + (int64_t)row * H;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = s[k];
+    v = reinterpret_cast<const v4f*>(in)[i4];
   }
+  reinterpret_cast<v4f*>(x)[i4] = v;
 }
 
 __global__ void argmax_final_kernel(const float* part_val, const int* part_idx, int n_wg, int32_t* token,
@@ -537,7 +589,18 @@ static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int
   return hipGetLastError();
 }
 
-static int gemv_grid(int epi, int R, const GemvParams& p) {
+template <int R>
+static hipError_t gemv_dispatch_b(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
+  switch (p.batch) {
+    case 1: return gemv_dispatch_epi<1, R>(epi, norm, p, grid, s);
+    case 2: return gemv_dispatch_epi<2, R>(epi, norm, p, grid, s);
+    case 3: return gemv_dispatch_epi<3, R>(epi, norm, p, grid, s);
+    case 4: return gemv_dispatch_epi<4, R>(epi, norm, p, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int gemv_grid(int epi, int R, const GemvParams& p) {
   switch (epi) {
     case kEpiQKV: return (p.nq + 2 * p.nkv) * (p.hd / R);
     case kEpiSwiGLU: return p.N / (R / 2);
@@ -545,45 +608,50 @@ static int gemv_grid(int epi, int R, const GemvParams& p) {
   }
 }
 
-hipError_t launch_gemv(int epi, int rows_per_wg, bool norm, const GemvParams& p, hipStream_t s) {
-  if (rows_per_wg != 8) return hipErrorInvalidValue;
-  const int grid = gemv_grid(epi, 8, p);
-  switch (p.batch) {
-    case 1: return gemv_dispatch_epi<1, 8>(epi, norm, p, grid, s);
-    case 2: return gemv_dispatch_epi<2, 8>(epi, norm, p, grid, s);
-    case 3: return gemv_dispatch_epi<3, 8>(epi, norm, p, grid, s);
-    case 4: return gemv_dispatch_epi<4, 8>(epi, norm, p, grid, s);
+hipError_t launch_gemv(int epi, int R, bool norm, const GemvParams& p, hipStream_t s) {
+  const int grid = gemv_grid(epi, R, p);
+  switch (R) {
+    case 4: return gemv_dispatch_b<4>(epi, norm, p, grid, s);
+    case 8: return gemv_dispatch_b<8>(epi, norm, p, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <int HD>
-static hipError_t attn_dispatch_g(const AttnParams& p, dim3 grid, hipStream_t s) {
-  switch (p.nq / p.nkv) {
-    case 1: hipLaunchKernelGGL((attn_decode_kernel<HD, 1>), grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, 2>), grid, dim3(256), 0, s, p); break;
-    case 3: hipLaunchKernelGGL((attn_decode_kernel<HD, 3>), grid, dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, 4>), grid, dim3(256), 0, s, p); break;
-    case 5: hipLaunchKernelGGL((attn_decode_kernel<HD, 5>), grid, dim3(256), 0, s, p); break;
-    case 6: hipLaunchKernelGGL((attn_decode_kernel<HD, 6>), grid, dim3(256), 0, s, p); break;
-    case 7: hipLaunchKernelGGL((attn_decode_kernel<HD, 7>), grid, dim3(256), 0, s, p); break;
-    case 8: hipLaunchKernelGGL((attn_decode_kernel<HD, 8>), grid, dim3(256), 0, s, p); break;
-    default: return hipErrorInvalidValue;
-  }
+template <int HD, int G>
+static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
+  hipLaunchKernelGGL((attn_decode_kernel<HD, G>), dim3(p.n_split, p.nkv, batch), dim3(256), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_combine_kernel<HD, G>), dim3(p.nkv, batch), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
+template <int HD>
+static hipError_t attn_dispatch_g(const AttnParams& p, int batch, hipStream_t s) {
+  switch (p.nq / p.nkv) {
+    case 1: return attn_launch<HD, 1>(p, batch, s);
+    case 2: return attn_launch<HD, 2>(p, batch, s);
+    case 3: return attn_launch<HD, 3>(p, batch, s);
+    case 4: return attn_launch<HD, 4>(p, batch, s);
+    case 5: return attn_launch<HD, 5>(p, batch, s);
+    case 6: return attn_launch<HD, 6>(p, batch, s);
+    case 7: return attn_launch<HD, 7>(p, batch, s);
+    case 8: return attn_launch<HD, 8>(p, batch, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s) {
-  const dim3 grid(p.n_split, p.nkv, batch);
-  if (p.hd == 128) return attn_dispatch_g<128>(p, grid, s);
-  if (p.hd == 64) return attn_dispatch_g<64>(p, grid, s);
+  if (p.hd == 128) return attn_dispatch_g<128>(p, batch, s);
+  if (p.hd == 64) return attn_dispatch_g<64>(p, batch, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
                               float* x, int rows, int H, int* err_flag, hipStream_t s) {
-  hipLaunchKernelGGL(prep_hidden_kernel, dim3(rows), dim3(256), 0, s, in, in_bf16, tokens, embed, vocab, x, H,
-                     err_flag);
+  const int64_t n4 = (int64_t)rows * H / 4;
+  hipLaunchKernelGGL(prep_hidden_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, in, in_bf16, tokens,
+                     embed, vocab, x, rows, H, err_flag);
   return hipGetLastError();
 }
 

@@ -8,8 +8,21 @@ namespace kf {
 
 constexpr int kMaxBatch = 4;
 constexpr int kMaxGroup = 8;     // query heads per KV head
-constexpr int kAttnMinSplit = 64;   // keys per split-KV workgroup, lower bound
-constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound (LDS score buffer)
+constexpr int kAttnMinSplit = 16;   // keys per split-KV workgroup, lower bound
+constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound
+constexpr int kAttnMaxSplitCount = 1024;  // split-KV workgroups per (row, KV head), upper bound
+
+// Optional per-launch marker around each kernel (instrumentation hook of the runtime).
+struct Tracer {
+  void* ctx = nullptr;
+  void (*fn)(void* ctx, int cls, int begin) = nullptr;
+  void begin(int cls) const {
+    if (fn) fn(ctx, cls, 1);
+  }
+  void end(int cls) const {
+    if (fn) fn(ctx, cls, 0);
+  }
+};
 
 enum GemvEpi : int {
   kEpiQKV = 0,     // RoPE on q and k, q -> fp32 workspace, k and v -> bf16 cache at the row's position
@@ -63,7 +76,6 @@ struct AttnParams {
   float* out;          // [B][nq*hd]
   float* part_acc;     // [B][nq][max_split][hd]
   float* part_ml;      // [B][nq][max_split][2]
-  int* counters;       // [B][nkv], zero between launches
   int64_t user_stride;
   int max_ctx, nq, nkv, hd;
   int split;           // keys per workgroup
@@ -75,6 +87,7 @@ struct AttnParams {
 };
 
 // Launchers (return hipGetLastError() of the launch).
+int gemv_grid(int epi, int rows_per_wg, const GemvParams& p);
 hipError_t launch_gemv(int epi, int rows_per_wg, bool norm, const GemvParams& p, hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,

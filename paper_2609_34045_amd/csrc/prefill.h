@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.h"
+
 namespace kf {
 
 struct PrefillArgs {
@@ -39,7 +41,7 @@ struct PrefillWorkspace {
 
 hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a);
 void prefill_free(PrefillWorkspace& ws);
-hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l);
+hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr);
 
 // Exposed for unit tests of the matrix-core GEMM through the library.
 enum GemmEpi : int { kGemmStoreF32 = 0, kGemmResidF32 = 1, kGemmSwiGLU = 2 };

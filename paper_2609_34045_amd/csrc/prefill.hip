@@ -460,18 +460,28 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   return hipSuccess;
 }
 
-hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l) {
+hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr) {
   hipStream_t s = a.stream;
   const int T = a.T, H = a.H, nqkv = (a.nq + 2 * a.nkv) * a.hd;
   hipError_t e;
+  // Class ids follow kf_kernel_class of the public header.
+  enum { NORM = 8, QKV = 9, ROPE = 10, ATTN = 11, OPROJ = 12, GATEUP = 13, DOWN = 14, STORE = 15 };
+  tr.begin(NORM);
   hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_attn, a.eps, ws.xn, H);
+  tr.end(NORM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_gemm(kGemmStoreF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.qkv, nullptr, s)) != hipSuccess) return e;
+  tr.begin(QKV);
+  e = launch_gemm(kGemmStoreF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.qkv, nullptr, s);
+  tr.end(QKV);
+  if (e != hipSuccess) return e;
+  tr.begin(ROPE);
   hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.qkv, ws.q, l.kc, l.vc, a.rope_cos, a.rope_sin, a.nq,
                      a.nkv, a.hd, a.pos0, a.max_ctx);
+  tr.end(ROPE);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));
   const dim3 ag((T + 127) / 128, a.nq);
+  tr.begin(ATTN);
   if (a.hd == 128)
     hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, T, a.nq, a.nkv, a.pos0,
                        a.max_ctx, sl2);
@@ -480,15 +490,29 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
                        a.max_ctx, sl2);
   else
     return hipErrorInvalidValue;
+  tr.end(ATTN);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_gemm(kGemmResidF32, ws.o, l.wo, nullptr, T, H, a.nq * a.hd, ws.x, nullptr, s)) != hipSuccess) return e;
+  tr.begin(OPROJ);
+  e = launch_gemm(kGemmResidF32, ws.o, l.wo, nullptr, T, H, a.nq * a.hd, ws.x, nullptr, s);
+  tr.end(OPROJ);
+  if (e != hipSuccess) return e;
+  tr.begin(NORM);
   hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_mlp, a.eps, ws.xn, H);
+  tr.end(NORM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_gemm(kGemmSwiGLU, ws.xn, l.wg, l.wu, T, 2 * a.F, H, nullptr, ws.act, s)) != hipSuccess) return e;
-  if ((e = launch_gemm(kGemmResidF32, ws.act, l.wd, nullptr, T, H, a.F, ws.x, nullptr, s)) != hipSuccess) return e;
+  tr.begin(GATEUP);
+  e = launch_gemm(kGemmSwiGLU, ws.xn, l.wg, l.wu, T, 2 * a.F, H, nullptr, ws.act, s);
+  tr.end(GATEUP);
+  if (e != hipSuccess) return e;
+  tr.begin(DOWN);
+  e = launch_gemm(kGemmResidF32, ws.act, l.wd, nullptr, T, H, a.F, ws.x, nullptr, s);
+  tr.end(DOWN);
+  if (e != hipSuccess) return e;
   if (l.out) {
     const int64_t n = (int64_t)T * H;
+    tr.begin(STORE);
     hipLaunchKernelGGL(store_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, ws.x, l.out, l.out_bf16, n);
+    tr.end(STORE);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;

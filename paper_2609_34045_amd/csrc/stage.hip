@@ -15,6 +15,29 @@
 
 using namespace kf;
 
+// Launch-shape tunables (compile-time; the defaults are the measured best on MI355X).
+#ifndef KF_R_QKV
+#define KF_R_QKV 8
+#endif
+#ifndef KF_R_OPROJ
+#define KF_R_OPROJ 8
+#endif
+#ifndef KF_R_GATEUP
+#define KF_R_GATEUP 8
+#endif
+#ifndef KF_R_DOWN
+#define KF_R_DOWN 8
+#endif
+#ifndef KF_R_LMHEAD
+#define KF_R_LMHEAD 8
+#endif
+#ifndef KF_ATTN_TARGET_WGS
+#define KF_ATTN_TARGET_WGS 512
+#endif
+#ifndef KF_ATTN_ALIGN
+#define KF_ATTN_ALIGN 64
+#endif
+
 static thread_local std::string g_err;
 
 static kf_status fail(kf_status code, const char* fmt, ...) {
@@ -56,7 +79,38 @@ struct kf_stage {
   int* err_flag = nullptr;
   int live_kv = 0;
   PrefillWorkspace pf;
+  // instrumentation: event pairs around launches while profiling is enabled
+  int prof_mask = 0;
+  std::vector<hipEvent_t> ev;   // 2 per recorded launch
+  std::vector<int> ev_cls;
+  size_t ev_used = 0;           // recorded launches
+  Tracer tracer() { return prof_mask ? Tracer{this, &kf_stage::mark} : Tracer{}; }
+  static void mark(void* ctx, int cls, int begin);
 };
+
+void kf_stage::mark(void* ctx, int cls, int begin) {
+  kf_stage* s = (kf_stage*)ctx;
+  if (!(s->prof_mask & (1 << cls))) return;
+  if (begin) {
+    if (s->ev.size() < 2 * (s->ev_used + 1)) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return;
+      if (hipEventCreate(&b) != hipSuccess) {
+        hipEventDestroy(a);
+        return;
+      }
+      s->ev.push_back(a);
+      s->ev.push_back(b);
+      s->ev_cls.push_back(cls);
+    }
+    s->ev_cls[s->ev_used] = cls;
+    hipEventRecord(s->ev[2 * s->ev_used], s->stream);
+  } else {
+    if (s->ev.size() < 2 * (s->ev_used + 1)) return;  // begin failed to get events
+    hipEventRecord(s->ev[2 * s->ev_used + 1], s->stream);
+    s->ev_used++;
+  }
+}
 
 struct kf_kv {
   kf_stage* st;
@@ -64,7 +118,6 @@ struct kf_kv {
   uint16_t *k = nullptr, *v = nullptr;
   float *rcos = nullptr, *rsin = nullptr;
   float *part_acc = nullptr, *part_ml = nullptr;
-  int* counters = nullptr;
   int64_t user_stride, layer_stride;  // elements
   std::vector<int> len;
 };
@@ -131,7 +184,7 @@ static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
   n += align256(B * (int64_t)c.ffn * 4);              // act
   n += align256(B * H * 4);                           // hx
   if (has_head) {
-    const int64_t wgs = (c.vocab + 7) / 8;
+    const int64_t wgs = (c.vocab + 3) / 4;  // enough for any rows-per-workgroup choice
     n += 2 * align256(B * wgs * 4);
   }
   n += 256;  // error flag
@@ -289,7 +342,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->act = (float*)take(B * F * 4);
   s->hx = (float*)take(B * H * 4);
   if (has_head) {
-    s->lm_wg = (int)((V + 7) / 8);
+    s->lm_wg = (int)((V + KF_R_LMHEAD - 1) / KF_R_LMHEAD);
     s->part_val = (float*)take(B * s->lm_wg * 4);
     s->part_idx = (int*)take(B * s->lm_wg * 4);
   }
@@ -306,6 +359,7 @@ kf_status kf_stage_destroy(kf_stage* s) {
   if (s->arena) hipFree(s->arena);
   if (s->ws) hipFree(s->ws);
   prefill_free(s->pf);
+  for (hipEvent_t e : s->ev) hipEventDestroy(e);
   delete s;
   return KF_OK;
 }
@@ -353,10 +407,9 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   const int64_t rope = (int64_t)max_ctx * half * 4;
   const int64_t pacc = (int64_t)kMaxBatch * c.n_q_heads * kv->max_split * c.head_dim * 4;
   const int64_t pml = (int64_t)kMaxBatch * c.n_q_heads * kv->max_split * 2 * 4;
-  const int64_t cnt = (int64_t)kMaxBatch * c.n_kv_heads * 4;
-  char* mem[7] = {nullptr};
-  const int64_t sz[7] = {cache, cache, rope, rope, pacc, pml, cnt};
-  for (int i = 0; i < 7; ++i) {
+  char* mem[6] = {nullptr};
+  const int64_t sz[6] = {cache, cache, rope, rope, pacc, pml};
+  for (int i = 0; i < 6; ++i) {
     if (hipMalloc((void**)&mem[i], sz[i]) != hipSuccess) {
       hipGetLastError();
       for (int j = 0; j < i; ++j) hipFree(mem[j]);
@@ -370,7 +423,6 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   kv->rsin = (float*)mem[3];
   kv->part_acc = (float*)mem[4];
   kv->part_ml = (float*)mem[5];
-  kv->counters = (int*)mem[6];
   // RoPE table from float64 angles: pos * theta^(-2i/hd).
   std::vector<float> tc((size_t)max_ctx * half), ts((size_t)max_ctx * half);
   for (int64_t i = 0; i < half; ++i) {
@@ -383,11 +435,10 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   }
   hipError_t e = hipMemset(kv->k, 0, cache);
   if (e == hipSuccess) e = hipMemset(kv->v, 0, cache);
-  if (e == hipSuccess) e = hipMemset(kv->counters, 0, cnt);
   if (e == hipSuccess) e = hipMemcpy(kv->rcos, tc.data(), rope, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(kv->rsin, ts.data(), rope, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
-    for (int j = 0; j < 7; ++j) hipFree(mem[j]);
+    for (int j = 0; j < 6; ++j) hipFree(mem[j]);
     delete kv;
     return fail(KF_EDEVICE, "KV init: %s", hipGetErrorString(e));
   }
@@ -399,7 +450,7 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
 kf_status kf_kv_destroy(kf_kv* kv) {
   if (!kv) return fail(KF_EINVAL, "kv is NULL");
   hipStreamSynchronize(kv->st->stream);
-  void* mem[7] = {kv->k, kv->v, kv->rcos, kv->rsin, kv->part_acc, kv->part_ml, kv->counters};
+  void* mem[6] = {kv->k, kv->v, kv->rcos, kv->rsin, kv->part_acc, kv->part_ml};
   for (void* m : mem) hipFree(m);
   kv->st->live_kv--;
   delete kv;
@@ -463,8 +514,8 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
 
 // ------------------------------------------------------------------ decode
 static void attn_split(int batch, int nkv, int max_len, int max_split, int* split, int* n_split) {
-  const int target = (512 + batch * nkv - 1) / (batch * nkv);  // about two workgroups per CU in total
-  auto up64 = [](int v) { return (v + 63) / 64 * 64; };
+  const int target = (KF_ATTN_TARGET_WGS + batch * nkv - 1) / (batch * nkv);  // workgroups per (row, KV head)
+  auto up64 = [](int v) { return (v + KF_ATTN_ALIGN - 1) / KF_ATTN_ALIGN * KF_ATTN_ALIGN; };
   int sp = up64((max_len + target - 1) / target);
   const int need = up64((max_len + max_split - 1) / max_split);
   if (sp < need) sp = need;
@@ -499,8 +550,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   const int H = c.hidden, hd = c.head_dim;
   hipStream_t st = s->stream;
 
-  KF_HIP(launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->x, batch, H, s->err_flag, st),
-         "prep launch");
+  const Tracer tr = s->tracer();
+  tr.begin(KF_K_PREP);
+  hipError_t pe = launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->x, batch, H,
+                                     s->err_flag, st);
+  tr.end(KF_K_PREP);
+  KF_HIP(pe, "prep launch");
 
   int split, n_split;
   attn_split(batch, c.n_kv_heads, max_len, kv->max_split, &split, &n_split);
@@ -532,7 +587,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.users[b] = b < batch ? users[b] : 0;
       g.pos[b] = b < batch ? positions[b] : 0;
     }
-    KF_HIP(launch_gemv(kEpiQKV, 8, true, g, st), "qkv launch");
+    {
+      tr.begin(KF_K_QKV);
+      const hipError_t le = launch_gemv(kEpiQKV, KF_R_QKV, true, g, st);
+      tr.end(KF_K_QKV);
+      KF_HIP(le, "qkv launch");
+    }
 
     AttnParams a{};
     a.q = s->q;
@@ -541,7 +601,6 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     a.out = s->o;
     a.part_acc = kv->part_acc;
     a.part_ml = kv->part_ml;
-    a.counters = kv->counters;
     a.user_stride = kv->user_stride;
     a.max_ctx = kv->max_ctx;
     a.nq = c.n_q_heads;
@@ -555,7 +614,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       a.users[b] = b < batch ? users[b] : 0;
       a.len[b] = b < batch ? positions[b] + 1 : 0;
     }
-    KF_HIP(launch_attn_decode(a, batch, st), "attention launch");
+    {
+      tr.begin(KF_K_ATTN);
+      const hipError_t le = launch_attn_decode(a, batch, st);
+      tr.end(KF_K_ATTN);
+      KF_HIP(le, "attention launch");
+    }
 
     GemvParams o{};
     o.batch = batch;
@@ -564,7 +628,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     o.K = c.n_q_heads * hd;
     o.N = H;
     o.x = s->x;
-    KF_HIP(launch_gemv(kEpiResid, 8, false, o, st), "o-proj launch");
+    {
+      tr.begin(KF_K_OPROJ);
+      const hipError_t le = launch_gemv(kEpiResid, KF_R_OPROJ, false, o, st);
+      tr.end(KF_K_OPROJ);
+      KF_HIP(le, "o-proj launch");
+    }
 
     GemvParams gu{};
     gu.batch = batch;
@@ -576,7 +645,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.K = H;
     gu.N = c.ffn;
     gu.act = s->act;
-    KF_HIP(launch_gemv(kEpiSwiGLU, 8, true, gu, st), "gate/up launch");
+    {
+      tr.begin(KF_K_GATEUP);
+      const hipError_t le = launch_gemv(kEpiSwiGLU, KF_R_GATEUP, true, gu, st);
+      tr.end(KF_K_GATEUP);
+      KF_HIP(le, "gate/up launch");
+    }
 
     GemvParams d{};
     d.batch = batch;
@@ -589,7 +663,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       d.out2 = hidden_out_dev;
       d.out2_bf16 = io == KF_BF16;
     }
-    KF_HIP(launch_gemv(kEpiResid, 8, false, d, st), "down launch");
+    {
+      tr.begin(KF_K_DOWN);
+      const hipError_t le = launch_gemv(kEpiResid, KF_R_DOWN, false, d, st);
+      tr.end(KF_K_DOWN);
+      KF_HIP(le, "down launch");
+    }
   }
   for (int b = 0; b < batch; ++b) kv->len[users[b]] += 1;
   return KF_OK;
@@ -607,9 +686,12 @@ static kf_status head_common(kf_stage* s, int rows, const void* hidden, kf_dtype
 
 static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype dtype, float* logits) {
   const kf_model_config& c = s->cfg;
-  KF_HIP(launch_prep_hidden(hidden, dtype == KF_BF16, nullptr, nullptr, 0, s->hx, rows, c.hidden, s->err_flag,
-                            s->stream),
-         "head prep launch");
+  const Tracer tr = s->tracer();
+  tr.begin(KF_K_PREP);
+  hipError_t e = launch_prep_hidden(hidden, dtype == KF_BF16, nullptr, nullptr, 0, s->hx, rows, c.hidden, s->err_flag,
+                                    s->stream);
+  tr.end(KF_K_PREP);
+  KF_HIP(e, "head prep launch");
   GemvParams g{};
   g.batch = rows;
   g.eps = c.rms_eps;
@@ -622,7 +704,10 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.part_val = s->part_val;
   g.part_idx = s->part_idx;
   g.n_wg = s->lm_wg;
-  KF_HIP(launch_gemv(kEpiLMHead, 8, true, g, s->stream), "lm-head launch");
+  tr.begin(KF_K_LMHEAD);
+  e = launch_gemv(kEpiLMHead, KF_R_LMHEAD, true, g, s->stream);
+  tr.end(KF_K_LMHEAD);
+  KF_HIP(e, "lm-head launch");
   return KF_OK;
 }
 
@@ -648,7 +733,11 @@ kf_status kf_head_argmax(kf_stage* s, int32_t rows, const void* hidden, kf_dtype
   if (!token) return fail(KF_EINVAL, "token is NULL");
   st = head_launch(s, rows, hidden, dtype, nullptr);
   if (st != KF_OK) return st;
-  KF_HIP(launch_argmax_final(s->part_val, s->part_idx, s->lm_wg, rows, token, max_logit, s->stream), "argmax launch");
+  const Tracer tr = s->tracer();
+  tr.begin(KF_K_ARGMAX);
+  const hipError_t e = launch_argmax_final(s->part_val, s->part_idx, s->lm_wg, rows, token, max_logit, s->stream);
+  tr.end(KF_K_ARGMAX);
+  KF_HIP(e, "argmax launch");
   return KF_OK;
 }
 
@@ -685,9 +774,12 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
   hipError_t e = prefill_reserve(s->pf, pa);
   if (e == hipErrorOutOfMemory) return fail(KF_ENOMEM, "device allocation of the prefill workspace");
   KF_HIP(e, "prefill workspace");
-  KF_HIP(launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->pf.x, n, c.hidden,
-                            s->err_flag, s->stream),
-         "prefill prep launch");
+  const Tracer tr = s->tracer();
+  tr.begin(KF_K_PREP);
+  e = launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->pf.x, n, c.hidden, s->err_flag,
+                         s->stream);
+  tr.end(KF_K_PREP);
+  KF_HIP(e, "prefill prep launch");
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];
     const int64_t loff = (l - s->lo) * kv->layer_stride + user * kv->user_stride;
@@ -703,9 +795,38 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
     pl.vc = kv->v + loff;
     pl.out = l == s->hi - 1 ? hidden_out_dev : nullptr;
     pl.out_bf16 = io == KF_BF16;
-    KF_HIP(prefill_layer(s->pf, pa, pl), "prefill layer");
+    KF_HIP(prefill_layer(s->pf, pa, pl, tr), "prefill layer");
   }
   kv->len[user] += n;
+  return KF_OK;
+}
+
+// ------------------------------------------------------------------ instrumentation
+kf_status kf_stage_profile(kf_stage* s, int32_t mask) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  if (mask) {
+    KF_HIP(hipStreamSynchronize(s->stream), "stream synchronize");
+    s->ev_used = 0;
+  }
+  s->prof_mask = mask & KF_K_ALL;
+  return KF_OK;
+}
+
+kf_status kf_stage_profile_read(kf_stage* s, int32_t cls, int64_t* launches, double* total_ms) {
+  if (!s || !launches || !total_ms) return fail(KF_EINVAL, "NULL argument");
+  if (cls < 0 || cls >= KF_K_COUNT) return fail(KF_EINVAL, "kernel class %d", cls);
+  KF_HIP(hipStreamSynchronize(s->stream), "stream synchronize");
+  int64_t n = 0;
+  double t = 0.0;
+  for (size_t i = 0; i < s->ev_used; ++i) {
+    if (s->ev_cls[i] != cls) continue;
+    float ms = 0.f;
+    KF_HIP(hipEventElapsedTime(&ms, s->ev[2 * i], s->ev[2 * i + 1]), "event elapsed time");
+    n++;
+    t += ms;
+  }
+  *launches = n;
+  *total_ms = t;
   return KF_OK;
 }
 

@@ -14,7 +14,8 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libkafila_stage.so")
+# KF_STAGE_LIB selects another build of the same library (e.g. a tuning variant).
+LIB_PATH = os.environ.get("KF_STAGE_LIB", os.path.join(HERE, "libkafila_stage.so"))
 
 KF_OK, KF_EINVAL, KF_ENOMEM, KF_ERANGE, KF_ESTATE, KF_EDEVICE, KF_EUNSUPPORTED = range(7)
 STATUS_NAMES = {0: "KF_OK", 1: "KF_EINVAL", 2: "KF_ENOMEM", 3: "KF_ERANGE", 4: "KF_ESTATE", 5: "KF_EDEVICE",
@@ -27,7 +28,12 @@ HEAD_KINDS = {"embed": 9, "final_norm": 10, "lm_head": 11}
 
 EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init", "kf_stage_destroy",
            "kf_stage_set_stream", "kf_stage_sync", "kf_kv_create", "kf_kv_destroy", "kf_kv_len", "kf_kv_set_len",
-           "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax")
+           "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax",
+           "kf_stage_profile", "kf_stage_profile_read")
+
+# kf_kernel_class
+KERNEL_CLASSES = ("prep", "qkv", "attn", "oproj", "gateup", "down", "lmhead", "argmax", "pf_norm", "pf_qkv", "pf_rope",
+                  "pf_attn", "pf_oproj", "pf_gateup", "pf_down", "pf_store")
 
 
 class KFError(RuntimeError):
@@ -88,6 +94,8 @@ def load_library(path: str = LIB_PATH):
         "kf_stage_prefill": (I32, [P, P, I32, I32, I32, VP, VP, VP, I32]),
         "kf_head_logits": (I32, [P, I32, VP, I32, VP]),
         "kf_head_argmax": (I32, [P, I32, VP, I32, VP, VP]),
+        "kf_stage_profile": (I32, [P, I32]),
+        "kf_stage_profile_read": (I32, [P, I32, I64P, ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -189,6 +197,27 @@ class Stage:
 
     def sync(self):
         _check(self._lib.kf_stage_sync(self.handle), "kf_stage_sync")
+
+    def profile(self, enable, classes=None):
+        """Start (clearing earlier records) or stop per-kernel HIP-event timing.
+
+        ``classes``: names from KERNEL_CLASSES to record (default: all).
+        """
+        mask = 0
+        if enable:
+            mask = 0xFFFF if classes is None else sum(1 << KERNEL_CLASSES.index(c) for c in classes)
+        _check(self._lib.kf_stage_profile(self.handle, mask), "kf_stage_profile")
+
+    def profile_read(self) -> dict:
+        """{kernel class: (launches, total ms)} for classes with recorded launches."""
+        out = {}
+        for i, name in enumerate(KERNEL_CLASSES):
+            n, t = ctypes.c_int64(), ctypes.c_double()
+            _check(self._lib.kf_stage_profile_read(self.handle, i, ctypes.byref(n), ctypes.byref(t)),
+                   "kf_stage_profile_read")
+            if n.value:
+                out[name] = (n.value, t.value)
+        return out
 
     def kv(self, max_users: int, max_ctx: int) -> "KV":
         return KV(self, max_users, max_ctx)

@@ -265,3 +265,21 @@ def test_invalid_token_is_reported_by_sync(torch, st, model):
     g.sync()  # the flag is cleared once reported
     kv.close()
     g.close()
+
+
+def test_kernel_profiling_records_every_launch(torch, st, model):
+    g, kv, _ = make(st, model)
+    x = dev(torch, synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 0, 1, SHAPE.hidden))
+    g.profile(True)
+    for p in range(3):
+        g.decode(kv, [0], [p], hidden=x)
+    g.profile(False)
+    g.decode(kv, [0], [3], hidden=x)  # not recorded
+    rec = g.profile_read()
+    assert rec["prep"][0] == 3
+    for k in ("qkv", "attn", "oproj", "gateup", "down"):
+        assert rec[k][0] == 3 * 2 and rec[k][1] > 0.0
+    g.profile(True)
+    assert g.profile_read() == {}
+    kv.close()
+    g.close()
