@@ -56,7 +56,7 @@ typedef enum {
   KF_EUNSUPPORTED = 6  /* a model shape the kernels are not built for */
 } kf_status;
 
-typedef enum { KF_F32 = 0, KF_BF16 = 1 } kf_dtype; /* element type of hidden-state I/O */
+typedef enum { KF_F32 = 0, KF_BF16 = 1, KF_F16 = 2 } kf_dtype; /* element types at the boundary */
 
 typedef struct {
   int32_t n_layers;   /* layers in the whole model (the stage holds a sub-range) */
@@ -139,7 +139,9 @@ kf_status kf_stage_sync(kf_stage* stage);
 /*
  * Reserve a KV cache for max_users concurrent users of context up to max_ctx tokens
  * each, for every layer the stage holds (the declared concurrency x context of
- * Section V-C).  Layout on the device: bf16 K and V, [layer][user][kv_head][pos][hd].
+ * Section V-C).  Layout on the device: fp16 K and V, [layer][user][kv_head][pos][hd]
+ * (fp16 keeps 8x the mantissa of bf16 in the same bytes; keys and values must stay
+ * below 65504 in magnitude).
  * All user lengths start at 0.  KF_ENOMEM if the device cannot hold it.
  */
 kf_status kf_kv_create(kf_stage* stage, int32_t max_users, int32_t max_ctx, kf_kv** out);
@@ -154,16 +156,17 @@ kf_status kf_kv_set_len(kf_kv* kv, int32_t user, int32_t len);
 
 /*
  * Copy n positions of keys (already rotated) and values for one held layer and user,
- * from k_dev / v_dev laid out [n, nkv, hd] in dtype (KF_BF16 bits or KF_F32, rounded
- * to bf16 to nearest even), into positions [pos0, pos0 + n).  Does not change lengths.
+ * from k_dev / v_dev laid out [n, nkv, hd] in dtype (KF_F16 or KF_BF16 bits, or KF_F32),
+ * stored as fp16 rounded to nearest even, into positions [pos0, pos0 + n).  Does not
+ * change lengths.
  * KF_ERANGE if pos0 + n > max_ctx.  Enqueued on the stage's stream.
  */
 kf_status kf_kv_write(kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, const void* k_dev,
                       const void* v_dev, kf_dtype dtype);
 
-/* Copy positions [pos0, pos0 + n) of one layer and user out as bf16 bits, [n, nkv, hd]. */
-kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, uint16_t* k_dev,
-                     uint16_t* v_dev);
+/* Copy positions [pos0, pos0 + n) of one layer and user out as fp32 (exact), [n, nkv, hd]. */
+kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, float* k_dev,
+                     float* v_dev);
 
 /*
  * Forward one token for each of `batch` (1..KF_MAX_BATCH) users (decode).
@@ -185,7 +188,8 @@ kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32
  * Forward a chunk of n_tokens consecutive tokens of one user starting at pos0 (prefill).
  * pos0 must equal the user's length and pos0 + n_tokens <= max_ctx.  Token i attends
  * slots 0..pos0+i.  tokens_dev int32 [n] or hidden_in_dev [n, H]; hidden_out_dev [n, H].
- * Dense products run on the matrix cores with bf16 operands and fp32 accumulation.
+ * Dense products run on the matrix cores with fp16 operands (bf16 weights converted
+ * exactly while staged) and fp32 accumulation.
  * On success the user's length advances by n_tokens.
  */
 kf_status kf_stage_prefill(kf_stage* stage, kf_kv* kv, int32_t user, int32_t pos0, int32_t n_tokens,

@@ -32,17 +32,32 @@ layer) and a separately written scalar brute force.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 F64 = np.float64
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
-    """Exact value of bf16 bit patterns (uint16) as float64."""
+    """Exact value of bf16 bit patterns (uint16) as float64 (row blocks widened on threads)."""
     bits = np.asarray(bits)
     if bits.dtype != np.uint16:
         raise TypeError("bf16 tensors are passed as uint16 bit patterns")
-    return (bits.astype(np.uint32) << 16).view(np.float32).astype(F64)
+    if bits.size < (1 << 22) or bits.ndim == 0:
+        return (bits.astype(np.uint32) << 16).view(np.float32).astype(F64)
+    out = np.empty(bits.shape, dtype=F64)
+    flat_in, flat_out = bits.reshape(-1), out.reshape(-1)
+    step = 1 << 21
+
+    def one(i):
+        out_blk = flat_out[i:i + step]
+        out_blk[:] = (flat_in[i:i + step].astype(np.uint32) << 16).view(np.float32)
+
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(one, range(0, flat_in.size, step)))
+    return out
 
 
 def rms_norm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -91,17 +106,18 @@ def attention_rows(q: np.ndarray, keys: list, values: list, n_kv_heads: int) -> 
     """GQA attention for a list of query rows.
 
     q: [N, n_q, hd]; keys[n], values[n]: [len_n, n_kv, hd] (the keys row n may see).
-    Returns [N, n_q * hd].
+    Query head h reads KV head h // (n_q / n_kv); the query heads of one KV head
+    are scored together.  Returns [N, n_q * hd].
     """
     N, nq, hd = q.shape
     group = nq // n_kv_heads
     out = np.empty((N, nq, hd), dtype=F64)
     for n in range(N):
         K, V = keys[n], values[n]
-        for h in range(nq):
-            g = h // group
-            s = K[:, g, :] @ q[n, h] / np.sqrt(F64(hd))
-            out[n, h] = softmax(s) @ V[:, g, :]
+        for g in range(n_kv_heads):
+            hs = slice(g * group, (g + 1) * group)
+            s = (q[n, hs] @ K[:, g, :].T) / np.sqrt(F64(hd))  # [group, len]
+            out[n, hs] = softmax(s) @ V[:, g, :]
     return out.reshape(N, nq * hd)
 
 

@@ -14,7 +14,7 @@
 //   * SwiGLU runs in the gate/up GEMV's epilogue; the residual add in the
 //     O and down GEMVs' epilogues.
 //   * The LM-head GEMV reduces (max, lowest index) per workgroup.
-// Attention is split-KV over a bf16 cache, [user][kv_head][pos][hd]; each
+// Attention is split-KV over an fp16 cache, [user][kv_head][pos][hd]; each
 // workgroup serves all query heads of one KV head, and a second small kernel
 // merges the splits of each (row, KV head) (online-softmax rescaling).
 #include "kernels.h"
@@ -38,6 +38,19 @@ __device__ __forceinline__ void bf16x8(const v4u w, float (&f)[8]) {
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f8 __attribute__((ext_vector_type(8)));
+
+// 8 fp16 (16 bytes) to fp32.
+__device__ __forceinline__ void f16x8(const v4u w, float (&f)[8]) {
+  const f8 v = __builtin_convertvector(__builtin_bit_cast(h8, w), f8);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = v[i];
+}
+
+// fp32 to fp16 bits, round to nearest even.
+__device__ __forceinline__ uint16_t f32_to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
 
 // Round to nearest even; NaN stays NaN.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
@@ -221,13 +234,13 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
           q[i + half] = z2;
         } else {
           uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq) * p.max_ctx + pos) * hd;
-          k[i] = f32_to_bf16(z1);
-          k[i + half] = f32_to_bf16(z2);
+          k[i] = f32_to_f16(z1);
+          k[i + half] = f32_to_f16(z2);
         }
       } else {
         uint16_t* v = p.vc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq - p.nkv) * p.max_ctx + pos) * hd;
-        v[i] = f32_to_bf16(y1);
-        v[i + half] = f32_to_bf16(y2);
+        v[i] = f32_to_f16(y1);
+        v[i + half] = f32_to_f16(y2);
       }
     }
   } else if (EPI == kEpiResid) {
@@ -337,7 +350,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       float kf[8];
-      bf16x8(kw[j], kf);
+      f16x8(kw[j], kf);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         float a = 0.f;
@@ -375,7 +388,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       float vf[8];
-      bf16x8(vw[j], vf);
+      f16x8(vw[j], vf);
 #pragma unroll
       for (int h = 0; h < G; ++h)
 #pragma unroll
@@ -543,8 +556,8 @@ __global__ void store_hidden_kernel(const float* x, void* out, int out_bf16, int
   else reinterpret_cast<float*>(out)[i] = x[i];
 }
 
-// src [n][nkv][hd] -> dst [kv_head][max_ctx][hd] (dst already offset to the first position)
-__global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const void* sk, const void* sv, int src_bf16, int n,
+// src [n][nkv][hd] -> dst [kv_head][max_ctx][hd] (dst already offset to the first position), stored as fp16.
+__global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const void* sk, const void* sv, int src_type, int n,
                                 int nkv, int hd, int max_ctx) {
   const int64_t total = (int64_t)n * nkv * hd;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -553,17 +566,20 @@ __global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const void* sk, cons
   const int g = (int)((i / hd) % nkv);
   const int t = (int)(i / ((int64_t)hd * nkv));
   const int64_t at = ((int64_t)g * max_ctx + t) * hd + d;
-  if (src_bf16) {
+  if (src_type == 2) {
     dk[at] = reinterpret_cast<const uint16_t*>(sk)[i];
     dv[at] = reinterpret_cast<const uint16_t*>(sv)[i];
+  } else if (src_type == 1) {
+    dk[at] = f32_to_f16(bf16_to_f32(reinterpret_cast<const uint16_t*>(sk)[i]));
+    dv[at] = f32_to_f16(bf16_to_f32(reinterpret_cast<const uint16_t*>(sv)[i]));
   } else {
-    dk[at] = f32_to_bf16(reinterpret_cast<const float*>(sk)[i]);
-    dv[at] = f32_to_bf16(reinterpret_cast<const float*>(sv)[i]);
+    dk[at] = f32_to_f16(reinterpret_cast<const float*>(sk)[i]);
+    dv[at] = f32_to_f16(reinterpret_cast<const float*>(sv)[i]);
   }
 }
 
-__global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, uint16_t* dk, uint16_t* dv, int n, int nkv,
-                               int hd, int max_ctx) {
+__global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, float* dk, float* dv, int n, int nkv, int hd,
+                               int max_ctx) {
   const int64_t total = (int64_t)n * nkv * hd;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= total) return;
@@ -571,8 +587,8 @@ __global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, uint16_t*
   const int g = (int)((i / hd) % nkv);
   const int t = (int)(i / ((int64_t)hd * nkv));
   const int64_t at = ((int64_t)g * max_ctx + t) * hd + d;
-  dk[i] = sk[at];
-  dv[i] = sv[at];
+  dk[i] = (float)__builtin_bit_cast(_Float16, sk[at]);
+  dv[i] = (float)__builtin_bit_cast(_Float16, sv[at]);
 }
 
 // ------------------------------------------------------------------ launchers
@@ -667,16 +683,16 @@ hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t 
   return hipGetLastError();
 }
 
-hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_bf16,
+hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_type,
                            int n, int nkv, int hd, int max_ctx, hipStream_t s) {
   const int64_t total = (int64_t)n * nkv * hd;
   hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, dst_k, dst_v, src_k,
-                     src_v, src_bf16, n, nkv, hd, max_ctx);
+                     src_v, src_type, n, nkv, hd, max_ctx);
   return hipGetLastError();
 }
 
-hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k, uint16_t* dst_v, int n,
-                          int nkv, int hd, int max_ctx, hipStream_t s) {
+hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, float* dst_k, float* dst_v, int n, int nkv,
+                          int hd, int max_ctx, hipStream_t s) {
   const int64_t total = (int64_t)n * nkv * hd;
   hipLaunchKernelGGL(kv_read_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, src_k, src_v, dst_k,
                      dst_v, n, nkv, hd, max_ctx);

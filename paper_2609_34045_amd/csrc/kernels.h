@@ -49,7 +49,7 @@ struct GemvParams {
 
   // kEpiQKV
   float* q;            // [B][nq*hd]
-  uint16_t* kc;        // K cache of this layer: [user][kv_head][pos][hd]
+  uint16_t* kc;        // K cache of this layer (fp16 bits): [user][kv_head][pos][hd]
   uint16_t* vc;
   int64_t user_stride; // elements between users in kc / vc
   int max_ctx;
@@ -71,7 +71,7 @@ struct GemvParams {
 
 struct AttnParams {
   const float* q;      // [B][nq*hd] rotated queries
-  const uint16_t* kc;  // layer base, [user][kv_head][pos][hd]
+  const uint16_t* kc;  // layer base (fp16 bits), [user][kv_head][pos][hd]
   const uint16_t* vc;
   float* out;          // [B][nq*hd]
   float* part_acc;     // [B][nq][max_split][hd]
@@ -95,9 +95,10 @@ hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
                                float* max_logit, hipStream_t s);
 hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t n, hipStream_t s);
-hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_bf16,
+// src_type: 0 fp32, 1 bf16, 2 fp16 (the kf_dtype values)
+hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_type,
                            int n, int nkv, int hd, int max_ctx, hipStream_t s);
-hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, uint16_t* dst_k, uint16_t* dst_v, int n,
-                          int nkv, int hd, int max_ctx, hipStream_t s);
+hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, float* dst_k, float* dst_v, int n, int nkv,
+                          int hd, int max_ctx, hipStream_t s);
 
 }  // namespace kf

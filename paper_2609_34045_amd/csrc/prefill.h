@@ -21,7 +21,7 @@ struct PrefillArgs {
 
 struct PrefillLayer {
   const uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
-  uint16_t* kc;  // K cache of this layer and user: [kv_head][pos][hd]
+  uint16_t* kc;  // K cache of this layer and user (fp16 bits): [kv_head][pos][hd]
   uint16_t* vc;
   void* out;     // hidden output after this layer (last layer only), else NULL
   int out_bf16;
@@ -32,11 +32,11 @@ struct PrefillWorkspace {
   int cap_T = 0;
   char* mem = nullptr;
   float* x = nullptr;      // [T][H] residual stream
-  uint16_t* xn = nullptr;  // [T][H] normalised, bf16
+  uint16_t* xn = nullptr;  // [T][H] normalised, fp16
   float* qkv = nullptr;    // [T][(nq+2nkv) hd] raw projections
-  uint16_t* q = nullptr;   // [T][nq][hd] rotated queries, bf16
-  uint16_t* o = nullptr;   // [T][nq hd] attention output, bf16
-  uint16_t* act = nullptr; // [T][F] SwiGLU output, bf16
+  uint16_t* q = nullptr;   // [T][nq][hd] rotated queries, fp16
+  uint16_t* o = nullptr;   // [T][nq hd] attention output, fp16
+  uint16_t* act = nullptr; // [T][F] SwiGLU output, fp16
 };
 
 hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a);

@@ -1,13 +1,17 @@
 // Chunked-prefill kernels for gfx950: a chunk of T tokens of one user.
 //
 // With T in the hundreds the projections are dense contractions,
-// [T, K] x [N, K]^T, and run on the matrix cores (v_mfma_f32_32x32x16_bf16:
-// bf16 operands, fp32 accumulation).  Both operands are K-contiguous in HBM
-// (activations row-major, weights [out, in]), so every MFMA operand fragment
-// is one 16-byte run of a row.  Attention is causal flash attention over the
-// cache [0, pos0) plus the chunk, also on the matrix cores.
+// [T, K] x [N, K]^T, and run on the matrix cores (v_mfma_f32_32x32x16_f16:
+// fp16 operands, fp32 accumulation).  Activations are kept in fp16 (8x the
+// mantissa of bf16 at the same width); bf16 weights are converted to fp16 as
+// they are staged into LDS, which is exact for every bf16 value of magnitude
+// in [2^-14, 65504] (smaller ones keep an absolute error below 2^-25).  Both
+// operands are K-contiguous in HBM (activations row-major, weights
+// [out, in]), so every MFMA operand fragment is one 16-byte run of a row.
+// Attention is causal flash attention over the fp16 cache [0, pos0) plus the
+// chunk, also on the matrix cores.
 //
-// Operand fragment layout of v_mfma_f32_32x32x16_bf16 (lane l of 64):
+// Operand fragment layout of v_mfma_f32_32x32x16_f16 (lane l of 64):
 //   A: row l%32, k = 8*(l/32) .. +7      B: column l%32, k = 8*(l/32) .. +7
 //   D: element v (0..15) at row 8*(v/4) + 4*(l/32) + v%4, column l%32
 #include <cmath>
@@ -20,7 +24,9 @@ namespace kf {
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef unsigned v2u __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ uint16_t to_bf16(float f) {
@@ -30,15 +36,23 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 __device__ __forceinline__ float from_bf16(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ uint16_t to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(v4u v) {
-  bf16x8 r;
-  __builtin_memcpy(&r, &v, 16);
-  return r;
+// Two fp32 to packed fp16 (round to nearest even).
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, h2));
+}
+
+// 8 bf16 (16 bytes) to 8 fp16 (16 bytes).
+__device__ __forceinline__ v4u bf16x8_to_f16x8(v4u w) {
+  return v4u{pack_f16(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u)),
+             pack_f16(__uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)),
+             pack_f16(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xffff0000u)),
+             pack_f16(__uint_as_float(w.w << 16), __uint_as_float(w.w & 0xffff0000u))};
 }
 
 __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b), c, 0, 0, 0);
 }
 
 // ------------------------------------------------------------------ GEMM
@@ -50,12 +64,12 @@ constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;  // +16 B row pad again
 }
 
 struct GemmParams {
-  const uint16_t* A;   // [M][K]
-  const uint16_t* W;   // [N][K]   (SwiGLU: gate rows)
+  const uint16_t* A;   // [M][K] fp16 activations
+  const uint16_t* W;   // [N][K] bf16 weights (SwiGLU: gate rows)
   const uint16_t* W2;  // SwiGLU: up rows
   int M, N, K;         // SwiGLU: N counts gate and up rows together (2F)
   float* C;            // [M][N] fp32 (store or residual add)
-  uint16_t* Cb;        // SwiGLU: [M][N/2] bf16
+  uint16_t* Cb;        // SwiGLU: [M][N/2] fp16
 };
 
 template <int EPI>
@@ -123,7 +137,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       *reinterpret_cast<v4u*>(&As[buf][lrow[i] * LDK + lcol[i]]) = ra[i];
-      *reinterpret_cast<v4u*>(&Ws[buf][lrow[i] * LDK + lcol[i]]) = rw[i];
+      *reinterpret_cast<v4u*>(&Ws[buf][lrow[i] * LDK + lcol[i]]) = bf16x8_to_f16x8(rw[i]);
     }
   };
 
@@ -164,7 +178,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
         const int j = (n0 >> 1) + wn * 32 + col_in;
         if (j < (p.N >> 1)) {
           const float g = acc[i][0][v], u = acc[i][1][v];
-          p.Cb[(int64_t)row * (p.N >> 1) + j] = to_bf16(g / (1.0f + expf(-g)) * u);
+          p.Cb[(int64_t)row * (p.N >> 1) + j] = to_f16(g / (1.0f + expf(-g)) * u);
         }
       } else {
 #pragma unroll
@@ -198,8 +212,8 @@ hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ row RMSNorm -> bf16
-__global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const float* x, const uint16_t* g, float eps,
+// ------------------------------------------------------------------ row RMSNorm -> fp16
+__global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(const float* x, const uint16_t* g, float eps,
                                                                 uint16_t* out, int H) {
   const int row = blockIdx.x, tid = threadIdx.x;
   const float* xr = x + (int64_t)row * H;
@@ -212,11 +226,11 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_bf16_kernel(const float* x, 
   __syncthreads();
   const float rs = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)H + eps);
   uint16_t* o = out + (int64_t)row * H;
-  for (int k = tid; k < H; k += 256) o[k] = to_bf16(xr[k] * rs * from_bf16(g[k]));
+  for (int k = tid; k < H; k += 256) o[k] = to_f16(xr[k] * rs * from_bf16(g[k]));
 }
 
 // ------------------------------------------------------------------ RoPE + KV append
-// qkv [T][(nq+2nkv) hd] fp32 -> q [T][nq][hd] bf16 (rotated), K/V cache at pos0 + i (bf16).
+// qkv [T][(nq+2nkv) hd] fp32 -> q [T][nq][hd] fp16 (rotated), K/V cache at pos0 + i (fp16).
 __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, uint16_t* q, uint16_t* kc, uint16_t* vc,
                                                       const float* cosT, const float* sinT, int nq, int nkv, int hd,
                                                       int pos0, int max_ctx) {
@@ -231,17 +245,17 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, uint16_t
       const float z1 = a * c - b * s, z2 = b * c + a * s;
       if (h < nq) {
         uint16_t* dst = q + ((int64_t)i * nq + h) * hd;
-        dst[j] = to_bf16(z1);
-        dst[j + half] = to_bf16(z2);
+        dst[j] = to_f16(z1);
+        dst[j + half] = to_f16(z2);
       } else {
         uint16_t* dst = kc + ((int64_t)(h - nq) * max_ctx + pos) * hd;
-        dst[j] = to_bf16(z1);
-        dst[j + half] = to_bf16(z2);
+        dst[j] = to_f16(z1);
+        dst[j + half] = to_f16(z2);
       }
     } else {
       uint16_t* dst = vc + ((int64_t)(h - nq - nkv) * max_ctx + pos) * hd;
-      dst[j] = to_bf16(a);
-      dst[j + half] = to_bf16(b);
+      dst[j] = to_f16(a);
+      dst[j + half] = to_f16(b);
     }
   }
 }
@@ -258,8 +272,8 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
                                                            const uint16_t* vc, uint16_t* out, int T, int nq, int nkv,
                                                            int pos0, int max_ctx, float scale_log2) {
   constexpr int KB = 32;            // keys per block
-  constexpr int LDK = HD + 8;       // K tile row stride (bf16)
-  constexpr int LDV = KB + 4;       // V^T tile row stride (bf16), keeps 8-byte alignment
+  constexpr int LDK = HD + 8;       // K tile row stride (fp16 elements)
+  constexpr int LDV = KB + 4;       // V^T tile row stride (fp16 elements), keeps 8-byte alignment
   constexpr int DB = HD / 32;       // 32-row d-blocks of O^T
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KB * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
@@ -383,7 +397,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
       uint32_t w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        w[e] = (uint32_t)to_bf16(st[8 * sidx + 2 * e]) | ((uint32_t)to_bf16(st[8 * sidx + 2 * e + 1]) << 16);
+        w[e] = pack_f16(st[8 * sidx + 2 * e], st[8 * sidx + 2 * e + 1]);
       pf[sidx] = v4u{w[0], w[1], w[2], w[3]};
     }
     // V^T fragments with the same key order: keys 16 sidx + 4 half_sel + {0..3} and 16 sidx + 8 + 4 half_sel + {0..3}.
@@ -407,7 +421,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = to_bf16(o[d][v] * inv);
+      for (int v = 0; v < 16; ++v) dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = to_f16(o[d][v] * inv);
   }
 }
 
@@ -467,7 +481,7 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   // Class ids follow kf_kernel_class of the public header.
   enum { NORM = 8, QKV = 9, ROPE = 10, ATTN = 11, OPROJ = 12, GATEUP = 13, DOWN = 14, STORE = 15 };
   tr.begin(NORM);
-  hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_attn, a.eps, ws.xn, H);
+  hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_attn, a.eps, ws.xn, H);
   tr.end(NORM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   tr.begin(QKV);
@@ -497,7 +511,7 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   tr.end(OPROJ);
   if (e != hipSuccess) return e;
   tr.begin(NORM);
-  hipLaunchKernelGGL(rmsnorm_rows_bf16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_mlp, a.eps, ws.xn, H);
+  hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_mlp, a.eps, ws.xn, H);
   tr.end(NORM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   tr.begin(GATEUP);

@@ -488,17 +488,17 @@ kf_status kf_kv_write(kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int3
   if (st != KF_OK) return st;
   if (n == 0) return KF_OK;
   if (!k_dev || !v_dev) return fail(KF_EINVAL, "NULL source");
-  if (dtype != KF_F32 && dtype != KF_BF16) return fail(KF_EINVAL, "dtype");
+  if (dtype != KF_F32 && dtype != KF_BF16 && dtype != KF_F16) return fail(KF_EINVAL, "dtype");
   const kf_model_config& c = kv->st->cfg;
   const int64_t off = (layer - kv->st->lo) * kv->layer_stride + user * kv->user_stride + (int64_t)pos0 * c.head_dim;
-  KF_HIP(launch_kv_write(kv->k + off, kv->v + off, k_dev, v_dev, dtype == KF_BF16, n, c.n_kv_heads, c.head_dim,
+  KF_HIP(launch_kv_write(kv->k + off, kv->v + off, k_dev, v_dev, (int)dtype, n, c.n_kv_heads, c.head_dim,
                          kv->max_ctx, kv->st->stream),
          "kv_write launch");
   return KF_OK;
 }
 
-kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, uint16_t* k_dev,
-                     uint16_t* v_dev) {
+kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, float* k_dev,
+                     float* v_dev) {
   if (!kv) return fail(KF_EINVAL, "kv is NULL");
   kf_status st = kv_slice_check(kv, layer, user, pos0, n);
   if (st != KF_OK) return st;

@@ -20,7 +20,7 @@ LIB_PATH = os.environ.get("KF_STAGE_LIB", os.path.join(HERE, "libkafila_stage.so
 KF_OK, KF_EINVAL, KF_ENOMEM, KF_ERANGE, KF_ESTATE, KF_EDEVICE, KF_EUNSUPPORTED = range(7)
 STATUS_NAMES = {0: "KF_OK", 1: "KF_EINVAL", 2: "KF_ENOMEM", 3: "KF_ERANGE", 4: "KF_ESTATE", 5: "KF_EDEVICE",
                 6: "KF_EUNSUPPORTED"}
-KF_F32, KF_BF16 = 0, 1
+KF_F32, KF_BF16, KF_F16 = 0, 1, 2
 MAX_BATCH = 4
 
 LAYER_KINDS = {"attn_norm": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "mlp_norm": 5, "wg": 6, "wu": 7, "wd": 8}
@@ -321,13 +321,17 @@ class KV:
         _check(self._lib.kf_kv_set_len(self.handle, user, n), "kf_kv_set_len")
 
     def write(self, layer: int, user: int, pos0: int, k, v):
-        """k, v: device tensors [n, nkv, hd], bfloat16 (or int16/uint16 bf16 bits) or float32."""
+        """k, v: device tensors [n, nkv, hd]: float32, float16, bfloat16, or int16 holding bf16 bits."""
         import torch
         _require_device(k, "k")
         _require_device(v, "v")
+        if k.dtype != v.dtype:
+            raise TypeError("k and v dtypes differ")
         if k.dtype == torch.float32:
             dt = KF_F32
-        elif k.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        elif k.dtype == torch.float16:
+            dt = KF_F16
+        elif k.dtype in (torch.bfloat16, torch.int16):
             dt = KF_BF16
         else:
             raise TypeError("k/v dtype")
@@ -335,10 +339,10 @@ class KV:
                "kf_kv_write")
 
     def read(self, layer: int, user: int, pos0: int, n: int):
-        """Returns (k, v) as bfloat16 device tensors [n, nkv, hd]."""
+        """Returns (k, v) as float32 device tensors [n, nkv, hd] (exact copies of the fp16 cache)."""
         import torch
         s = self.stage.shape
-        k = torch.empty((n, s.n_kv_heads, s.head_dim), dtype=torch.bfloat16, device="cuda")
+        k = torch.empty((n, s.n_kv_heads, s.head_dim), dtype=torch.float32, device="cuda")
         v = torch.empty_like(k)
         _check(self._lib.kf_kv_read(self.handle, layer, user, pos0, n, _ptr(k), _ptr(v)), "kf_kv_read")
         return k, v
