@@ -92,6 +92,26 @@ struct Butterfly<1, 0> {
 
 constexpr int ilog2(int n) { return n <= 1 ? 0 : 1 + ilog2(n / 2); }
 
+// Reductions over lane groups of 8 or 16 (one half or one whole 16-lane DPP row),
+// result in every lane of the group.  DPP operands feed the ALU directly, without
+// the LDS round trip of a lane shuffle: quad_perm swaps lanes 1 and 2 apart, then
+// the half-row and row mirrors pair each lane with one in the other quad / half.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 8 || N == 16, "group of 8 or 16 lanes");
+  v += dpp<kDppXor1>(v);
+  v += dpp<kDppXor2>(v);
+  v += dpp<kDppHalfMirror>(v);
+  if (N == 16) v += dpp<kDppMirror>(v);
+  return v;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
@@ -294,12 +314,17 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
 // and V of a chunk are loaded together, so one memory latency covers both); the
 // four waves' (max, sum, acc) states are merged through LDS and written as the
 // split's partial.
+#ifndef KF_ATTN_J
+#define KF_ATTN_J 4
+#endif
+
 template <int HD, int G>
 __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
-  constexpr int LPK = HD / 8;      // lanes per key
-  constexpr int KPW = 64 / LPK;    // keys per wave per pass
-  constexpr int J = 4;             // keys per lane group per chunk
+  constexpr int LPK = HD / 8;      // lanes per key (one 16-byte slice each)
+  constexpr int KPW = 64 / LPK;    // key groups per wave
+  constexpr int J = KF_ATTN_J;     // keys per key group per chunk
   constexpr int CH = KPW * J;      // keys per wave chunk
+  constexpr int SUB = 4 * KPW;     // (wave, key group) partial states per workgroup
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int len = p.len[b];
@@ -307,14 +332,41 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
   const int hq0 = g * G;
 
-  __shared__ float wacc[4][G][HD];
-  __shared__ float wml[4][G][2];
+  __shared__ float sacc[SUB][G][HD];
+  __shared__ float sl[SUB][G];
+  __shared__ float sm[4][G];
 
   const int64_t head_off = (int64_t)p.users[b] * p.user_stride + (int64_t)g * p.max_ctx * HD;
   const uint16_t* kb = p.kc + head_off + (int64_t)s0 * HD;
   const uint16_t* vb = p.vc + head_off + (int64_t)s0 * HD;
   const int d0 = (lane % LPK) * 8;
   const int kgrp = lane / LPK;
+
+  float acc[G][8], m_run[G], l_run[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m_run[h] = -INFINITY;
+    l_run[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[h][i] = 0.f;
+  }
+
+  // The first chunk's K and V are requested before the query, which the
+  // previous kernel has just written.
+  int c0 = wave * CH;
+  v4u kw[J], vw[J];
+  bool ok[J];
+  auto load_chunk = [&](int c) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int t = c + j * KPW + kgrp;
+      ok[j] = t < nk;
+      const int tt = ok[j] ? t : 0;
+      kw[j] = *reinterpret_cast<const v4u*>(kb + (int64_t)tt * HD + d0);
+      vw[j] = *reinterpret_cast<const v4u*>(vb + (int64_t)tt * HD + d0);
+    }
+  };
+  if (c0 < nk) load_chunk(c0);
 
   float qv[G][8];
 #pragma unroll
@@ -326,26 +378,8 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     qv[h][4] = hi.x * p.scale_log2; qv[h][5] = hi.y * p.scale_log2;
     qv[h][6] = hi.z * p.scale_log2; qv[h][7] = hi.w * p.scale_log2;
   }
-  float acc[G][8], m_run[G], l_run[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_run[h] = -INFINITY;
-    l_run[h] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[h][i] = 0.f;
-  }
 
-  for (int c0 = wave * CH; c0 < nk; c0 += 4 * CH) {
-    v4u kw[J], vw[J];
-    bool ok[J];
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      const int t = c0 + j * KPW + kgrp;
-      ok[j] = t < nk;
-      const int tt = ok[j] ? t : 0;
-      kw[j] = *reinterpret_cast<const v4u*>(kb + (int64_t)tt * HD + d0);
-      vw[j] = *reinterpret_cast<const v4u*>(vb + (int64_t)tt * HD + d0);
-    }
+  for (; c0 < nk; c0 += 4 * CH) {
     float sc[J][G];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
@@ -356,23 +390,26 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
         float a = 0.f;
 #pragma unroll
         for (int i = 0; i < 8; ++i) a += qv[h][i] * kf[i];
-        sc[j][h] = a;
+        sc[j][h] = group_sum<LPK>(a);
       }
     }
+    float vf[J][8];
 #pragma unroll
-    for (int o = LPK / 2; o >= 1; o >>= 1)
+    for (int j = 0; j < J; ++j) f16x8(vw[j], vf[j]);
+    bool okc[J];
 #pragma unroll
-      for (int j = 0; j < J; ++j)
-#pragma unroll
-        for (int h = 0; h < G; ++h) sc[j][h] += __shfl_xor(sc[j][h], o);
+    for (int j = 0; j < J; ++j) okc[j] = ok[j];
+    if (c0 + 4 * CH < nk) load_chunk(c0 + 4 * CH);  // next chunk in flight during this one's math
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       float mc = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < J; ++j) mc = ok[j] ? fmaxf(mc, sc[j][h]) : mc;
-#pragma unroll
-      for (int o = LPK; o < 64; o <<= 1) mc = fmaxf(mc, __shfl_xor(mc, o));
-      const float m_new = fmaxf(m_run[h], mc);  // finite: the chunk has at least one valid key
+      for (int j = 0; j < J; ++j) mc = okc[j] ? fmaxf(mc, sc[j][h]) : mc;
+      // max over the wave's key groups (a chunk has at least one valid key, so mc is finite)
+      if (LPK == 8) mc = fmaxf(mc, dpp<kDppMirror>(mc));
+      mc = fmaxf(mc, __shfl_xor(mc, 16));
+      mc = fmaxf(mc, __shfl_xor(mc, 32));
+      const float m_new = fmaxf(m_run[h], mc);
       const float alpha = exp2f(m_run[h] - m_new);
       m_run[h] = m_new;
       l_run[h] *= alpha;
@@ -380,59 +417,47 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
       for (int i = 0; i < 8; ++i) acc[h][i] *= alpha;
 #pragma unroll
       for (int j = 0; j < J; ++j) {
-        const float pj = ok[j] ? exp2f(sc[j][h] - m_new) : 0.f;
-        sc[j][h] = pj;
+        const float pj = okc[j] ? exp2f(sc[j][h] - m_new) : 0.f;
         l_run[h] += pj;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[h][i] += pj * vf[j][i];
       }
     }
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      float vf[8];
-      f16x8(vw[j], vf);
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[h][i] += sc[j][h] * vf[i];
-    }
   }
-  // Sum over the key groups of the wave (same dims, distinct keys, same running max).
+
+  // Every lane's (key group, 8 dims) state goes to LDS; the running max is wave-uniform.
+  const int sub = wave * KPW + kgrp;
 #pragma unroll
-  for (int o = LPK; o < 64; o <<= 1) {
+  for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      l_run[h] += __shfl_xor(l_run[h], o);
+    for (int i = 0; i < 8; ++i) sacc[sub][h][d0 + i] = acc[h][i];
+  if ((lane % LPK) == 0) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[h][i] += __shfl_xor(acc[h][i], o);
-    }
-  }
-  if (lane < LPK) {
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) wacc[wave][h][d0 + i] = acc[h][i];
+    for (int h = 0; h < G; ++h) sl[sub][h] = l_run[h];
   }
   if (lane == 0) {
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      wml[wave][h][0] = m_run[h];
-      wml[wave][h][1] = l_run[h];
-    }
+    for (int h = 0; h < G; ++h) sm[wave][h] = m_run[h];
   }
   __syncthreads();
 
-  // Merge the four waves into this split's partial.
+  // Merge the workgroup's states into this split's partial (max, sum, unnormalised acc).
   for (int e = tid; e < G * HD; e += 256) {
     const int h = e / HD, d = e % HD;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
-      if (wml[w][h][1] > 0.f) M = fmaxf(M, wml[w][h][0]);
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][h]);
     float v = 0.f, l = 0.f;
+    if (M != -INFINITY) {
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float sw = wml[w][h][1] > 0.f ? exp2f(wml[w][h][0] - M) : 0.f;
-      v += sw * wacc[w][h][d];
-      l += sw * wml[w][h][1];
+      for (int w = 0; w < 4; ++w) {
+        const float sw = exp2f(sm[w][h] - M);  // 0 for a wave without keys (its max is -inf)
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+          v += sw * sacc[w * KPW + k][h][d];
+          l += sw * sl[w * KPW + k][h];
+        }
+      }
     }
     const int64_t row = ((int64_t)b * p.nq + hq0 + h) * p.max_split + split;
     p.part_acc[row * HD + d] = v;
@@ -441,7 +466,6 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
       p.part_ml[row * 2 + 1] = l;
     }
   }
-
 }
 
 // Merge of the split-KV partials of one (row, KV head): all G query heads, all hd dims.
@@ -456,6 +480,19 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams p) {
   const int hq0 = g * G, ns = p.n_split;
   __shared__ float wsplit[G][kAttnMaxSplitCount];
   __shared__ float inv_l[G];
+  // The first PRE splits of this thread's partial rows are loaded before the
+  // weights are known, so both memory round trips overlap.
+  constexpr int PRE = 8, ITEMS = (G * HD / 4 + 255) / 256;
+  v4f pre[ITEMS][PRE];
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    const int e = tid + 256 * it;
+    const int h = e / (HD / 4), d4 = e % (HD / 4);
+    const v4f* src = reinterpret_cast<const v4f*>(p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD) + d4;
+#pragma unroll
+    for (int sp = 0; sp < PRE; ++sp)
+      pre[it][sp] = (e < G * HD / 4 && sp < ns) ? src[(int64_t)sp * (HD / 4)] : v4f{0.f, 0.f, 0.f, 0.f};
+  }
   for (int h = wave; h < G; h += 4) {
     const float* mlh = p.part_ml + ((int64_t)b * p.nq + hq0 + h) * p.max_split * 2;
     float M = -INFINITY;
@@ -473,12 +510,17 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams p) {
     if (lane == 0) inv_l[h] = 1.0f / L;
   }
   __syncthreads();
-  for (int e = tid; e < G * HD / 4; e += 256) {
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    const int e = tid + 256 * it;
+    if (e >= G * HD / 4) break;
     const int h = e / (HD / 4), d4 = e % (HD / 4);
     const v4f* src = reinterpret_cast<const v4f*>(p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD) + d4;
     v4f o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sp = 0; sp < PRE; ++sp) o += (sp < ns ? wsplit[h][sp] : 0.f) * pre[it][sp];
 #pragma unroll 8
-    for (int s = 0; s < ns; ++s) o += wsplit[h][s] * src[(int64_t)s * (HD / 4)];
+    for (int sp = PRE; sp < ns; ++sp) o += wsplit[h][sp] * src[(int64_t)sp * (HD / 4)];
     reinterpret_cast<v4f*>(p.out + (int64_t)b * p.nq * HD + (hq0 + h) * HD)[d4] = o * inv_l[h];
   }
 }

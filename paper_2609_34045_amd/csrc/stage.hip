@@ -93,9 +93,11 @@ void kf_stage::mark(void* ctx, int cls, int begin) {
   if (!(s->prof_mask & (1 << cls))) return;
   if (begin) {
     if (s->ev.size() < 2 * (s->ev_used + 1)) {
+      // Timing-only events: no system-scope fence (cache writeback and invalidate)
+      // on record, which would otherwise slow the work that follows.
       hipEvent_t a, b;
-      if (hipEventCreate(&a) != hipSuccess) return;
-      if (hipEventCreate(&b) != hipSuccess) {
+      if (hipEventCreateWithFlags(&a, hipEventDisableSystemFence) != hipSuccess) return;
+      if (hipEventCreateWithFlags(&b, hipEventDisableSystemFence) != hipSuccess) {
         hipEventDestroy(a);
         return;
       }
