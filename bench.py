@@ -31,7 +31,7 @@ import synth  # noqa: E402
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 METRIC = "stage decode tokens/s + achieved HBM GB/s (% of peak), batch 1 and 4"
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_decode_gateup_8b_mid.json")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_decode_gateup_8b_mid.txt")
 DECODE_SRC = os.path.join(ROOT, "paper_2609_34045_amd", "csrc", "decode.hip")
 
 
@@ -48,6 +48,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="CPU oracle sample budget (0 disables)")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="skip the per-launch HIP-event pass (no roofline figure)")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="first run a plain device-to-device copy of this many MiB (counter calibration)")
+    ap.add_argument("--prefill", action="store_true",
+                    help="time the workload's prefill chunk (matrix cores) instead of decode")
     return ap.parse_args()
 
 
@@ -84,6 +88,77 @@ def traffic_from_counters(wl_name: str):
     if rec.get("workload") != wl_name or rec.get("decode_hip_sha256_16") != source_hash(DECODE_SRC):
         return None
     return rec.get("bytes_per_launch")
+
+
+def prefill_flops(wl, T: int, pos0: int) -> float:
+    """Algorithmic flops of one prefill chunk: the projections plus causal attention (no masked work)."""
+    s = wl.shape
+    L = wl.layer_hi - wl.layer_lo
+    proj = 2.0 * T * L * ((2 * s.n_q_heads + 2 * s.n_kv_heads) * s.head_dim * s.hidden + 3 * s.ffn * s.hidden)
+    keys = sum(pos0 + i + 1 for i in range(T))
+    attn = 4.0 * s.head_dim * s.n_q_heads * L * keys
+    return proj + attn
+
+
+def bench_prefill(args, wl, torch, kf):
+    """Time the chunk [ctx - T, ctx) on top of an injected cache [0, ctx - T), K times."""
+    s = wl.shape
+    T = wl.prefill_chunk
+    ctx = wl.contexts[0]
+    pos0 = ctx - T
+    layers = {l: synth.layer_weights(s, wl.cfg_id, l, wl.seed) for l in range(wl.layer_lo, wl.layer_hi)}
+    g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, None)
+    kv = g.kv(1, ctx + 8)
+    for l in range(wl.layer_lo, wl.layer_hi):
+        kb, vb = synth.injected_kv(s, wl.cfg_id, l, 0, pos0, wl.seed)
+        kv.write(l, 0, 0, torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+    del layers
+    h = torch.from_numpy(synth.hidden_states(wl.cfg_id, synth.STREAM_PREFILL_HIDDEN, 0, T, s.hidden, wl.seed)).cuda()
+    out = torch.empty_like(h)
+
+    def run(n):
+        for _ in range(n):
+            kv.set_len(0, pos0)
+            g.prefill(kv, 0, pos0, hidden=h, out=out)
+
+    run(args.warmup)
+    g.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(args.steps)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof = {}
+    if not args.no_kernel_events:
+        g.profile(True)
+        run(args.steps)
+        g.profile(False)
+        prof = g.profile_read()
+    fl = prefill_flops(wl, T, pos0)
+    ms = 1e3 * wall / args.steps
+    tf = fl / (ms * 1e-3) / 1e12
+    dom = prof.get("pf_gateup", (0, 0.0))
+    gu_fl = 2.0 * T * 2 * s.ffn * s.hidden
+    gu_tf = gu_fl / (dom[1] / dom[0] * 1e-3) / 1e12 if dom[0] else None
+    line = {
+        "metric": "stage prefill TFLOP/s (% of bf16/fp16 matrix-core peak)",
+        "value": round(tf, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}), prefill chunk of {T} tokens at "
+                               f"positions [{pos0},{ctx}) over an injected cache", "chunk": T, "pos0": pos0},
+        "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"kernel": "gate/up GEMM + SwiGLU (prefill)", "bound": "mfma",
+                     "achieved": round(gu_tf, 1) if gu_tf else None, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(gu_tf / PEAK_BF16_TFLOPS, 4) if gu_tf else None, "traffic": None,
+                     "algorithmic_flops_per_launch": gu_fl,
+                     "avg_launch_us": round(1e3 * dom[1] / dom[0], 2) if dom[0] else None},
+        "per_kernel": {k: {"launches": n, "avg_us": round(1e3 * t / n, 2)} for k, (n, t) in prof.items()},
+        "algorithmic_flops_per_chunk": fl,
+    }
+    print(json.dumps(line), flush=True)
+    kv.close()
+    g.close()
 
 
 # ------------------------------------------------------------------ CPU oracle baseline
@@ -134,7 +209,23 @@ def main():
 
     from paper_2609_34045_amd import stage as kf
 
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 20
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log(f"[bench] copied {args.copy_calibration_mb} MiB three times (calibration)")
     wl = synth.WORKLOADS[args.workload]
+    if args.prefill:
+        if not wl.prefill_chunk:
+            sys.exit(f"workload {wl.name} has no prefill chunk")
+        torch.cuda.set_device(0)
+        return bench_prefill(args, wl, torch, kf)
     s, B = wl.shape, wl.batch
     ctx = list(wl.contexts)
     torch.cuda.set_device(0)

@@ -24,7 +24,18 @@ namespace kf {
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ v4u ld_stream(const v4u* p) { return __builtin_nontemporal_load(p); }
+#ifndef KF_GEMV_NT
+#define KF_GEMV_NT 1
+#endif
+// Weights are read once per step: non-temporal loads keep them from displacing
+// the small, reused activations in the caches.
+__device__ __forceinline__ v4u ld_stream(const v4u* p) {
+#if KF_GEMV_NT
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
 
 __device__ __forceinline__ void bf16x8(const v4u w, float (&f)[8]) {
   f[0] = __uint_as_float(w.x << 16);
@@ -126,15 +137,14 @@ __device__ __forceinline__ float wave_max(float v) {
 // ------------------------------------------------------------------ GEMV
 // Workgroup of 256 threads owns R output rows of every batch row; its threads
 // stride over K in 16-byte chunks (thread t takes chunks t, t+256, ...), so
-// each wave's loads of a row are 1 KB contiguous.  U chunks of all R rows are
-// in flight per thread before any is consumed.
-#ifndef KF_GEMV_U
-#define KF_GEMV_U 1
-#endif
-
-template <int B, int R, int EPI, bool NORM>
+// each wave's loads of a row are 1 KB contiguous.
+// U chunks of all R rows are in flight per thread before any is consumed: a
+// larger U shortens the serial chain of memory round trips per workgroup
+// (what bounds the small matrices), a smaller U saves registers (occupancy,
+// what bounds the large ones).
+template <int B, int R, int U, int EPI, bool NORM>
 __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
-  constexpr int T = 256, U = KF_GEMV_U;
+  constexpr int T = 256;
   constexpr int NV = R * B + (NORM ? B : 0);
   constexpr int NVP = NV <= 8 ? 8 : NV <= 16 ? 16 : NV <= 32 ? 32 : 64;
   static_assert(NV <= 64, "too many partial sums per workgroup");
@@ -634,26 +644,27 @@ __global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, float* dk
 }
 
 // ------------------------------------------------------------------ launchers
-template <int B, int R>
+template <int B, int R, int U>
 static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
-  if (epi == kEpiQKV && norm) hipLaunchKernelGGL((gemv_kernel<B, R, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
+  if (epi == kEpiQKV && norm)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiResid && !norm)
-    hipLaunchKernelGGL((gemv_kernel<B, R, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiSwiGLU && norm)
-    hipLaunchKernelGGL((gemv_kernel<B, R, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiLMHead && norm)
-    hipLaunchKernelGGL((gemv_kernel<B, R, kEpiLMHead, true>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true>), dim3(grid), dim3(256), 0, s, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-template <int R>
+template <int R, int U>
 static hipError_t gemv_dispatch_b(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
   switch (p.batch) {
-    case 1: return gemv_dispatch_epi<1, R>(epi, norm, p, grid, s);
-    case 2: return gemv_dispatch_epi<2, R>(epi, norm, p, grid, s);
-    case 3: return gemv_dispatch_epi<3, R>(epi, norm, p, grid, s);
-    case 4: return gemv_dispatch_epi<4, R>(epi, norm, p, grid, s);
+    case 1: return gemv_dispatch_epi<1, R, U>(epi, norm, p, grid, s);
+    case 2: return gemv_dispatch_epi<2, R, U>(epi, norm, p, grid, s);
+    case 3: return gemv_dispatch_epi<3, R, U>(epi, norm, p, grid, s);
+    case 4: return gemv_dispatch_epi<4, R, U>(epi, norm, p, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -666,13 +677,13 @@ int gemv_grid(int epi, int R, const GemvParams& p) {
   }
 }
 
-hipError_t launch_gemv(int epi, int R, bool norm, const GemvParams& p, hipStream_t s) {
+hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
   const int grid = gemv_grid(epi, R, p);
-  switch (R) {
-    case 4: return gemv_dispatch_b<4>(epi, norm, p, grid, s);
-    case 8: return gemv_dispatch_b<8>(epi, norm, p, grid, s);
-    default: return hipErrorInvalidValue;
-  }
+  if (R == 8 && U == 1) return gemv_dispatch_b<8, 1>(epi, norm, p, grid, s);
+  if (R == 8 && U == 2) return gemv_dispatch_b<8, 2>(epi, norm, p, grid, s);
+  if (R == 4 && U == 2) return gemv_dispatch_b<4, 2>(epi, norm, p, grid, s);
+  if (R == 4 && U == 4) return gemv_dispatch_b<4, 4>(epi, norm, p, grid, s);
+  return hipErrorInvalidValue;
 }
 
 template <int HD, int G>

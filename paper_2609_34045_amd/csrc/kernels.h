@@ -88,7 +88,7 @@ struct AttnParams {
 
 // Launchers (return hipGetLastError() of the launch).
 int gemv_grid(int epi, int rows_per_wg, const GemvParams& p);
-hipError_t launch_gemv(int epi, int rows_per_wg, bool norm, const GemvParams& p, hipStream_t s);
+hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p, hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
                               float* x, int rows, int H, int* err_flag, hipStream_t s);

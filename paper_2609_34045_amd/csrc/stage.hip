@@ -31,6 +31,21 @@ using namespace kf;
 #ifndef KF_R_LMHEAD
 #define KF_R_LMHEAD 8
 #endif
+#ifndef KF_U_QKV
+#define KF_U_QKV 1
+#endif
+#ifndef KF_U_OPROJ
+#define KF_U_OPROJ 1
+#endif
+#ifndef KF_U_GATEUP
+#define KF_U_GATEUP 1
+#endif
+#ifndef KF_U_DOWN
+#define KF_U_DOWN 1
+#endif
+#ifndef KF_U_LMHEAD
+#define KF_U_LMHEAD 1
+#endif
 #ifndef KF_ATTN_TARGET_WGS
 #define KF_ATTN_TARGET_WGS 512
 #endif
@@ -591,7 +606,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
     {
       tr.begin(KF_K_QKV);
-      const hipError_t le = launch_gemv(kEpiQKV, KF_R_QKV, true, g, st);
+      const hipError_t le = launch_gemv(kEpiQKV, KF_R_QKV, KF_U_QKV, true, g, st);
       tr.end(KF_K_QKV);
       KF_HIP(le, "qkv launch");
     }
@@ -632,7 +647,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     o.x = s->x;
     {
       tr.begin(KF_K_OPROJ);
-      const hipError_t le = launch_gemv(kEpiResid, KF_R_OPROJ, false, o, st);
+      const hipError_t le = launch_gemv(kEpiResid, KF_R_OPROJ, KF_U_OPROJ, false, o, st);
       tr.end(KF_K_OPROJ);
       KF_HIP(le, "o-proj launch");
     }
@@ -649,7 +664,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.act = s->act;
     {
       tr.begin(KF_K_GATEUP);
-      const hipError_t le = launch_gemv(kEpiSwiGLU, KF_R_GATEUP, true, gu, st);
+      const hipError_t le = launch_gemv(kEpiSwiGLU, KF_R_GATEUP, KF_U_GATEUP, true, gu, st);
       tr.end(KF_K_GATEUP);
       KF_HIP(le, "gate/up launch");
     }
@@ -667,7 +682,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
     {
       tr.begin(KF_K_DOWN);
-      const hipError_t le = launch_gemv(kEpiResid, KF_R_DOWN, false, d, st);
+      const hipError_t le = launch_gemv(kEpiResid, KF_R_DOWN, KF_U_DOWN, false, d, st);
       tr.end(KF_K_DOWN);
       KF_HIP(le, "down launch");
     }
@@ -707,7 +722,7 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.part_idx = s->part_idx;
   g.n_wg = s->lm_wg;
   tr.begin(KF_K_LMHEAD);
-  e = launch_gemv(kEpiLMHead, KF_R_LMHEAD, true, g, s->stream);
+  e = launch_gemv(kEpiLMHead, KF_R_LMHEAD, KF_U_LMHEAD, true, g, s->stream);
   tr.end(KF_K_LMHEAD);
   KF_HIP(e, "lm-head launch");
   return KF_OK;
