@@ -1,0 +1,363 @@
+// Prefill projections on the matrix cores: C[M][N] (+)= A[M][K] x W[N][K]^T.
+//
+// A is fp16 activations, W is bf16 weights (converted to fp16 exactly while
+// staged), both K-contiguous; the product runs on v_mfma_f32_32x32x16_f16 with
+// fp32 accumulation.  At a 512-token chunk the projections are large enough
+// to be bound by the matrix cores, which sets the tile shape:
+//   * 256 x 256 x 32 workgroup tiles, four waves (one per SIMD) of 128 x 128,
+//     16 accumulator blocks each (held in the accumulation registers): per K
+//     step a wave reads 16 KB of fragments from LDS for 32 MFMAs (about half
+//     of the LDS bandwidth at full rate);
+//   * operands go from global memory straight into a 4-stage LDS ring with
+//     global_load_lds (no register staging), so loads run three to four K
+//     steps (1.3 - 1.7 us of math at full rate) ahead; chunks are XOR-swizzled
+//     within a row so that fragment reads are free of bank conflicts;
+//   * with one wave per SIMD nothing else hides LDS latency, so each wave
+//     reads the fragments of the next 16-wide K slice while the MFMAs of the
+//     current one run;
+//   * weights stay bf16 in LDS and are converted to fp16 after the fragment
+//     read (exact; 12 ALU operations per 8 values, alongside the MFMAs);
+//   * narrow projections (few 256-wide column tiles) are split along K over
+//     several workgroups whose partial sums are added with fp32 atomics, so
+//     that the grid covers the 256 CUs.
+// Operand fragment layout of v_mfma_f32_32x32x16_f16 (lane l of 64):
+//   A: row l%32, k = 8*(l/32) .. +7      B: column l%32, k = 8*(l/32) .. +7
+//   D: element v (0..15) at row 8*(v/4) + 4*(l/32) + v%4, column l%32
+#include <type_traits>
+
+#include "kernels.h"
+#include "prefill.h"
+
+namespace kf {
+namespace {
+
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int NT = 256;                     // threads per workgroup (4 waves, one per SIMD)
+#ifndef KF_GEMM_READS_PER_SLOT
+#define KF_GEMM_READS_PER_SLOT 1  // fragment reads issued per MFMA slot
+#endif
+#ifndef KF_GEMM_CVT_SLOT
+#define KF_GEMM_CVT_SLOT 8  // first MFMA slot of a half step that converts weights
+#endif
+#ifndef KF_GEMM_STAGGER
+#define KF_GEMM_STAGGER 1  // rotate the split-K atomic epilogue per K slice
+#endif
+#ifndef KF_GEMM_SPLIT_FLOOR
+#define KF_GEMM_SPLIT_FLOOR 1  // K slices per tile: floor (1) or ceiling (0) of 256 / tiles
+#endif
+#ifndef KF_GEMM_STAGES
+#define KF_GEMM_STAGES 4
+#endif
+constexpr int STAGES = KF_GEMM_STAGES;      // LDS ring depth: loads run up to STAGES K steps ahead
+static_assert(STAGES >= 3 && STAGES <= 5, "ring depth");
+constexpr int TILE_BYTES = BM * BK * 2;     // one operand's tile per stage (16 KB)
+constexpr int ROW_BYTES = BK * 2;           // 64 B: four 16-byte chunks per tile row
+constexpr int LOADS = TILE_BYTES / 1024 / 4;  // 1 KB direct loads per wave per operand per stage (4)
+
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, h2));
+}
+__device__ __forceinline__ v4u bf16x8_to_f16x8(v4u w) {
+  return v4u{pack_f16(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u)),
+             pack_f16(__uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)),
+             pack_f16(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xffff0000u)),
+             pack_f16(__uint_as_float(w.w << 16), __uint_as_float(w.w & 0xffff0000u))};
+}
+__device__ __forceinline__ uint16_t to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+__device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b), c, 0, 0, 0);
+}
+
+// Chunk c (0..3) of tile row r is stored at slot c ^ f(r) of that row, with
+// f(r) = (r/2 ^ r/4) % 4: any 8 consecutive rows hit distinct 16-byte bank
+// groups of a 32-bank LDS, and any 16 consecutive rows of a 64-bank one, so
+// the fragment reads (one row per lane) are free of bank conflicts.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ (((r >> 1) ^ (r >> 2)) & 3); }
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier that orders LDS accesses without waiting on outstanding
+// global loads (the compiler may not move memory operations across it).
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+struct Params {
+  const uint16_t* A;
+  const uint16_t* W;
+  const uint16_t* W2;
+  int M, N, K;
+  int splitk;  // K slices (1: plain store / read-modify-write epilogue)
+  float* C;
+  uint16_t* Cb;
+};
+
+template <int EPI>
+__global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
+  // STAGES x (A tile, W tile), each [256 rows][4 swizzled 16-byte chunks]; W stays bf16 here.
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * 2 * TILE_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 128 x 128
+  const int mt = (p.M + BM - 1) / BM, nt = (p.N + BN - 1) / BN, ntiles = mt * nt;
+  const int nwg = ntiles * p.splitk;
+  // Tiles sharing a weight panel (same column tile) go to the same XCD, where
+  // they reuse it through that XCD's L2 (workgroups are dealt round-robin).
+  int bid = blockIdx.x;
+  if (nwg % 8 == 0) bid = (bid % 8) * (nwg / 8) + bid / 8;
+  const int ks = bid % p.splitk, t = bid / p.splitk;
+  const int tm = t % mt, tn = t / mt;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int K = p.K;
+  const int nk_all = K / BK;
+  const int k_begin = (int)((int64_t)nk_all * ks / p.splitk), k_end = (int)((int64_t)nk_all * (ks + 1) / p.splitk);
+  const int nk = k_end - k_begin;
+
+  // Direct global -> LDS loads: load j of this wave fills tile rows
+  // 16 (4 j + wave) .. +15; lane l writes row 16 (4 j + wave) + l/4, slot l%4,
+  // so it fetches the chunk that belongs in that slot.
+  const int w_rows = EPI == kGemmSwiGLU ? (p.N >> 1) : p.N;
+  const uint16_t* asrc[LOADS];
+  const uint16_t* wsrc[LOADS];
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int r = 16 * (4 * j + wave) + (lane >> 2);
+    const int c = swz(r, lane & 3);
+    const int ar = m0 + r < p.M ? m0 + r : p.M - 1;  // rows past M load a valid row; they are never stored
+    asrc[j] = p.A + (int64_t)ar * K + (int64_t)k_begin * BK + c * 8;
+    // weight tile row r: for SwiGLU, 32-row groups alternate gate / up rows of the same outputs
+    int wr;
+    const uint16_t* wb;
+    if (EPI == kGemmSwiGLU) {
+      wr = (n0 >> 1) + (r >> 6) * 32 + (r & 31);
+      wb = ((r >> 5) & 1) ? p.W2 : p.W;
+    } else {
+      wr = n0 + r;
+      wb = p.W;
+    }
+    if (wr >= w_rows) wr = w_rows - 1;  // columns past N load a valid row; they are never stored
+    wsrc[j] = wb + (int64_t)wr * K + (int64_t)k_begin * BK + c * 8;
+  }
+  auto issue = [&](int kt, int stage) {
+    uint8_t* abuf = smem + stage * 2 * TILE_BYTES;
+    uint8_t* wbuf = abuf + TILE_BYTES;
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      __builtin_amdgcn_global_load_lds(asrc[j] + (int64_t)kt * BK, (lds_ptr)(abuf + 1024 * (4 * j + wave)), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(wsrc[j] + (int64_t)kt * BK, (lds_ptr)(wbuf + 1024 * (4 * j + wave)), 16, 0, 0);
+    }
+  };
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  // The K loop is scheduled by hand: each half step is 16 MFMA slots; the
+  // first slots also issue the fragment reads for the next half (and, after
+  // the barrier, one global->LDS load each), the last slots convert the weight
+  // fragments read (whose reads have returned by then).
+  const int rl = lane & 31, kh = lane >> 5;
+  // fragment read q (0..7) of sub-step s (16 values of K) of a stage: weight
+  // block q (still bf16) for q < 4, then A block q-4, so that the conversions
+  // wait only on the first four reads
+  auto read_frag = [&](int stage, int s, int q, v4u (&fa)[4], v4u (&fw)[4]) {
+    const bool w = q < 4;
+    const uint8_t* buf = smem + stage * 2 * TILE_BYTES + (w ? TILE_BYTES : 0);
+    const int r = (w ? wn : wm) * 128 + 32 * (q & 3) + rl;
+    const v4u v = *reinterpret_cast<const v4u*>(buf + r * ROW_BYTES + swz(r, 2 * s + kh) * 16);
+    if (w) fw[q & 3] = v;
+    else fa[q & 3] = v;
+  };
+  // conversion of dword d (0..15) of the weight fragments (fragment d/4)
+  auto convert_dword = [&](v4u (&fw)[4], int d) {
+    const uint32_t w = fw[d >> 2][d & 3];
+    fw[d >> 2][d & 3] = pack_f16(__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u));
+  };
+  // global->LDS load q (0..7) of step kt into a stage: A for even q, W for odd q
+  auto load_part = [&](int kt, int stage, int q) {
+    uint8_t* buf = smem + stage * 2 * TILE_BYTES + (q & 1) * TILE_BYTES + 1024 * (4 * (q >> 1) + wave);
+    const uint16_t* src = ((q & 1) ? wsrc[q >> 1] : asrc[q >> 1]) + (int64_t)kt * BK;
+    __builtin_amdgcn_global_load_lds(src, (lds_ptr)buf, 16, 0, 0);
+  };
+  // One half step: the 16 MFMAs on (fa, fw), the reads of the next fragments
+  // into (na, nw) and their conversion, and optionally the loads of step kt.
+  // Reads go out RPS per slot from slot 0; the 16 dword conversions are spread
+  // over slots C0..15.
+  auto half = [&](const v4u (&fa)[4], const v4u (&fw)[4], int rstage, int rs, v4u (&na)[4], v4u (&nw)[4],
+                  bool load, int kt, int lstage) {
+    constexpr int RPS = KF_GEMM_READS_PER_SLOT, C0 = KF_GEMM_CVT_SLOT;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      acc[q >> 2][q & 3] = mfma32(fa[q >> 2], fw[q & 3], acc[q >> 2][q & 3]);
+#pragma unroll
+      for (int r = 0; r < RPS; ++r)
+        if (q * RPS + r < 8) read_frag(rstage, rs, q * RPS + r, na, nw);
+      if (load && q < 8) load_part(kt, lstage, q);
+      if (q >= C0) {
+#pragma unroll
+        for (int d = (q - C0) * 16 / (16 - C0); d < (q - C0 + 1) * 16 / (16 - C0); ++d) convert_dword(nw, d);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Ring: step k lives in stage k % STAGES.  The fragments of sub-step s+1 are
+  // read while the MFMAs of sub-step s run.  The barrier in the middle of step
+  // k releases step k+1's data to every wave and hands stage k % STAGES (whose
+  // last reads were in step k's first half) to the loads of step k + STAGES.
+  // Past the last step those loads repeat step nk-1 into stages that are not
+  // read again, which keeps the loop free of branches and the wait counts fixed.
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s) issue(s < nk ? s : nk - 1, s);
+  wait_vm<(STAGES - 1) * 2 * LOADS>();  // step 0 has landed
+  block_barrier();
+  v4u fa0[4], fw0[4], fa1[4], fw1[4];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) read_frag(0, 0, q, fa0, fw0);
+#pragma unroll
+  for (int d = 0; d < 16; ++d) convert_dword(fw0, d);
+  for (int k = 0; k + 1 < nk; ++k) {
+    __builtin_amdgcn_sched_barrier(0);
+    half(fa0, fw0, k % STAGES, 1, fa1, fw1, false, 0, 0);
+    // this wave's loads for step k+1 are complete once only the next STAGES-2 steps' remain
+    wait_vm<(STAGES - 2) * 2 * LOADS>();
+    // Every wave's loads for step k+1 have landed and every wave's reads of
+    // stage k % STAGES have returned (they fed the conversions above).  A bare
+    // barrier: a fence here would also drain the loads in flight.
+    block_barrier();
+    half(fa1, fw1, (k + 1) % STAGES, 0, fa0, fw0, true, k + STAGES < nk ? k + STAGES : nk - 1, k % STAGES);
+  }
+  {
+    const int k = nk - 1;
+    half(fa0, fw0, k % STAGES, 1, fa1, fw1, false, 0, 0);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[q >> 2][q & 3] = mfma32(fa1[q >> 2], fw1[q & 3], acc[q >> 2][q & 3]);
+  }
+  wait_vm<0>();  // no load may still be writing LDS when the workgroup ends
+
+  // Epilogue.
+  const int rq = 4 * (lane >> 5);
+  if (EPI != kGemmSwiGLU && p.splitk > 1) {
+    // K slices of one tile finish together: each starts its atomic additions
+    // at a different row block so that they do not queue on the same lines.
+    auto atomic_epilogue = [&](auto rot_c) {
+      constexpr int ROT = decltype(rot_c)::value;
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int i = (ii + ROT) & 3;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 128 + 32 * i + 8 * (v >> 2) + rq + (v & 3);
+          if (row >= p.M) continue;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int col = n0 + wn * 128 + 32 * j + rl;
+            if (col < p.N) atomicAdd(p.C + (int64_t)row * p.N + col, acc[i][j][v]);
+          }
+        }
+      }
+    };
+#if KF_GEMM_STAGGER
+    switch (ks & 3) {
+      case 0: atomic_epilogue(std::integral_constant<int, 0>()); break;
+      case 1: atomic_epilogue(std::integral_constant<int, 1>()); break;
+      case 2: atomic_epilogue(std::integral_constant<int, 2>()); break;
+      default: atomic_epilogue(std::integral_constant<int, 3>()); break;
+    }
+#else
+    atomic_epilogue(std::integral_constant<int, 0>());
+#endif
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = m0 + wm * 128 + 32 * i + 8 * (v >> 2) + rq + (v & 3);
+      if (row >= p.M) continue;
+      if (EPI == kGemmSwiGLU) {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {  // blocks (2jj, 2jj+1) are gate / up of the same outputs
+          const int j = (n0 >> 1) + wn * 64 + 32 * jj + rl;
+          if (j < (p.N >> 1)) {
+            const float g = acc[i][2 * jj][v], u = acc[i][2 * jj + 1][v];
+            p.Cb[(int64_t)row * (p.N >> 1) + j] = to_f16(g / (1.0f + expf(-g)) * u);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int col = n0 + wn * 128 + 32 * j + rl;
+          if (col >= p.N) continue;
+          float* c = p.C + (int64_t)row * p.N + col;
+          if (EPI == kGemmResidF32) *c += acc[i][j][v];
+          else *c = acc[i][j][v];
+        }
+      }
+    }
+  }
+}
+
+__global__ void zero_f32_kernel(float* p, int64_t n) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+}  // namespace
+
+#ifndef KF_GEMM_MAX_SPLIT
+#define KF_GEMM_MAX_SPLIT 8  // upper bound on K slices per output tile
+#endif
+
+int gemm_splitk(int epi, int M, int N, int K) {
+  if (epi == kGemmSwiGLU) return 1;  // the nonlinearity needs complete sums
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  const int nk = K / BK;
+  if (tiles >= 192 || nk < 128) return 1;  // enough tiles, or a short (cheap) reduction
+  int s = KF_GEMM_SPLIT_FLOOR ? 256 / tiles : (256 + tiles - 1) / tiles;
+  if (s > nk / 64) s = nk / 64;  // keep at least 64 K steps per slice
+  if (s > KF_GEMM_MAX_SPLIT) s = KF_GEMM_MAX_SPLIT;
+  return s < 1 ? 1 : s;
+}
+
+hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
+                       float* C, uint16_t* Cb, hipStream_t s) {
+  if (M <= 0 || N <= 0 || K <= 0 || K % BK) return hipErrorInvalidValue;
+  if (epi == kGemmSwiGLU && N % 2) return hipErrorInvalidValue;
+  Params p{A, W, W2, M, N, K, gemm_splitk(epi, M, N, K), C, Cb};
+  if (epi == kGemmStoreF32 && p.splitk > 1) {
+    const int64_t n = (int64_t)M * N;
+    hipLaunchKernelGGL(zero_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, C, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int grid = ((M + BM - 1) / BM) * ((N + BN - 1) / BN) * p.splitk;
+  switch (epi) {
+    case kGemmStoreF32: hipLaunchKernelGGL(gemm256_kernel<kGemmStoreF32>, dim3(grid), dim3(NT), 0, s, p); break;
+    case kGemmResidF32: hipLaunchKernelGGL(gemm256_kernel<kGemmResidF32>, dim3(grid), dim3(NT), 0, s, p); break;
+    case kGemmSwiGLU: hipLaunchKernelGGL(gemm256_kernel<kGemmSwiGLU>, dim3(grid), dim3(NT), 0, s, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace kf

@@ -43,8 +43,9 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a);
 void prefill_free(PrefillWorkspace& ws);
 hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr);
 
-// Exposed for unit tests of the matrix-core GEMM through the library.
+// Matrix-core GEMM of the prefill projections (gemm.hip).
 enum GemmEpi : int { kGemmStoreF32 = 0, kGemmResidF32 = 1, kGemmSwiGLU = 2 };
+int gemm_splitk(int epi, int M, int N, int K);
 hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
                        float* C, uint16_t* Cb, hipStream_t s);
 

@@ -55,163 +55,6 @@ __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b), c, 0, 0, 0);
 }
 
-// ------------------------------------------------------------------ GEMM
-// Workgroup tile 128 x 128 x 64, four waves in a 2 x 2 arrangement, each wave
-// 64 x 64 (2 x 2 MFMA blocks).  Global -> registers -> LDS, double-buffered so
-// one barrier per K step separates reading one buffer from refilling the other.
-namespace gemm {
-constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;  // +16 B row pad against LDS bank conflicts
-}
-
-struct GemmParams {
-  const uint16_t* A;   // [M][K] fp16 activations
-  const uint16_t* W;   // [N][K] bf16 weights (SwiGLU: gate rows)
-  const uint16_t* W2;  // SwiGLU: up rows
-  int M, N, K;         // SwiGLU: N counts gate and up rows together (2F)
-  float* C;            // [M][N] fp32 (store or residual add)
-  uint16_t* Cb;        // SwiGLU: [M][N/2] fp16
-};
-
-template <int EPI>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
-  using namespace gemm;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDK];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int mt = (p.M + BM - 1) / BM, nt = (p.N + BN - 1) / BN, ntiles = mt * nt;
-  // Tiles that share a weight panel go to the same XCD (workgroups are dealt
-  // round-robin over the 8 XCDs), so the panel is fetched from HBM once per L2.
-  int t = blockIdx.x;
-  if (ntiles % 8 == 0) t = (t % 8) * (ntiles / 8) + t / 8;
-  const int tm = t % mt, tn = t / mt;
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int K = p.K;
-
-  // Global load assignment: 4 chunks of 16 B per thread per operand per K step.
-  const v4u* ga[4];
-  const v4u* gw[4];
-  bool oka[4], okw[4];
-  int lrow[4], lcol[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int idx = tid + 256 * i;
-    const int r = idx >> 3, ch = idx & 7;
-    lrow[i] = r;
-    lcol[i] = ch * 8;
-    oka[i] = m0 + r < p.M;
-    ga[i] = reinterpret_cast<const v4u*>(p.A + (int64_t)(oka[i] ? m0 + r : 0) * K + ch * 8);
-    const uint16_t* wbase;
-    int wr;
-    if (EPI == kGemmSwiGLU) {
-      wbase = ((r >> 5) & 1) ? p.W2 : p.W;
-      wr = (n0 >> 1) + (r >> 6) * 32 + (r & 31);
-      okw[i] = wr < (p.N >> 1);
-    } else {
-      wbase = p.W;
-      wr = n0 + r;
-      okw[i] = wr < p.N;
-    }
-    gw[i] = reinterpret_cast<const v4u*>(wbase + (int64_t)(okw[i] ? wr : 0) * K + ch * 8);
-  }
-
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  v4u ra[4], rw[4];
-  const v4u zero = {0u, 0u, 0u, 0u};
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = oka[i] ? ga[i][kt * (BK / 8)] : zero;
-      rw[i] = okw[i] ? __builtin_nontemporal_load(gw[i] + kt * (BK / 8)) : zero;
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<v4u*>(&As[buf][lrow[i] * LDK + lcol[i]]) = ra[i];
-      *reinterpret_cast<v4u*>(&Ws[buf][lrow[i] * LDK + lcol[i]]) = bf16x8_to_f16x8(rw[i]);
-    }
-  };
-
-  const int nk = K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int arow = wm * 64 + (lane & 31), wrow = wn * 64 + (lane & 31), kof = 8 * (lane >> 5);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      v4u fa[2], fw[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        fa[i] = *reinterpret_cast<const v4u*>(&As[buf][(arow + 32 * i) * LDK + s * 16 + kof]);
-        fw[i] = *reinterpret_cast<const v4u*>(&Ws[buf][(wrow + 32 * i) * LDK + s * 16 + kof]);
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(fa[i], fw[j], acc[i][j]);
-    }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
-  }
-
-  // Epilogue.
-  const int col_in = lane & 31, rq = 4 * (lane >> 5);
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = m0 + wm * 64 + 32 * i + 8 * (v >> 2) + rq + (v & 3);
-      if (row >= p.M) continue;
-      if (EPI == kGemmSwiGLU) {
-        const int j = (n0 >> 1) + wn * 32 + col_in;
-        if (j < (p.N >> 1)) {
-          const float g = acc[i][0][v], u = acc[i][1][v];
-          p.Cb[(int64_t)row * (p.N >> 1) + j] = to_f16(g / (1.0f + expf(-g)) * u);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = n0 + wn * 64 + 32 * j + col_in;
-          if (col >= p.N) continue;
-          float* c = p.C + (int64_t)row * p.N + col;
-          if (EPI == kGemmResidF32) *c += acc[i][j][v];
-          else *c = acc[i][j][v];
-        }
-      }
-    }
-  }
-}
-
-hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
-                       float* C, uint16_t* Cb, hipStream_t s) {
-  using namespace gemm;
-  if (M <= 0 || N <= 0 || K <= 0 || K % BK) return hipErrorInvalidValue;
-  GemmParams p{A, W, W2, M, N, K, C, Cb};
-  const int grid = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  switch (epi) {
-    case kGemmStoreF32: hipLaunchKernelGGL(gemm_kernel<kGemmStoreF32>, dim3(grid), dim3(256), 0, s, p); break;
-    case kGemmResidF32: hipLaunchKernelGGL(gemm_kernel<kGemmResidF32>, dim3(grid), dim3(256), 0, s, p); break;
-    case kGemmSwiGLU:
-      if (N % 2) return hipErrorInvalidValue;
-      hipLaunchKernelGGL(gemm_kernel<kGemmSwiGLU>, dim3(grid), dim3(256), 0, s, p);
-      break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
 // ------------------------------------------------------------------ row RMSNorm -> fp16
 __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(const float* x, const uint16_t* g, float eps,
                                                                 uint16_t* out, int H) {
