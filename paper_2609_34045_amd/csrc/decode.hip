@@ -478,60 +478,130 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   }
 }
 
-// Merge of the split-KV partials of one (row, KV head): all G query heads, all hd dims.
-// Runs as its own launch so that the kernel boundary orders the partials' writes
-// before these reads (a device-scope fence per workgroup costs far more on gfx950).
-// The per-split weights 2^(m_s - M) are computed once into LDS; the weighted sum
-// over splits then has no data-dependent branch, so its loads stay in flight.
-template <int HD, int G>
-__global__ __launch_bounds__(256) void attn_combine_kernel(const AttnParams p) {
-  const int g = blockIdx.x, b = blockIdx.y;
+// Output projection fused with the merge of the split-KV partials.  Workgroup
+// (row block rb, query head h) merges head h's partials of every batch row
+// into o_h in LDS (wave b takes row b: weights 2^(m_s - M) per split, sum of
+// the weighted partial vectors, divided by the weighted sum of the partial
+// denominators) and adds W_o[rows, h*hd:(h+1)*hd] o_h to the residual rows
+// with fp32 atomics: the nq heads of a row arrive in any order.  A row's
+// slice is read by 16 lanes x 16 bytes, so every load reads whole rows.  The
+// merging waves request their partials (L2- or cache-resident, written by the
+// attention kernel just before) ahead of the weights: loads return in order,
+// so the merge runs while the weights are still on their way from HBM.
+template <int B, int HD>
+__global__ __launch_bounds__(256) void oproj_heads_kernel(const AttnParams a, const uint16_t* __restrict__ w,
+                                                          float* __restrict__ x, int N) {
+  constexpr int LPR = HD / 8;            // lanes per row
+  constexpr int RPI = 64 / LPR;          // rows per wave-wide load
+  constexpr int RPW = kOprojRows / 4;    // rows per wave
+  constexpr int IT = RPW / RPI;          // loads per lane
+  static_assert(IT == LPR, "one reduced row per lane");
+  constexpr int DPL = HD / 64, PRE = 32;
+  const int rb = blockIdx.x, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int hq0 = g * G, ns = p.n_split;
-  __shared__ float wsplit[G][kAttnMaxSplitCount];
-  __shared__ float inv_l[G];
-  // The first PRE splits of this thread's partial rows are loaded before the
-  // weights are known, so both memory round trips overlap.
-  constexpr int PRE = 8, ITEMS = (G * HD / 4 + 255) / 256;
-  v4f pre[ITEMS][PRE];
+  const int K = a.nq * HD, ns = a.n_split;
+  const int row0 = rb * kOprojRows + wave * RPW + lane / LPR;
+  const int c8 = (lane % LPR) * 8;
+  __shared__ float so[B][HD];
+  __shared__ float wsplit[B][kAttnMaxSplitCount];
+
+  // merging waves: the first PRE splits' partial vectors and the first 64 splits' (max, sum)
+  const int b = wave < B ? wave : 0;
+  const int64_t r0 = ((int64_t)b * a.nq + h) * a.max_split;
+  const float* acc = a.part_acc + r0 * HD + lane * DPL;
+  const float* ml = a.part_ml + r0 * 2;
+  float pre[PRE][DPL];
+  float m0 = -INFINITY, l0 = 0.f;
+  if (wave < B) {
+    // splits past ns re-read split ns-1 (in bounds) and get weight 0 below
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    const int e = tid + 256 * it;
-    const int h = e / (HD / 4), d4 = e % (HD / 4);
-    const v4f* src = reinterpret_cast<const v4f*>(p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD) + d4;
-#pragma unroll
-    for (int sp = 0; sp < PRE; ++sp)
-      pre[it][sp] = (e < G * HD / 4 && sp < ns) ? src[(int64_t)sp * (HD / 4)] : v4f{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < PRE; ++sp) {
+      const float* src = acc + (int64_t)(sp < ns ? sp : ns - 1) * HD;
+      if (DPL == 2) {
+        const float2 v = *reinterpret_cast<const float2*>(src);
+        pre[sp][0] = v.x;
+        pre[sp][DPL - 1] = v.y;
+      } else {
+        pre[sp][0] = src[0];
+      }
+    }
+    const float2 v = *reinterpret_cast<const float2*>(ml + 2 * (lane < ns ? lane : ns - 1));
+    m0 = v.x;
+    l0 = v.y;  // lanes past ns are masked after the weight loads are issued
   }
-  for (int h = wave; h < G; h += 4) {
-    const float* mlh = p.part_ml + ((int64_t)b * p.nq + hq0 + h) * p.max_split * 2;
-    float M = -INFINITY;
-    for (int s = lane; s < ns; s += 64)
-      if (mlh[2 * s + 1] > 0.f) M = fmaxf(M, mlh[2 * s]);
+
+  v4u wv[IT];
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    const int row = min(row0 + i * RPI, N - 1);  // rows past N load row N-1; their sums are dropped
+    wv[i] = ld_stream(reinterpret_cast<const v4u*>(w + (int64_t)row * K + h * HD + c8));
+  }
+
+  if (wave < B) {
+    if (lane >= ns) l0 = 0.f;
+    // splits without keys carry (max, sum) = (-inf, 0) and get weight 0
+    float M = l0 > 0.f ? m0 : -INFINITY;
+    for (int s = lane + 64; s < ns; s += 64)
+      if (ml[2 * s + 1] > 0.f) M = fmaxf(M, ml[2 * s]);
     M = wave_max(M);
     float L = 0.f;
-    for (int s = lane; s < ns; s += 64) {
-      const float l = mlh[2 * s + 1];
-      const float w = l > 0.f ? exp2f(mlh[2 * s] - M) : 0.f;
-      wsplit[h][s] = w;
-      L += w * l;
+    {
+      const float ws = l0 > 0.f ? exp2f(m0 - M) : 0.f;
+      if (lane < ns) wsplit[b][lane] = ws;
+      L = ws * l0;
+    }
+    for (int s = lane + 64; s < ns; s += 64) {
+      const float l = ml[2 * s + 1];
+      const float ws = l > 0.f ? exp2f(ml[2 * s] - M) : 0.f;
+      wsplit[b][s] = ws;
+      L += ws * l;
     }
     L = wave_sum(L);
-    if (lane == 0) inv_l[h] = 1.0f / L;
+    float o[DPL];
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) o[i] = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < PRE; ++sp) {
+      const float ws = sp < ns ? wsplit[b][sp] : 0.f;
+#pragma unroll
+      for (int i = 0; i < DPL; ++i) o[i] += ws * pre[sp][i];
+    }
+#pragma unroll 8
+    for (int sp = PRE; sp < ns; ++sp) {
+      const float ws = wsplit[b][sp];
+#pragma unroll
+      for (int i = 0; i < DPL; ++i) o[i] += ws * acc[(int64_t)sp * HD + i];
+    }
+    const float inv = 1.0f / L;
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) so[b][lane * DPL + i] = o[i] * inv;
   }
   __syncthreads();
+
+  float ov[B][8];
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    const int e = tid + 256 * it;
-    if (e >= G * HD / 4) break;
-    const int h = e / (HD / 4), d4 = e % (HD / 4);
-    const v4f* src = reinterpret_cast<const v4f*>(p.part_acc + ((int64_t)b * p.nq + hq0 + h) * p.max_split * HD) + d4;
-    v4f o = {0.f, 0.f, 0.f, 0.f};
+  for (int bb = 0; bb < B; ++bb)
 #pragma unroll
-    for (int sp = 0; sp < PRE; ++sp) o += (sp < ns ? wsplit[h][sp] : 0.f) * pre[it][sp];
-#pragma unroll 8
-    for (int sp = PRE; sp < ns; ++sp) o += wsplit[h][sp] * src[(int64_t)sp * (HD / 4)];
-    reinterpret_cast<v4f*>(p.out + (int64_t)b * p.nq * HD + (hq0 + h) * HD)[d4] = o * inv_l[h];
+    for (int e = 0; e < 8; ++e) ov[bb][e] = so[bb][c8 + e];
+  float sum[B][IT];
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    float wf[8];
+    bf16x8(wv[i], wf);
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) {
+      float t = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t += wf[e] * ov[bb][e];
+      sum[bb][i] = t;
+    }
+  }
+  // lane j of a row group ends with the group total of load j: row row0 + j * RPI
+  const int j = lane % LPR, row = row0 + j * RPI;
+#pragma unroll
+  for (int bb = 0; bb < B; ++bb) {
+    Butterfly<IT, LPR / 2>::run(sum[bb], lane);
+    if (row < N) atomicAdd(x + (int64_t)bb * N + row, sum[bb][0]);
   }
 }
 
@@ -566,38 +636,54 @@ __global__ void prep_hidden_kernel(const void* __restrict__ in, int in_bf16, con
   reinterpret_cast<v4f*>(x)[i4] = v;
 }
 
-__global__ void argmax_final_kernel(const float* part_val, const int* part_idx, int n_wg, int32_t* token,
-                                    float* max_logit) {
-  const int b = blockIdx.x, tid = threadIdx.x;
+// Second level of the greedy argmax: the per-workgroup (max, lowest row) pairs
+// of one batch row reduced by one 1024-thread workgroup.  Each thread requests
+// U pairs before comparing any, so the pass costs a few memory round trips.
+__device__ __forceinline__ void argmax_take(float v, int ix, float& best, int& bidx) {
+  if (v > best || (v == best && ix < bidx)) {
+    best = v;
+    bidx = ix;
+  }
+}
+
+__global__ __launch_bounds__(1024) void argmax_final_kernel(const float* part_val, const int* part_idx, int n_wg,
+                                                            int32_t* token, float* max_logit) {
+  constexpr int T = 1024, U = 8;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* pv = part_val + (int64_t)b * n_wg;
+  const int* pi = part_idx + (int64_t)b * n_wg;
   float best = -INFINITY;
   int bidx = 0x7fffffff;
-  for (int i = tid; i < n_wg; i += blockDim.x) {
-    const float v = part_val[(int64_t)b * n_wg + i];
-    const int ix = part_idx[(int64_t)b * n_wg + i];
-    if (v > best || (v == best && ix < bidx)) {
-      best = v;
-      bidx = ix;
+  for (int i0 = tid; i0 < n_wg; i0 += T * U) {
+    float v[U];
+    int ix[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u * T;
+      v[u] = i < n_wg ? pv[i] : -INFINITY;
+      ix[u] = i < n_wg ? pi[i] : 0x7fffffff;
     }
+#pragma unroll
+    for (int u = 0; u < U; ++u) argmax_take(v[u], ix[u], best, bidx);
   }
-  __shared__ float sv[256];
-  __shared__ int si[256];
-  sv[tid] = best;
-  si[tid] = bidx;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) argmax_take(__shfl_xor(best, o), __shfl_xor(bidx, o), best, bidx);
+  __shared__ float sv[T / 64];
+  __shared__ int si[T / 64];
+  if (lane == 0) {
+    sv[wave] = best;
+    si[wave] = bidx;
+  }
   __syncthreads();
-  for (int o = 128; o >= 1; o >>= 1) {
-    if (tid < o) {
-      const float v = sv[tid + o];
-      const int ix = si[tid + o];
-      if (v > sv[tid] || (v == sv[tid] && ix < si[tid])) {
-        sv[tid] = v;
-        si[tid] = ix;
-      }
+  if (wave == 0) {
+    best = lane < T / 64 ? sv[lane] : -INFINITY;
+    bidx = lane < T / 64 ? si[lane] : 0x7fffffff;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) argmax_take(__shfl_xor(best, o), __shfl_xor(bidx, o), best, bidx);
+    if (lane == 0) {
+      token[b] = bidx;
+      if (max_logit) max_logit[b] = best;
     }
-    __syncthreads();
-  }
-  if (tid == 0) {
-    token[b] = si[0];
-    if (max_logit) max_logit[b] = sv[0];
   }
 }
 
@@ -689,9 +775,6 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
 template <int HD, int G>
 static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
   hipLaunchKernelGGL((attn_decode_kernel<HD, G>), dim3(p.n_split, p.nkv, batch), dim3(256), 0, s, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_combine_kernel<HD, G>), dim3(p.nkv, batch), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
@@ -716,6 +799,25 @@ hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+template <int HD>
+static hipError_t oproj_dispatch(const AttnParams& a, const uint16_t* w, float* x, int N, int batch, hipStream_t s) {
+  const dim3 grid((N + kOprojRows - 1) / kOprojRows, a.nq);
+  switch (batch) {
+    case 1: hipLaunchKernelGGL((oproj_heads_kernel<1, HD>), grid, dim3(256), 0, s, a, w, x, N); break;
+    case 2: hipLaunchKernelGGL((oproj_heads_kernel<2, HD>), grid, dim3(256), 0, s, a, w, x, N); break;
+    case 3: hipLaunchKernelGGL((oproj_heads_kernel<3, HD>), grid, dim3(256), 0, s, a, w, x, N); break;
+    case 4: hipLaunchKernelGGL((oproj_heads_kernel<4, HD>), grid, dim3(256), 0, s, a, w, x, N); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_oproj_heads(const AttnParams& a, const uint16_t* w, float* x, int N, int batch, hipStream_t s) {
+  if (a.hd == 128) return oproj_dispatch<128>(a, w, x, N, batch, s);
+  if (a.hd == 64) return oproj_dispatch<64>(a, w, x, N, batch, s);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
                               float* x, int rows, int H, int* err_flag, hipStream_t s) {
   const int64_t n4 = (int64_t)rows * H / 4;
@@ -726,7 +828,7 @@ hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens
 
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
                                float* max_logit, hipStream_t s) {
-  hipLaunchKernelGGL(argmax_final_kernel, dim3(rows), dim3(256), 0, s, part_val, part_idx, n_wg, token, max_logit);
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(rows), dim3(1024), 0, s, part_val, part_idx, n_wg, token, max_logit);
   return hipGetLastError();
 }
 

@@ -10,6 +10,7 @@ constexpr int kMaxBatch = 4;
 constexpr int kMaxGroup = 8;     // query heads per KV head
 constexpr int kAttnMinSplit = 16;   // keys per split-KV workgroup, lower bound
 constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound
+constexpr int kOprojRows = 256;     // output rows per workgroup of the head-split output projection
 constexpr int kAttnMaxSplitCount = 1024;  // split-KV workgroups per (row, KV head), upper bound
 
 // Optional per-launch marker around each kernel (instrumentation hook of the runtime).
@@ -73,7 +74,6 @@ struct AttnParams {
   const float* q;      // [B][nq*hd] rotated queries
   const uint16_t* kc;  // layer base (fp16 bits), [user][kv_head][pos][hd]
   const uint16_t* vc;
-  float* out;          // [B][nq*hd]
   float* part_acc;     // [B][nq][max_split][hd]
   float* part_ml;      // [B][nq][max_split][2]
   int64_t user_stride;
@@ -90,6 +90,8 @@ struct AttnParams {
 int gemv_grid(int epi, int rows_per_wg, const GemvParams& p);
 hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p, hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
+// x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] bf16).
+hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
                               float* x, int rows, int H, int* err_flag, hipStream_t s);
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,

@@ -19,9 +19,6 @@ using namespace kf;
 #ifndef KF_R_QKV
 #define KF_R_QKV 8
 #endif
-#ifndef KF_R_OPROJ
-#define KF_R_OPROJ 8
-#endif
 #ifndef KF_R_GATEUP
 #define KF_R_GATEUP 8
 #endif
@@ -34,9 +31,6 @@ using namespace kf;
 #ifndef KF_U_QKV
 #define KF_U_QKV 1
 #endif
-#ifndef KF_U_OPROJ
-#define KF_U_OPROJ 1
-#endif
 #ifndef KF_U_GATEUP
 #define KF_U_GATEUP 1
 #endif
@@ -47,7 +41,7 @@ using namespace kf;
 #define KF_U_LMHEAD 1
 #endif
 #ifndef KF_ATTN_TARGET_WGS
-#define KF_ATTN_TARGET_WGS 512
+#define KF_ATTN_TARGET_WGS 256
 #endif
 #ifndef KF_ATTN_ALIGN
 #define KF_ATTN_ALIGN 64
@@ -87,7 +81,7 @@ struct kf_stage {
   uint16_t *embed = nullptr, *lm_head = nullptr, *g_final = nullptr;
   // decode workspace
   char* ws = nullptr;
-  float *x = nullptr, *q = nullptr, *o = nullptr, *act = nullptr, *hx = nullptr;
+  float *x = nullptr, *q = nullptr, *act = nullptr, *hx = nullptr;
   float* part_val = nullptr;
   int* part_idx = nullptr;
   int lm_wg = 0;
@@ -197,7 +191,6 @@ static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
   int64_t n = 0;
   n += align256(B * H * 4);                           // x
   n += align256(B * c.n_q_heads * c.head_dim * 4);    // q
-  n += align256(B * c.n_q_heads * c.head_dim * 4);    // o
   n += align256(B * (int64_t)c.ffn * 4);              // act
   n += align256(B * H * 4);                           // hx
   if (has_head) {
@@ -355,7 +348,6 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   const int64_t B = kMaxBatch;
   s->x = (float*)take(B * H * 4);
   s->q = (float*)take(B * c.n_q_heads * hd * 4);
-  s->o = (float*)take(B * c.n_q_heads * hd * 4);
   s->act = (float*)take(B * F * 4);
   s->hx = (float*)take(B * H * 4);
   if (has_head) {
@@ -530,11 +522,14 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
 }
 
 // ------------------------------------------------------------------ decode
-static void attn_split(int batch, int nkv, int max_len, int max_split, int* split, int* n_split) {
-  const int target = (KF_ATTN_TARGET_WGS + batch * nkv - 1) / (batch * nkv);  // workgroups per (row, KV head)
-  auto up64 = [](int v) { return (v + KF_ATTN_ALIGN - 1) / KF_ATTN_ALIGN * KF_ATTN_ALIGN; };
-  int sp = up64((max_len + target - 1) / target);
-  const int need = up64((max_len + max_split - 1) / max_split);
+// Keys per split-KV workgroup: sized from the keys of the whole batch, so that
+// about KF_ATTN_TARGET_WGS workgroups carry keys however ragged the contexts
+// are (a row shorter than the longest has idle trailing splits, which exit at
+// once).  The split never exceeds the partial-buffer capacity per row.
+static void attn_split(int nkv, int64_t total_len, int max_len, int max_split, int* split, int* n_split) {
+  auto up = [](int64_t v) { return (int)((v + KF_ATTN_ALIGN - 1) / KF_ATTN_ALIGN * KF_ATTN_ALIGN); };
+  int sp = up((total_len * nkv + KF_ATTN_TARGET_WGS - 1) / KF_ATTN_TARGET_WGS);
+  const int need = up((max_len + max_split - 1) / max_split);
   if (sp < need) sp = need;
   if (sp < kAttnMinSplit) sp = kAttnMinSplit;
   if (sp > kAttnMaxSplit) sp = kAttnMaxSplit;
@@ -554,6 +549,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   if (!hidden_out_dev) return fail(KF_EINVAL, "hidden output is NULL");
   if (io != KF_F32 && io != KF_BF16) return fail(KF_EINVAL, "io dtype");
   int max_len = 0;
+  int64_t total_len = 0;
   for (int b = 0; b < batch; ++b) {
     const int u = users[b], p = positions[b];
     if (u < 0 || u >= kv->max_users) return fail(KF_EINVAL, "users[%d] = %d outside [0, %d)", b, u, kv->max_users);
@@ -562,6 +558,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     if (p != kv->len[u]) return fail(KF_EINVAL, "positions[%d] = %d but user %d holds %d positions", b, p, u, kv->len[u]);
     if (p >= kv->max_ctx) return fail(KF_ERANGE, "position %d beyond max_ctx %d", p, kv->max_ctx);
     if (p + 1 > max_len) max_len = p + 1;
+    total_len += p + 1;
   }
   const kf_model_config& c = s->cfg;
   const int H = c.hidden, hd = c.head_dim;
@@ -575,7 +572,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   KF_HIP(pe, "prep launch");
 
   int split, n_split;
-  attn_split(batch, c.n_kv_heads, max_len, kv->max_split, &split, &n_split);
+  attn_split(c.n_kv_heads, total_len, max_len, kv->max_split, &split, &n_split);
 
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];
@@ -615,7 +612,6 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     a.q = s->q;
     a.kc = kv->k + loff;
     a.vc = kv->v + loff;
-    a.out = s->o;
     a.part_acc = kv->part_acc;
     a.part_ml = kv->part_ml;
     a.user_stride = kv->user_stride;
@@ -638,16 +634,9 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       KF_HIP(le, "attention launch");
     }
 
-    GemvParams o{};
-    o.batch = batch;
-    o.w0 = L.wo;
-    o.in = s->o;
-    o.K = c.n_q_heads * hd;
-    o.N = H;
-    o.x = s->x;
     {
       tr.begin(KF_K_OPROJ);
-      const hipError_t le = launch_gemv(kEpiResid, KF_R_OPROJ, KF_U_OPROJ, false, o, st);
+      const hipError_t le = launch_oproj_heads(a, L.wo, s->x, H, batch, st);
       tr.end(KF_K_OPROJ);
       KF_HIP(le, "o-proj launch");
     }

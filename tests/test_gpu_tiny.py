@@ -169,19 +169,24 @@ def test_argmax_on_identical_hidden_batch(torch, st, model):
 
 
 def test_embedding_gather_is_exact(torch, st, model):
+    """Token input equals hidden input of the exact fp32 embedding rows; the two decodes agree
+    to fp32 summation-order rounding (the output projection adds heads in arrival order)."""
     g, kv, o = make(st, model, head=True)
     toks = np.array([0, 999, 5, 5], dtype=np.int32)
     a = g.decode(kv, [0, 1, 2, 3], [0, 0, 0, 0], tokens=dev(torch, toks))
     kv2 = g.kv(4, 16)
     emb = bf16_to_f64(model.head()["embed"][toks]).astype(np.float32)
     b = g.decode(kv2, [0, 1, 2, 3], [0, 0, 0, 0], hidden=dev(torch, emb))
-    assert torch.equal(a, b)
+    assert float(row_rel_err(host(b), host(a)).max()) <= 1e-5
     kv2.close()
     kv.close()
     g.close()
 
 
-def test_stage_composition_bit_exact(torch, st, model):
+def test_stage_composition(torch, st, model):
+    """Layers [0,2) as one stage equal [0,1) then [1,2): bit-exact for prefill (no split
+    reductions at this shape); decode adds the heads' output projections into the residual
+    with atomics in arrival order, so two runs agree to fp32 summation-order rounding."""
     whole = st.Stage(SHAPE, 0, 2, model.layer)
     first = st.Stage(SHAPE, 0, 1, model.layer)
     second = st.Stage(SHAPE, 1, 2, model.layer)
@@ -195,7 +200,7 @@ def test_stage_composition_bit_exact(torch, st, model):
         users, pos = [0, 1], [20 + step, step]
         a = whole.decode(kw, users, pos, hidden=x)
         b = second.decode(k2, users, pos, hidden=first.decode(k1, users, pos, hidden=x))
-        assert torch.equal(a, b)
+        assert float(row_rel_err(host(b), host(a)).max()) <= 1e-5
     for x in (kw, k1, k2, whole, first, second):
         x.close()
 
