@@ -142,6 +142,107 @@ __device__ __forceinline__ float wave_max(float v) {
 // larger U shortens the serial chain of memory round trips per workgroup
 // (what bounds the small matrices), a smaller U saves registers (occupancy,
 // what bounds the large ones).
+// Weight row of local row r (0..R-1) of workgroup wg, and whether it is a
+// real output row.  QKV workgroups take R/2 rotation pairs (i, i + hd/2) of
+// one head, so RoPE is applied in the epilogue; SwiGLU workgroups take R/2
+// gate rows and the R/2 up rows of the same outputs.
+template <int R, int EPI>
+__device__ __forceinline__ const uint16_t* gemv_row(const GemvParams& p, int wg, int r, bool& ok) {
+  ok = true;
+  if (EPI == kEpiQKV) {
+    const int wg_per_head = p.hd / R, head = wg / wg_per_head, i0 = (wg % wg_per_head) * (R / 2);
+    const int row = head * p.hd + (r < R / 2 ? i0 + r : p.hd / 2 + i0 + r - R / 2);
+    return p.w0 + (int64_t)row * p.K;
+  } else if (EPI == kEpiSwiGLU) {
+    const int row = wg * (R / 2) + (r < R / 2 ? r : r - R / 2);
+    return (r < R / 2 ? p.w0 : p.w1) + (int64_t)row * p.K;
+  } else {
+    const int row = wg * R + r;
+    ok = row < p.N;
+    return p.w0 + (int64_t)(ok ? row : 0) * p.K;
+  }
+}
+
+// Epilogue of a workgroup's R x B dot products fin[r * B + b] (plus, when the
+// launch normalises its input, fin[R * B + b] = sum of x_b^2 over K).  Runs
+// on the T threads (index tid) that own the group, after fin is complete.
+template <int B, int R, int EPI, bool NORM, int T>
+__device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const float* fin, int tid) {
+  float rs[B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) rs[b] = NORM ? 1.0f / sqrtf(fin[R * B + b] / (float)p.K + p.eps) : 1.0f;
+
+  if (EPI == kEpiQKV) {
+    if (tid < (R / 2) * B) {
+      const int wg_per_head = p.hd / R, head = wg / wg_per_head, i0 = (wg % wg_per_head) * (R / 2);
+      const int r = tid / B, b = tid % B;
+      const float y1 = fin[r * B + b] * rs[b];
+      const float y2 = fin[(r + R / 2) * B + b] * rs[b];
+      const int hd = p.hd, half = hd / 2, i = i0 + r, pos = p.pos[b];
+      if (head < p.nq + p.nkv) {
+        const float c = p.rope_cos[(int64_t)pos * half + i], s = p.rope_sin[(int64_t)pos * half + i];
+        const float z1 = y1 * c - y2 * s, z2 = y2 * c + y1 * s;
+        if (head < p.nq) {
+          float* q = p.q + (int64_t)b * p.nq * hd + head * hd;
+          q[i] = z1;
+          q[i + half] = z2;
+        } else {
+          uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq) * p.max_ctx + pos) * hd;
+          k[i] = f32_to_f16(z1);
+          k[i + half] = f32_to_f16(z2);
+        }
+      } else {
+        uint16_t* v = p.vc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq - p.nkv) * p.max_ctx + pos) * hd;
+        v[i] = f32_to_f16(y1);
+        v[i + half] = f32_to_f16(y2);
+      }
+    }
+  } else if (EPI == kEpiResid) {
+    for (int t = tid; t < R * B; t += T) {
+      const int r = t / B, b = t % B, row = wg * R + r;
+      if (row < p.N) {
+        const int64_t at = (int64_t)b * p.N + row;
+        const float v = p.x[at] + fin[t];
+        p.x[at] = v;
+        if (p.out2) {
+          if (p.out2_bf16) reinterpret_cast<uint16_t*>(p.out2)[at] = f32_to_bf16(v);
+          else reinterpret_cast<float*>(p.out2)[at] = v;
+        }
+      }
+    }
+  } else if (EPI == kEpiSwiGLU) {
+    if (tid < (R / 2) * B) {
+      const int r = tid / B, b = tid % B;
+      const float gt = fin[r * B + b] * rs[b];
+      const float up = fin[(r + R / 2) * B + b] * rs[b];
+      p.act[(int64_t)b * p.N + wg * (R / 2) + r] = gt / (1.0f + expf(-gt)) * up;
+    }
+  } else {  // kEpiLMHead
+    if (p.logits) {
+      for (int t = tid; t < R * B; t += T) {
+        const int r = t / B, b = t % B, row = wg * R + r;
+        if (row < p.N) p.logits[(int64_t)b * p.N + row] = fin[t] * rs[b];
+      }
+    }
+    if (tid < B) {
+      const int b = tid;
+      float best = fin[b] * rs[b];
+      int bidx = wg * R;
+      for (int r = 1; r < R; ++r) {
+        const float v = fin[r * B + b] * rs[b];
+        if (wg * R + r < p.N && v > best) {  // strict: the lower row keeps a tie
+          best = v;
+          bidx = wg * R + r;
+        }
+      }
+      p.part_val[(int64_t)b * p.n_wg + wg] = best;
+      p.part_idx[(int64_t)b * p.n_wg + wg] = bidx;
+    }
+  }
+}
+
+// Vector-ALU GEMV: each thread multiplies its 16-byte weight chunks by the
+// fp32 input rows, so a row's 8 products per chunk cost 8 FMAs per batch row.
 template <int B, int R, int U, int EPI, bool NORM>
 __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
@@ -154,35 +255,10 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
   const int wg = blockIdx.x;
   const int K = p.K, nch = K >> 3;
 
-  // Row pointers of this workgroup.
   const v4u* wrow[R];
   bool rok[R];
-  int head = 0, i0 = 0;
-  if (EPI == kEpiQKV) {
-    const int wg_per_head = p.hd / R;
-    head = wg / wg_per_head;
-    i0 = (wg % wg_per_head) * (R / 2);
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int row = head * p.hd + (r < R / 2 ? i0 + r : p.hd / 2 + i0 + r - R / 2);
-      wrow[r] = reinterpret_cast<const v4u*>(p.w0 + (int64_t)row * K);
-      rok[r] = true;
-    }
-  } else if (EPI == kEpiSwiGLU) {
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int row = wg * (R / 2) + (r < R / 2 ? r : r - R / 2);
-      wrow[r] = reinterpret_cast<const v4u*>((r < R / 2 ? p.w0 : p.w1) + (int64_t)row * K);
-      rok[r] = true;
-    }
-  } else {
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int row = wg * R + r;
-      rok[r] = row < p.N;
-      wrow[r] = reinterpret_cast<const v4u*>(p.w0 + (int64_t)(rok[r] ? row : 0) * K);
-    }
-  }
+  for (int r = 0; r < R; ++r) wrow[r] = reinterpret_cast<const v4u*>(gemv_row<R, EPI>(p, wg, r, rok[r]));
 
   float acc[NVP];
 #pragma unroll
@@ -244,76 +320,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
   __syncthreads();
   if (tid < NVP) fin[tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
   __syncthreads();
-
-  float rs[B];
-#pragma unroll
-  for (int b = 0; b < B; ++b) rs[b] = NORM ? 1.0f / sqrtf(fin[R * B + b] / (float)K + p.eps) : 1.0f;
-
-  if (EPI == kEpiQKV) {
-    if (tid < (R / 2) * B) {
-      const int r = tid / B, b = tid % B;
-      const float y1 = fin[r * B + b] * rs[b];
-      const float y2 = fin[(r + R / 2) * B + b] * rs[b];
-      const int hd = p.hd, half = hd / 2, i = i0 + r, pos = p.pos[b];
-      if (head < p.nq + p.nkv) {
-        const float c = p.rope_cos[(int64_t)pos * half + i], s = p.rope_sin[(int64_t)pos * half + i];
-        const float z1 = y1 * c - y2 * s, z2 = y2 * c + y1 * s;
-        if (head < p.nq) {
-          float* q = p.q + (int64_t)b * p.nq * hd + head * hd;
-          q[i] = z1;
-          q[i + half] = z2;
-        } else {
-          uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq) * p.max_ctx + pos) * hd;
-          k[i] = f32_to_f16(z1);
-          k[i + half] = f32_to_f16(z2);
-        }
-      } else {
-        uint16_t* v = p.vc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq - p.nkv) * p.max_ctx + pos) * hd;
-        v[i] = f32_to_f16(y1);
-        v[i + half] = f32_to_f16(y2);
-      }
-    }
-  } else if (EPI == kEpiResid) {
-    if (tid < R * B) {
-      const int r = tid / B, b = tid % B, row = wg * R + r;
-      if (row < p.N) {
-        const int64_t at = (int64_t)b * p.N + row;
-        const float v = p.x[at] + fin[tid];
-        p.x[at] = v;
-        if (p.out2) {
-          if (p.out2_bf16) reinterpret_cast<uint16_t*>(p.out2)[at] = f32_to_bf16(v);
-          else reinterpret_cast<float*>(p.out2)[at] = v;
-        }
-      }
-    }
-  } else if (EPI == kEpiSwiGLU) {
-    if (tid < (R / 2) * B) {
-      const int r = tid / B, b = tid % B;
-      const float gt = fin[r * B + b] * rs[b];
-      const float up = fin[(r + R / 2) * B + b] * rs[b];
-      p.act[(int64_t)b * p.N + wg * (R / 2) + r] = gt / (1.0f + expf(-gt)) * up;
-    }
-  } else {  // kEpiLMHead
-    if (p.logits && tid < R * B) {
-      const int r = tid / B, b = tid % B, row = wg * R + r;
-      if (row < p.N) p.logits[(int64_t)b * p.N + row] = fin[tid] * rs[b];
-    }
-    if (tid < B) {
-      const int b = tid;
-      float best = fin[b] * rs[b];
-      int bidx = wg * R;
-#pragma unroll
-      for (int r = 1; r < R; ++r) {
-        const float v = fin[r * B + b] * rs[b];
-        if (wg * R + r < p.N && v > best) {  // strict: the lower row keeps a tie
-          best = v;
-          bidx = wg * R + r;
-        }
-      }
-      p.part_val[(int64_t)b * p.n_wg + wg] = best;
-      p.part_idx[(int64_t)b * p.n_wg + wg] = bidx;
-    }
-  }
+  gemv_epilogue<B, R, EPI, NORM, T>(p, wg, fin, tid);
 }
 
 // ------------------------------------------------------------------ attention

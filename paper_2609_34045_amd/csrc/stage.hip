@@ -84,7 +84,8 @@ struct kf_stage {
   float *x = nullptr, *q = nullptr, *act = nullptr, *hx = nullptr;
   float* part_val = nullptr;
   int* part_idx = nullptr;
-  int lm_wg = 0;
+  int lm_wg = 0;       // capacity of the argmax partials per batch row
+  int lm_wg_used = 0;  // partials per row written by the last LM-head launch
   int* err_flag = nullptr;
   int live_kv = 0;
   PrefillWorkspace pf;
@@ -709,7 +710,8 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.logits = logits;
   g.part_val = s->part_val;
   g.part_idx = s->part_idx;
-  g.n_wg = s->lm_wg;
+  g.n_wg = gemv_grid(kEpiLMHead, KF_R_LMHEAD, g);
+  s->lm_wg_used = g.n_wg;
   tr.begin(KF_K_LMHEAD);
   e = launch_gemv(kEpiLMHead, KF_R_LMHEAD, KF_U_LMHEAD, true, g, s->stream);
   tr.end(KF_K_LMHEAD);
@@ -741,7 +743,7 @@ kf_status kf_head_argmax(kf_stage* s, int32_t rows, const void* hidden, kf_dtype
   if (st != KF_OK) return st;
   const Tracer tr = s->tracer();
   tr.begin(KF_K_ARGMAX);
-  const hipError_t e = launch_argmax_final(s->part_val, s->part_idx, s->lm_wg, rows, token, max_logit, s->stream);
+  const hipError_t e = launch_argmax_final(s->part_val, s->part_idx, s->lm_wg_used, rows, token, max_logit, s->stream);
   tr.end(KF_K_ARGMAX);
   KF_HIP(e, "argmax launch");
   return KF_OK;
