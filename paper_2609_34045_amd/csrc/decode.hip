@@ -163,11 +163,40 @@ __device__ __forceinline__ const uint16_t* gemv_row(const GemvParams& p, int wg,
   }
 }
 
+// Values an epilogue thread needs from memory, requested when the kernel
+// starts so that no memory round trip is left after the reduction: the RoPE
+// cos/sin of its rotation pair (QKV) or the residual value it updates.
+struct EpiPre {
+  float a, b;
+};
+
+template <int B, int R, int EPI>
+__device__ __forceinline__ EpiPre gemv_epi_prefetch(const GemvParams& p, int wg, int tid) {
+  EpiPre e{0.f, 0.f};
+  if (EPI == kEpiQKV) {
+    if (tid < (R / 2) * B) {
+      const int wg_per_head = p.hd / R, head = wg / wg_per_head, i0 = (wg % wg_per_head) * (R / 2);
+      const int r = tid / B, b = tid % B, half = p.hd / 2;
+      if (head < p.nq + p.nkv) {
+        e.a = p.rope_cos[(int64_t)p.pos[b] * half + i0 + r];
+        e.b = p.rope_sin[(int64_t)p.pos[b] * half + i0 + r];
+      }
+    }
+  } else if (EPI == kEpiResid) {
+    if (tid < R * B) {
+      const int r = tid / B, b = tid % B, row = wg * R + r;
+      if (row < p.N) e.a = p.x[(int64_t)b * p.N + row];
+    }
+  }
+  return e;
+}
+
 // Epilogue of a workgroup's R x B dot products fin[r * B + b] (plus, when the
 // launch normalises its input, fin[R * B + b] = sum of x_b^2 over K).  Runs
 // on the T threads (index tid) that own the group, after fin is complete.
 template <int B, int R, int EPI, bool NORM, int T>
-__device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const float* fin, int tid) {
+__device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const float* fin, int tid,
+                                              const EpiPre& pre) {
   float rs[B];
 #pragma unroll
   for (int b = 0; b < B; ++b) rs[b] = NORM ? 1.0f / sqrtf(fin[R * B + b] / (float)p.K + p.eps) : 1.0f;
@@ -180,7 +209,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       const float y2 = fin[(r + R / 2) * B + b] * rs[b];
       const int hd = p.hd, half = hd / 2, i = i0 + r, pos = p.pos[b];
       if (head < p.nq + p.nkv) {
-        const float c = p.rope_cos[(int64_t)pos * half + i], s = p.rope_sin[(int64_t)pos * half + i];
+        const float c = pre.a, s = pre.b;
         const float z1 = y1 * c - y2 * s, z2 = y2 * c + y1 * s;
         if (head < p.nq) {
           float* q = p.q + (int64_t)b * p.nq * hd + head * hd;
@@ -198,11 +227,12 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       }
     }
   } else if (EPI == kEpiResid) {
-    for (int t = tid; t < R * B; t += T) {
-      const int r = t / B, b = t % B, row = wg * R + r;
+    static_assert(EPI != kEpiResid || R * B <= T, "one residual row per thread");
+    if (tid < R * B) {
+      const int t = tid, r = t / B, b = t % B, row = wg * R + r;
       if (row < p.N) {
         const int64_t at = (int64_t)b * p.N + row;
-        const float v = p.x[at] + fin[t];
+        const float v = pre.a + fin[t];
         p.x[at] = v;
         if (p.out2) {
           if (p.out2_bf16) reinterpret_cast<uint16_t*>(p.out2)[at] = f32_to_bf16(v);
@@ -259,6 +289,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
   bool rok[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) wrow[r] = reinterpret_cast<const v4u*>(gemv_row<R, EPI>(p, wg, r, rok[r]));
+  const EpiPre pre = gemv_epi_prefetch<B, R, EPI>(p, wg, tid);
 
   float acc[NVP];
 #pragma unroll
@@ -320,7 +351,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
   __syncthreads();
   if (tid < NVP) fin[tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
   __syncthreads();
-  gemv_epilogue<B, R, EPI, NORM, T>(p, wg, fin, tid);
+  gemv_epilogue<B, R, EPI, NORM, T>(p, wg, fin, tid, pre);
 }
 
 // ------------------------------------------------------------------ attention
