@@ -219,13 +219,13 @@ kf_status kf_head_argmax(kf_stage* stage, int32_t rows, const void* hidden_dev, 
 typedef enum {
   KF_K_PREP = 0,       /* hidden/token input to the fp32 residual stream */
   KF_K_QKV = 1,        /* decode: RMSNorm + QKV GEMV + RoPE + KV append */
-  KF_K_ATTN = 2,       /* decode: split-KV attention + merge */
-  KF_K_OPROJ = 3,      /* decode: O GEMV + residual */
+  KF_K_ATTN = 2,       /* decode: split-KV attention (partials per split) */
+  KF_K_OPROJ = 3,      /* decode: merge of the partials + O GEMV + residual */
   KF_K_GATEUP = 4,     /* decode: RMSNorm + gate/up GEMV + SwiGLU */
   KF_K_DOWN = 5,       /* decode: down GEMV + residual */
   KF_K_LMHEAD = 6,     /* head: final RMSNorm + LM-head GEMV + partial argmax */
   KF_K_ARGMAX = 7,     /* head: final argmax reduction */
-  KF_K_PF_NORM = 8,    /* prefill: row RMSNorm to bf16 */
+  KF_K_PF_NORM = 8,    /* prefill: row RMSNorm to fp16 */
   KF_K_PF_QKV = 9,     /* prefill: QKV GEMM (matrix cores) */
   KF_K_PF_ROPE = 10,   /* prefill: RoPE + KV append */
   KF_K_PF_ATTN = 11,   /* prefill: causal flash attention (matrix cores) */
