@@ -273,7 +273,35 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
 
 // Vector-ALU GEMV: each thread multiplies its 16-byte weight chunks by the
 // fp32 input rows, so a row's 8 products per chunk cost 8 FMAs per batch row.
-template <int B, int R, int U, int EPI, bool NORM>
+// Input chunk c (8 values) of batch row b taken from the stage input: an fp32
+// or bf16 hidden row, or the embedding row of a token (NaN for a token outside
+// [0, vocab)).  The conversions are exact.
+__device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, int c, v4f& lo, v4f& hi) {
+  const int K = p.K;
+  if (p.tokens) {
+    const int tok = p.tokens[b];
+    if (tok < 0 || tok >= p.vocab) {
+      const float qn = __uint_as_float(0x7fc00000u);
+      lo = hi = v4f{qn, qn, qn, qn};
+      return;
+    }
+    float f[8];
+    bf16x8(*reinterpret_cast<const v4u*>(p.embed + (int64_t)tok * K + c * 8), f);
+    lo = v4f{f[0], f[1], f[2], f[3]};
+    hi = v4f{f[4], f[5], f[6], f[7]};
+  } else if (p.src_bf16) {
+    float f[8];
+    bf16x8(*reinterpret_cast<const v4u*>(reinterpret_cast<const uint16_t*>(p.src) + (int64_t)b * K + c * 8), f);
+    lo = v4f{f[0], f[1], f[2], f[3]};
+    hi = v4f{f[4], f[5], f[6], f[7]};
+  } else {
+    const v4f* q = reinterpret_cast<const v4f*>(reinterpret_cast<const float*>(p.src) + (int64_t)b * K + c * 8);
+    lo = q[0];
+    hi = q[1];
+  }
+}
+
+template <int B, int R, int U, int EPI, bool NORM, bool SRC = false>
 __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
   constexpr int NV = R * B + (NORM ? B : 0);
@@ -290,6 +318,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
 #pragma unroll
   for (int r = 0; r < R; ++r) wrow[r] = reinterpret_cast<const v4u*>(gemv_row<R, EPI>(p, wg, r, rok[r]));
   const EpiPre pre = gemv_epi_prefetch<B, R, EPI>(p, wg, tid);
+  if (SRC && wg == 0 && p.tokens && tid < B && (p.tokens[tid] < 0 || p.tokens[tid] >= p.vocab)) atomicOr(p.err_flag, 1);
 
   float acc[NVP];
 #pragma unroll
@@ -310,9 +339,13 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
         const int c = (c0 + u * T < nch ? c0 + u * T : c0);  // past the end: re-read chunk c0, unused
 #pragma unroll
         for (int b = 0; b < B; ++b) {
-          const v4f* src = reinterpret_cast<const v4f*>(p.in + (int64_t)b * K + c * 8);
-          xl[u][b] = src[0];
-          xh[u][b] = src[1];
+          if (SRC) {
+            stage_input_chunk(p, b, c, xl[u][b], xh[u][b]);
+          } else {
+            const v4f* src = reinterpret_cast<const v4f*>(p.in + (int64_t)b * K + c * 8);
+            xl[u][b] = src[0];
+            xh[u][b] = src[1];
+          }
         }
         if (NORM) gv[u] = *reinterpret_cast<const v4u*>(p.gain + c * 8);
       }
@@ -332,6 +365,13 @@ __global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
     for (int u = 0; u < U; ++u) {
       const int c = c0 + u * T;
       if (c < nch) {
+        if (SRC && wg == 0 && p.x_init) {  // the residual stream starts as the stage input
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+            reinterpret_cast<v4f*>(p.x_init + (int64_t)b * K + c * 8)[0] = xl[u][b];
+            reinterpret_cast<v4f*>(p.x_init + (int64_t)b * K + c * 8)[1] = xh[u][b];
+          }
+        }
         float xf[B][8];
 #pragma unroll
         for (int b = 0; b < B; ++b) {
@@ -803,6 +843,16 @@ static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int
   return hipGetLastError();
 }
 
+template <int B, int R, int U>
+static hipError_t gemv_dispatch_src(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
+  if (epi == kEpiQKV && norm)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true, true>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiLMHead && norm)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true, true>), dim3(grid), dim3(256), 0, s, p);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 template <int R, int U>
 static hipError_t gemv_dispatch_b(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
   switch (p.batch) {
@@ -819,6 +869,19 @@ int gemv_grid(int epi, int R, const GemvParams& p) {
     case kEpiQKV: return (p.nq + 2 * p.nkv) * (p.hd / R);
     case kEpiSwiGLU: return p.N / (R / 2);
     default: return (p.N + R - 1) / R;
+  }
+}
+
+hipError_t launch_gemv_src(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
+  if ((p.src == nullptr) == (p.tokens == nullptr)) return hipErrorInvalidValue;
+  if (R != 8 || U != 1) return hipErrorInvalidValue;
+  const int grid = gemv_grid(epi, R, p);
+  switch (p.batch) {
+    case 1: return gemv_dispatch_src<1, 8, 1>(epi, norm, p, grid, s);
+    case 2: return gemv_dispatch_src<2, 8, 1>(epi, norm, p, grid, s);
+    case 3: return gemv_dispatch_src<3, 8, 1>(epi, norm, p, grid, s);
+    case 4: return gemv_dispatch_src<4, 8, 1>(epi, norm, p, grid, s);
+    default: return hipErrorInvalidValue;
   }
 }
 

@@ -63,6 +63,16 @@ struct GemvParams {
   // kEpiSwiGLU
   float* act;          // [B][N] with N = F
 
+  // Launches with the stage input as their input rows (instead of `in`): the
+  // first layer's QKV and the LM head.  Exactly one of src / tokens is set.
+  const void* src;         // [B][K] hidden input, fp32 or (src_bf16) bf16
+  int src_bf16;
+  const int32_t* tokens;   // [B] token ids: rows of `embed` [vocab][K] bf16
+  const uint16_t* embed;
+  int vocab;
+  float* x_init;           // optional [B][K]: workgroup 0 stores the input rows here (residual stream)
+  int* err_flag;           // bit 1 set for a token outside [0, vocab) (its row becomes NaN)
+
   // kEpiLMHead
   float* logits;       // optional [B][N]
   float* part_val;     // [B][n_wg]
@@ -89,6 +99,9 @@ struct AttnParams {
 // Launchers (return hipGetLastError() of the launch).
 int gemv_grid(int epi, int rows_per_wg, const GemvParams& p);
 hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p, hipStream_t s);
+// The same launch with the stage input (p.src or p.tokens) as its input rows.
+hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
+                           hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
 // x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] bf16).
 hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);

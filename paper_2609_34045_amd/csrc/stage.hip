@@ -81,7 +81,7 @@ struct kf_stage {
   uint16_t *embed = nullptr, *lm_head = nullptr, *g_final = nullptr;
   // decode workspace
   char* ws = nullptr;
-  float *x = nullptr, *q = nullptr, *act = nullptr, *hx = nullptr;
+  float *x = nullptr, *q = nullptr, *act = nullptr;
   float* part_val = nullptr;
   int* part_idx = nullptr;
   int lm_wg = 0;       // capacity of the argmax partials per batch row
@@ -193,7 +193,6 @@ static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
   n += align256(B * H * 4);                           // x
   n += align256(B * c.n_q_heads * c.head_dim * 4);    // q
   n += align256(B * (int64_t)c.ffn * 4);              // act
-  n += align256(B * H * 4);                           // hx
   if (has_head) {
     const int64_t wgs = (c.vocab + 3) / 4;  // enough for any rows-per-workgroup choice
     n += 2 * align256(B * wgs * 4);
@@ -350,7 +349,6 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->x = (float*)take(B * H * 4);
   s->q = (float*)take(B * c.n_q_heads * hd * 4);
   s->act = (float*)take(B * F * 4);
-  s->hx = (float*)take(B * H * 4);
   if (has_head) {
     s->lm_wg = (int)((V + KF_R_LMHEAD - 1) / KF_R_LMHEAD);
     s->part_val = (float*)take(B * s->lm_wg * 4);
@@ -566,12 +564,6 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   hipStream_t st = s->stream;
 
   const Tracer tr = s->tracer();
-  tr.begin(KF_K_PREP);
-  hipError_t pe = launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->x, batch, H,
-                                     s->err_flag, st);
-  tr.end(KF_K_PREP);
-  KF_HIP(pe, "prep launch");
-
   int split, n_split;
   attn_split(c.n_kv_heads, total_len, max_len, kv->max_split, &split, &n_split);
 
@@ -602,12 +594,22 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.users[b] = b < batch ? users[b] : 0;
       g.pos[b] = b < batch ? positions[b] : 0;
     }
-    {
-      tr.begin(KF_K_QKV);
-      const hipError_t le = launch_gemv(kEpiQKV, KF_R_QKV, KF_U_QKV, true, g, st);
-      tr.end(KF_K_QKV);
-      KF_HIP(le, "qkv launch");
+    hipError_t le;
+    tr.begin(KF_K_QKV);
+    if (l == s->lo) {  // the first layer reads the stage input and starts the residual stream from it
+      g.src = hidden_in_dev;
+      g.src_bf16 = io == KF_BF16;
+      g.tokens = tokens_dev;
+      g.embed = s->embed;
+      g.vocab = c.vocab;
+      g.x_init = s->x;
+      g.err_flag = s->err_flag;
+      le = launch_gemv_src(kEpiQKV, KF_R_QKV, KF_U_QKV, true, g, st);
+    } else {
+      le = launch_gemv(kEpiQKV, KF_R_QKV, KF_U_QKV, true, g, st);
     }
+    tr.end(KF_K_QKV);
+    KF_HIP(le, "qkv launch");
 
     AttnParams a{};
     a.q = s->q;
@@ -694,17 +696,13 @@ static kf_status head_common(kf_stage* s, int rows, const void* hidden, kf_dtype
 static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype dtype, float* logits) {
   const kf_model_config& c = s->cfg;
   const Tracer tr = s->tracer();
-  tr.begin(KF_K_PREP);
-  hipError_t e = launch_prep_hidden(hidden, dtype == KF_BF16, nullptr, nullptr, 0, s->hx, rows, c.hidden, s->err_flag,
-                                    s->stream);
-  tr.end(KF_K_PREP);
-  KF_HIP(e, "head prep launch");
   GemvParams g{};
   g.batch = rows;
   g.eps = c.rms_eps;
   g.w0 = s->lm_head;
   g.gain = s->g_final;
-  g.in = s->hx;
+  g.src = hidden;  // the LM head reads the caller's rows directly
+  g.src_bf16 = dtype == KF_BF16;
   g.K = c.hidden;
   g.N = c.vocab;
   g.logits = logits;
@@ -713,7 +711,7 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.n_wg = gemv_grid(kEpiLMHead, KF_R_LMHEAD, g);
   s->lm_wg_used = g.n_wg;
   tr.begin(KF_K_LMHEAD);
-  e = launch_gemv(kEpiLMHead, KF_R_LMHEAD, KF_U_LMHEAD, true, g, s->stream);
+  const hipError_t e = launch_gemv_src(kEpiLMHead, KF_R_LMHEAD, KF_U_LMHEAD, true, g, s->stream);
   tr.end(KF_K_LMHEAD);
   KF_HIP(e, "lm-head launch");
   return KF_OK;

@@ -282,7 +282,7 @@ def test_kernel_profiling_records_every_launch(torch, st, model):
     g.profile(False)
     g.decode(kv, [0], [3], hidden=x)  # not recorded
     rec = g.profile_read()
-    assert rec["prep"][0] == 3
+    assert "prep" not in rec  # the first QKV launch reads the stage input itself
     for k in ("qkv", "attn", "oproj", "gateup", "down"):
         assert rec[k][0] == 3 * 2 and rec[k][1] > 0.0
     g.profile(True)
