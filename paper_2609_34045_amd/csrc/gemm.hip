@@ -18,8 +18,9 @@
 //   * weights stay bf16 in LDS and are converted to fp16 after the fragment
 //     read (exact; 12 ALU operations per 8 values, alongside the MFMAs);
 //   * narrow projections (few 256-wide column tiles) are split along K over
-//     several workgroups whose partial sums are added with fp32 atomics, so
-//     that the grid covers the 256 CUs.
+//     several workgroups so that the grid covers the 256 CUs; the slices are
+//     either stored whole for the consuming kernel to add in order
+//     (kGemmPartialF32) or added with fp32 atomics.
 // Operand fragment layout of v_mfma_f32_32x32x16_f16 (lane l of 64):
 //   A: row l%32, k = 8*(l/32) .. +7      B: column l%32, k = 8*(l/32) .. +7
 //   D: element v (0..15) at row 8*(v/4) + 4*(l/32) + v%4, column l%32
@@ -256,7 +257,7 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
 
   // Epilogue.
   const int rq = 4 * (lane >> 5);
-  if (EPI != kGemmSwiGLU && p.splitk > 1) {
+  if ((EPI == kGemmStoreF32 || EPI == kGemmResidF32) && p.splitk > 1) {
     // K slices of one tile finish together: each starts its atomic additions
     // at a different row block so that they do not queue on the same lines.
     auto atomic_epilogue = [&](auto rot_c) {
@@ -310,6 +311,7 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
           if (col >= p.N) continue;
           float* c = p.C + (int64_t)row * p.N + col;
           if (EPI == kGemmResidF32) *c += acc[i][j][v];
+          else if (EPI == kGemmPartialF32) c[(int64_t)ks * p.M * p.N] = acc[i][j][v];
           else *c = acc[i][j][v];
         }
       }
@@ -355,6 +357,7 @@ hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint
     case kGemmStoreF32: hipLaunchKernelGGL(gemm256_kernel<kGemmStoreF32>, dim3(grid), dim3(NT), 0, s, p); break;
     case kGemmResidF32: hipLaunchKernelGGL(gemm256_kernel<kGemmResidF32>, dim3(grid), dim3(NT), 0, s, p); break;
     case kGemmSwiGLU: hipLaunchKernelGGL(gemm256_kernel<kGemmSwiGLU>, dim3(grid), dim3(NT), 0, s, p); break;
+    case kGemmPartialF32: hipLaunchKernelGGL(gemm256_kernel<kGemmPartialF32>, dim3(grid), dim3(NT), 0, s, p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

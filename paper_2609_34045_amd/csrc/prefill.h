@@ -33,7 +33,8 @@ struct PrefillWorkspace {
   char* mem = nullptr;
   float* x = nullptr;      // [T][H] residual stream
   uint16_t* xn = nullptr;  // [T][H] normalised, fp16
-  float* qkv = nullptr;    // [T][(nq+2nkv) hd] raw projections
+  float* part = nullptr;   // split-K partial sums [slices][T][N] of the last split projection
+  int pending = 0;         // slices of the down projection in `part` not yet added to x
   uint16_t* q = nullptr;   // [T][nq][hd] rotated queries, fp16
   uint16_t* o = nullptr;   // [T][nq hd] attention output, fp16
   uint16_t* act = nullptr; // [T][F] SwiGLU output, fp16
@@ -44,7 +45,9 @@ void prefill_free(PrefillWorkspace& ws);
 hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr);
 
 // Matrix-core GEMM of the prefill projections (gemm.hip).
-enum GemmEpi : int { kGemmStoreF32 = 0, kGemmResidF32 = 1, kGemmSwiGLU = 2 };
+// kGemmPartialF32 writes K slice ks to C + ks*M*N (plain stores); the consumer
+// adds the gemm_splitk(kGemmPartialF32, ...) slices in order.
+enum GemmEpi : int { kGemmStoreF32 = 0, kGemmResidF32 = 1, kGemmSwiGLU = 2, kGemmPartialF32 = 3 };
 int gemm_splitk(int epi, int M, int N, int K);
 hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
                        float* C, uint16_t* Cb, hipStream_t s);

@@ -17,6 +17,8 @@
 #include <cmath>
 
 #include "kernels.h"
+#include <algorithm>
+
 #include "prefill.h"
 
 namespace kf {
@@ -56,50 +58,94 @@ __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
 }
 
 // ------------------------------------------------------------------ row RMSNorm -> fp16
-__global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(const float* x, const uint16_t* g, float eps,
+// Row RMSNorm of the residual stream to fp16.  With nsplit > 0 the row first
+// takes the nsplit split-K slices of the projection that just ran (part, slice
+// stride `stride`), added in slice order, and the sum is written back to x.
+// Threads move 16 bytes at a time and request every slice before adding.
+constexpr int kMaxSlices = 8;
+
+__global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const float* part, int nsplit,
+                                                                int64_t stride, const uint16_t* g, float eps,
                                                                 uint16_t* out, int H) {
-  const int row = blockIdx.x, tid = threadIdx.x;
-  const float* xr = x + (int64_t)row * H;
+  const int row = blockIdx.x, tid = threadIdx.x, H4 = H / 4;
+  v4f* xr = reinterpret_cast<v4f*>(x + (int64_t)row * H);
+  const v4f* pr = reinterpret_cast<const v4f*>(part + (int64_t)row * H);
+  const int64_t st4 = stride / 4;
   float ss = 0.f;
-  for (int k = tid; k < H; k += 256) ss += xr[k] * xr[k];
+  for (int k = tid; k < H4; k += 256) {
+    v4f v = xr[k];
+    if (nsplit > 0) {
+      v4f sl[kMaxSlices];
+#pragma unroll
+      for (int i = 0; i < kMaxSlices; ++i)
+        if (i < nsplit) sl[i] = pr[i * st4 + k];
+#pragma unroll
+      for (int i = 0; i < kMaxSlices; ++i)
+        if (i < nsplit) v += sl[i];
+      xr[k] = v;
+    }
+    ss += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+  }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
   __shared__ float red[4];
   if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float rs = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)H + eps);
-  uint16_t* o = out + (int64_t)row * H;
-  for (int k = tid; k < H; k += 256) o[k] = to_f16(xr[k] * rs * from_bf16(g[k]));
+  uint2* o = reinterpret_cast<uint2*>(out + (int64_t)row * H);
+  const uint2* g4 = reinterpret_cast<const uint2*>(g);
+  for (int k = tid; k < H4; k += 256) {
+    const v4f v = xr[k] * rs;
+    const uint2 gw = g4[k];
+    o[k] = uint2{pack_f16(v.x * __uint_as_float(gw.x << 16), v.y * __uint_as_float(gw.x & 0xffff0000u)),
+                 pack_f16(v.z * __uint_as_float(gw.y << 16), v.w * __uint_as_float(gw.y & 0xffff0000u))};
+  }
 }
 
 // ------------------------------------------------------------------ RoPE + KV append
-// qkv [T][(nq+2nkv) hd] fp32 -> q [T][nq][hd] fp16 (rotated), K/V cache at pos0 + i (fp16).
-__global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, uint16_t* q, uint16_t* kc, uint16_t* vc,
-                                                      const float* cosT, const float* sinT, int nq, int nkv, int hd,
-                                                      int pos0, int max_ctx) {
-  const int i = blockIdx.x, half = hd / 2, pos = pos0 + i;
+// QKV [T][(nq+2nkv) hd] fp32, the sum of nsplit split-K slices of `qkv` (slice
+// stride `stride`) -> q [T][nq][hd] fp16 (rotated), K/V cache at pos0 + i (fp16).
+// A thread takes 4 consecutive rotation pairs (j .. j+3, j+hd/2 .. j+hd/2+3).
+__global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nsplit, int64_t stride, uint16_t* q,
+                                                      uint16_t* kc, uint16_t* vc, const float* cosT,
+                                                      const float* sinT, int nq, int nkv, int hd, int pos0,
+                                                      int max_ctx) {
+  const int i = blockIdx.x, half = hd / 2, q4 = half / 4, pos = pos0 + i;
   const int nh = nq + 2 * nkv;
   const float* src = qkv + (int64_t)i * nh * hd;
-  for (int e = threadIdx.x; e < nh * half; e += 256) {
-    const int h = e / half, j = e % half;
-    const float a = src[h * hd + j], b = src[h * hd + j + half];
-    if (h < nq + nkv) {
-      const float c = cosT[(int64_t)pos * half + j], s = sinT[(int64_t)pos * half + j];
-      const float z1 = a * c - b * s, z2 = b * c + a * s;
-      if (h < nq) {
-        uint16_t* dst = q + ((int64_t)i * nq + h) * hd;
-        dst[j] = to_f16(z1);
-        dst[j + half] = to_f16(z2);
-      } else {
-        uint16_t* dst = kc + ((int64_t)(h - nq) * max_ctx + pos) * hd;
-        dst[j] = to_f16(z1);
-        dst[j + half] = to_f16(z2);
-      }
-    } else {
-      uint16_t* dst = vc + ((int64_t)(h - nq - nkv) * max_ctx + pos) * hd;
-      dst[j] = to_f16(a);
-      dst[j + half] = to_f16(b);
+  for (int e = threadIdx.x; e < nh * q4; e += 256) {
+    const int h = e / q4, j = (e % q4) * 4;
+    v4f a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+    {
+      v4f sa[kMaxSlices], sb[kMaxSlices];
+#pragma unroll
+      for (int sl = 0; sl < kMaxSlices; ++sl)
+        if (sl < nsplit) {
+          sa[sl] = *reinterpret_cast<const v4f*>(src + sl * stride + h * hd + j);
+          sb[sl] = *reinterpret_cast<const v4f*>(src + sl * stride + h * hd + j + half);
+        }
+#pragma unroll
+      for (int sl = 0; sl < kMaxSlices; ++sl)
+        if (sl < nsplit) {
+          a += sa[sl];
+          b += sb[sl];
+        }
     }
+    uint16_t* dst;
+    v4f z1, z2;
+    if (h < nq + nkv) {
+      const v4f c = *reinterpret_cast<const v4f*>(cosT + (int64_t)pos * half + j);
+      const v4f s = *reinterpret_cast<const v4f*>(sinT + (int64_t)pos * half + j);
+      z1 = a * c - b * s;
+      z2 = b * c + a * s;
+      dst = h < nq ? q + ((int64_t)i * nq + h) * hd : kc + ((int64_t)(h - nq) * max_ctx + pos) * hd;
+    } else {
+      z1 = a;
+      z2 = b;
+      dst = vc + ((int64_t)(h - nq - nkv) * max_ctx + pos) * hd;
+    }
+    *reinterpret_cast<uint2*>(dst + j) = uint2{pack_f16(z1.x, z1.y), pack_f16(z1.z, z1.w)};
+    *reinterpret_cast<uint2*>(dst + j + half) = uint2{pack_f16(z2.x, z2.y), pack_f16(z2.z, z2.w)};
   }
 }
 
@@ -269,34 +315,44 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
 }
 
 // ------------------------------------------------------------------ final copy
-__global__ void store_rows_kernel(const float* x, void* out, int out_bf16, int64_t n) {
+// Hidden output of the stage: the residual stream plus the nsplit pending
+// split-K slices of the last down projection (slice stride n).
+__global__ void store_rows_kernel(const float* x, const float* part, int nsplit, void* out, int out_bf16,
+                                  int64_t n) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= n) return;
-  if (out_bf16) reinterpret_cast<uint16_t*>(out)[i] = to_bf16(x[i]);
-  else reinterpret_cast<float*>(out)[i] = x[i];
+  float v = x[i];
+  for (int sl = 0; sl < nsplit; ++sl) v += part[sl * n + i];
+  if (out_bf16) reinterpret_cast<uint16_t*>(out)[i] = to_bf16(v);
+  else reinterpret_cast<float*>(out)[i] = v;
 }
 
 // ------------------------------------------------------------------ host side
 static int64_t a256(int64_t n) { return (n + 255) & ~(int64_t)255; }
 
 void prefill_free(PrefillWorkspace& ws) {
-  if (ws.mem) hipFree(ws.mem);
+  if (ws.mem) (void)hipFree(ws.mem);
   ws = PrefillWorkspace{};
 }
 
 hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   if (a.T <= ws.cap_T && ws.mem) return hipSuccess;
   const int64_t T = a.T, H = a.H, nqkv = (int64_t)(a.nq + 2 * a.nkv) * a.hd;
-  const int64_t sz_x = a256(T * H * 4), sz_xn = a256(T * H * 2), sz_qkv = a256(T * nqkv * 4),
+  // the split-K slices of the largest of the QKV, O and down projections
+  const int64_t part_qkv = (int64_t)gemm_splitk(kGemmPartialF32, a.T, (int)nqkv, H) * T * nqkv;
+  const int64_t part_o = (int64_t)gemm_splitk(kGemmPartialF32, a.T, H, a.nq * a.hd) * T * H;
+  const int64_t part_d = (int64_t)gemm_splitk(kGemmPartialF32, a.T, H, a.F) * T * H;
+  const int64_t part = std::max(part_qkv, std::max(part_o, part_d));
+  const int64_t sz_x = a256(T * H * 4), sz_xn = a256(T * H * 2), sz_part = a256(part * 4),
                 sz_q = a256(T * a.nq * a.hd * 2), sz_o = a256(T * a.nq * a.hd * 2), sz_act = a256(T * a.F * 2);
-  const int64_t total = sz_x + sz_xn + sz_qkv + sz_q + sz_o + sz_act;
+  const int64_t total = sz_x + sz_xn + sz_part + sz_q + sz_o + sz_act;
   char* mem = nullptr;
   // Drain work that may still use the old buffer before freeing it.
   hipError_t e = hipStreamSynchronize(a.stream);
   if (e != hipSuccess) return e;
   e = hipMalloc((void**)&mem, total);
   if (e != hipSuccess) {
-    hipGetLastError();
+    (void)hipGetLastError();
     return hipErrorOutOfMemory;
   }
   prefill_free(ws);
@@ -307,8 +363,8 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   p += sz_x;
   ws.xn = (uint16_t*)p;
   p += sz_xn;
-  ws.qkv = (float*)p;
-  p += sz_qkv;
+  ws.part = (float*)p;
+  p += sz_part;
   ws.q = (uint16_t*)p;
   p += sz_q;
   ws.o = (uint16_t*)p;
@@ -320,20 +376,28 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
 hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr) {
   hipStream_t s = a.stream;
   const int T = a.T, H = a.H, nqkv = (a.nq + 2 * a.nkv) * a.hd;
+  const int64_t TH = (int64_t)T * H;
   hipError_t e;
   // Class ids follow kf_kernel_class of the public header.
   enum { NORM = 8, QKV = 9, ROPE = 10, ATTN = 11, OPROJ = 12, GATEUP = 13, DOWN = 14, STORE = 15 };
+  // The previous layer's down projection may still be pending as split-K slices.
   tr.begin(NORM);
-  hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_attn, a.eps, ws.xn, H);
+  hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, ws.part, ws.pending, TH, l.g_attn,
+                     a.eps, ws.xn, H);
   tr.end(NORM);
+  ws.pending = 0;
   if ((e = hipGetLastError()) != hipSuccess) return e;
   tr.begin(QKV);
-  e = launch_gemm(kGemmStoreF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.qkv, nullptr, s);
+  const int s_qkv = gemm_splitk(kGemmPartialF32, T, nqkv, H);
+  if (s_qkv > kMaxSlices || gemm_splitk(kGemmPartialF32, T, H, a.nq * a.hd) > kMaxSlices ||
+      gemm_splitk(kGemmPartialF32, T, H, a.F) > kMaxSlices)
+    return hipErrorInvalidValue;  // more split-K slices than the consuming kernels add
+  e = launch_gemm(kGemmPartialF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.part, nullptr, s);
   tr.end(QKV);
   if (e != hipSuccess) return e;
   tr.begin(ROPE);
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.qkv, ws.q, l.kc, l.vc, a.rope_cos, a.rope_sin, a.nq,
-                     a.nkv, a.hd, a.pos0, a.max_ctx);
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.part, s_qkv, (int64_t)T * nqkv, ws.q, l.kc, l.vc,
+                     a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, a.max_ctx);
   tr.end(ROPE);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));
@@ -349,26 +413,33 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
     return hipErrorInvalidValue;
   tr.end(ATTN);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  tr.begin(OPROJ);
-  e = launch_gemm(kGemmResidF32, ws.o, l.wo, nullptr, T, H, a.nq * a.hd, ws.x, nullptr, s);
-  tr.end(OPROJ);
-  if (e != hipSuccess) return e;
+  // O and down: split along K into slices that the next norm (or the output
+  // store) adds in order; an unsplit projection adds into x directly.
+  auto resid_proj = [&](int cls, const uint16_t* A, const uint16_t* W, int K, int* pend) {
+    const int sp = gemm_splitk(kGemmPartialF32, T, H, K);
+    tr.begin(cls);
+    const hipError_t le = sp > 1 ? launch_gemm(kGemmPartialF32, A, W, nullptr, T, H, K, ws.part, nullptr, s)
+                                 : launch_gemm(kGemmResidF32, A, W, nullptr, T, H, K, ws.x, nullptr, s);
+    tr.end(cls);
+    *pend = sp > 1 ? sp : 0;
+    return le;
+  };
+  int pend_o = 0;
+  if ((e = resid_proj(OPROJ, ws.o, l.wo, a.nq * a.hd, &pend_o)) != hipSuccess) return e;
   tr.begin(NORM);
-  hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, l.g_mlp, a.eps, ws.xn, H);
+  hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, ws.part, pend_o, TH, l.g_mlp, a.eps,
+                     ws.xn, H);
   tr.end(NORM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   tr.begin(GATEUP);
   e = launch_gemm(kGemmSwiGLU, ws.xn, l.wg, l.wu, T, 2 * a.F, H, nullptr, ws.act, s);
   tr.end(GATEUP);
   if (e != hipSuccess) return e;
-  tr.begin(DOWN);
-  e = launch_gemm(kGemmResidF32, ws.act, l.wd, nullptr, T, H, a.F, ws.x, nullptr, s);
-  tr.end(DOWN);
-  if (e != hipSuccess) return e;
+  if ((e = resid_proj(DOWN, ws.act, l.wd, a.F, &ws.pending)) != hipSuccess) return e;
   if (l.out) {
-    const int64_t n = (int64_t)T * H;
     tr.begin(STORE);
-    hipLaunchKernelGGL(store_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, ws.x, l.out, l.out_bf16, n);
+    hipLaunchKernelGGL(store_rows_kernel, dim3((unsigned)((TH + 255) / 256)), dim3(256), 0, s, ws.x, ws.part,
+                       ws.pending, l.out, l.out_bf16, TH);
     tr.end(STORE);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }

@@ -786,6 +786,7 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
                          s->stream);
   tr.end(KF_K_PREP);
   KF_HIP(e, "prefill prep launch");
+  s->pf.pending = 0;  // x now holds the whole input; no split-K slices are pending
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];
     const int64_t loff = (l - s->lo) * kv->layer_stride + user * kv->user_stride;
