@@ -63,6 +63,9 @@ __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
 // stride `stride`), added in slice order, and the sum is written back to x.
 // Threads move 16 bytes at a time and request every slice before adding.
 constexpr int kMaxSlices = 8;
+#ifndef KF_PF_ATTN_SPLIT
+#define KF_PF_ATTN_SPLIT 2  // key splits of the prefill attention when the chunk gives < 512 workgroups
+#endif
 
 __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const float* part, int nsplit,
                                                                 int64_t stride, const uint16_t* g, float eps,
@@ -156,10 +159,16 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
 // the lane's probabilities are already a B fragment of O^T += V^T P^T once the
 // MFMA's k index is mapped to the keys the lane holds.  V^T is written to LDS
 // transposed when the block is staged.
+//
+// The keys may be split over gridDim.z workgroups (more workgroups in flight,
+// two per CU): split z takes key blocks [z nblk / Z, (z+1) nblk / Z) and, when
+// Z > 1, writes its unnormalised output and (max, sum) per query to part_acc /
+// part_ml for attn_prefill_combine_kernel.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
-                                                           const uint16_t* vc, uint16_t* out, int T, int nq, int nkv,
-                                                           int pos0, int max_ctx, float scale_log2) {
+                                                           const uint16_t* vc, uint16_t* out, float* part_acc,
+                                                           float* part_ml, int T, int nq, int nkv, int pos0,
+                                                           int max_ctx, float scale_log2) {
   constexpr int KB = 32;            // keys per block
   constexpr int LDK = HD + 8;       // K tile row stride (fp16 elements)
   constexpr int LDV = KB + 4;       // V^T tile row stride (fp16 elements), keeps 8-byte alignment
@@ -176,7 +185,9 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
   const int qpos = pos0 + qi;
   const int last_q = min(i0 + 127, T - 1);
   const int nkeys = pos0 + last_q + 1;  // keys visible to the workgroup's last query
-  const int nblk = (nkeys + KB - 1) / KB;
+  const int nblk_all = (nkeys + KB - 1) / KB;
+  const int Z = gridDim.z, z = blockIdx.z;
+  const int blk0 = (int)((int64_t)nblk_all * z / Z), blk1 = (int)((int64_t)nblk_all * (z + 1) / Z);
   const uint16_t* kbase = kc + (int64_t)g * max_ctx * HD;
   const uint16_t* vbase = vc + (int64_t)g * max_ctx * HD;
 
@@ -235,12 +246,14 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
     }
   };
 
-  gload(0);
-  lstore(0);
+  if (blk0 < blk1) {
+    gload(blk0);
+    lstore(0);
+  }
   __syncthreads();
-  for (int blk = 0; blk < nblk; ++blk) {
-    const int buf = blk & 1;
-    if (blk + 1 < nblk) gload(blk + 1);
+  for (int blk = blk0; blk < blk1; ++blk) {
+    const int buf = (blk - blk0) & 1;
+    if (blk + 1 < blk1) gload(blk + 1);
 
     // S^T[key][query] for the 32 keys of this block.
     f32x16 st;
@@ -262,11 +275,15 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
     }
     mb = fmaxf(mb, __shfl_xor(mb, 32));
     const float m_new = fmaxf(m_run, mb);
-    const float alpha = exp2f(m_run - m_new);  // 0 on the first block (m_run = -inf, m_new finite)
+    // Until a visible key has been seen (possible in a later key split) the
+    // maximum is -inf; 0 then stands in as reference so that every
+    // probability, and the rescale of the empty state, is exactly 0.
+    const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(m_run - m_ref);  // 0 while m_run = -inf
     float ls = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const float pv = exp2f(st[v] - m_new);
+      const float pv = exp2f(st[v] - m_ref);
       st[v] = pv;
       ls += pv;
     }
@@ -300,10 +317,25 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
         o[d] = mfma32(v4u{lo.x, lo.y, hi.x, hi.y}, pf[sidx], o[d]);
       }
     }
-    if (blk + 1 < nblk) lstore(buf ^ 1);
+    if (blk + 1 < blk1) lstore(buf ^ 1);
     __syncthreads();
   }
 
+  if (Z > 1) {  // unnormalised partial of this key split
+    if (qok) {
+      const int64_t r = ((int64_t)z * T + qi) * nq + h;
+      float* dst = part_acc + r * HD;
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = o[d][v];
+      if (half_sel == 0) {
+        part_ml[r * 2] = m_run;
+        part_ml[r * 2 + 1] = l_run;
+      }
+    }
+    return;
+  }
   if (qok) {
     const float inv = 1.0f / l_run;
     uint16_t* dst = out + ((int64_t)qi * nq + h) * HD;
@@ -312,6 +344,32 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
 #pragma unroll
       for (int v = 0; v < 16; ++v) dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = to_f16(o[d][v] * inv);
   }
+}
+
+// Merge of Z key splits: o[q][h][d] = sum_z 2^(m_z - M) acc_z[d] / sum_z 2^(m_z - M) l_z
+// (a split without keys has m = -inf, l = 0 and weight 0).  One thread per 4 dims.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_prefill_combine_kernel(const float* part_acc, const float* part_ml,
+                                                                   uint16_t* out, int rows, int Z) {
+  const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;  // over rows * HD/4
+  if (e >= (int64_t)rows * (HD / 4)) return;
+  const int64_t r = e / (HD / 4);
+  const int d4 = (int)(e % (HD / 4));
+  float M = -INFINITY;
+  for (int z = 0; z < Z; ++z) {
+    const float m = part_ml[((int64_t)z * rows + r) * 2], l = part_ml[((int64_t)z * rows + r) * 2 + 1];
+    if (l > 0.f) M = fmaxf(M, m);
+  }
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+  float L = 0.f;
+  for (int z = 0; z < Z; ++z) {
+    const float m = part_ml[((int64_t)z * rows + r) * 2], l = part_ml[((int64_t)z * rows + r) * 2 + 1];
+    const float w = l > 0.f ? exp2f(m - M) : 0.f;
+    acc += w * reinterpret_cast<const v4f*>(part_acc + ((int64_t)z * rows + r) * HD)[d4];
+    L += w * l;
+  }
+  acc *= 1.0f / L;
+  reinterpret_cast<uint2*>(out + r * HD)[d4] = uint2{pack_f16(acc.x, acc.y), pack_f16(acc.z, acc.w)};
 }
 
 // ------------------------------------------------------------------ final copy
@@ -342,7 +400,8 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   const int64_t part_qkv = (int64_t)gemm_splitk(kGemmPartialF32, a.T, (int)nqkv, H) * T * nqkv;
   const int64_t part_o = (int64_t)gemm_splitk(kGemmPartialF32, a.T, H, a.nq * a.hd) * T * H;
   const int64_t part_d = (int64_t)gemm_splitk(kGemmPartialF32, a.T, H, a.F) * T * H;
-  const int64_t part = std::max(part_qkv, std::max(part_o, part_d));
+  const int64_t part_attn = (int64_t)KF_PF_ATTN_SPLIT * T * a.nq * (a.hd + 2);  // key-split attention partials
+  const int64_t part = std::max(std::max(part_qkv, part_attn), std::max(part_o, part_d));
   const int64_t sz_x = a256(T * H * 4), sz_xn = a256(T * H * 2), sz_part = a256(part * 4),
                 sz_q = a256(T * a.nq * a.hd * 2), sz_o = a256(T * a.nq * a.hd * 2), sz_act = a256(T * a.F * 2);
   const int64_t total = sz_x + sz_xn + sz_part + sz_q + sz_o + sz_act;
@@ -401,18 +460,31 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   tr.end(ROPE);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));
-  const dim3 ag((T + 127) / 128, a.nq);
+  // Key splits: enough workgroups for two per CU when the chunk alone gives fewer.
+  const int qtiles = (T + 127) / 128;
+  const int Z = qtiles * a.nq >= 512 ? 1 : KF_PF_ATTN_SPLIT;
+  const dim3 ag(qtiles, a.nq, Z);
+  float* pacc = ws.part;
+  float* pml = ws.part + (int64_t)Z * T * a.nq * a.hd;
   tr.begin(ATTN);
   if (a.hd == 128)
-    hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, T, a.nq, a.nkv, a.pos0,
-                       a.max_ctx, sl2);
+    hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, pacc, pml, T, a.nq,
+                       a.nkv, a.pos0, a.max_ctx, sl2);
   else if (a.hd == 64)
-    hipLaunchKernelGGL(attn_prefill_kernel<64>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, T, a.nq, a.nkv, a.pos0,
-                       a.max_ctx, sl2);
+    hipLaunchKernelGGL(attn_prefill_kernel<64>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, pacc, pml, T, a.nq,
+                       a.nkv, a.pos0, a.max_ctx, sl2);
   else
     return hipErrorInvalidValue;
-  tr.end(ATTN);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (Z > 1) {
+    const int rows = T * a.nq;
+    const int64_t n = (int64_t)rows * (a.hd / 4);
+    const dim3 cg((unsigned)((n + 255) / 256));
+    if (a.hd == 128) hipLaunchKernelGGL(attn_prefill_combine_kernel<128>, cg, dim3(256), 0, s, pacc, pml, ws.o, rows, Z);
+    else hipLaunchKernelGGL(attn_prefill_combine_kernel<64>, cg, dim3(256), 0, s, pacc, pml, ws.o, rows, Z);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  tr.end(ATTN);
   // O and down: split along K into slices that the next norm (or the output
   // store) adds in order; an unsplit projection adds into x directly.
   auto resid_proj = [&](int cls, const uint16_t* A, const uint16_t* W, int K, int* pend) {
