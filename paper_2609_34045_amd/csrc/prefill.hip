@@ -209,12 +209,16 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
     for (int v = 0; v < 16; ++v) o[d][v] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Staging: 32 keys x HD elements for K and V; a thread moves 16 B of each.
+  // Staging: 32 keys x HD elements for K and V.  K: a thread moves 16-byte
+  // chunks (key, ch).  V is stored transposed (Vt[d][key]): a thread loads the
+  // same 16-byte chunk of two adjacent keys and writes, for each of its 8 d, one
+  // 32-bit word holding both keys (consecutive lanes: consecutive key pairs).
   // Global loads for the next block are issued before this block's MFMAs and
   // written to the other LDS buffer after them.
   constexpr int CH = HD / 8;               // 16-byte chunks per key
   constexpr int PER = (KB * CH + 255) / 256;
-  v4u rk[PER], rv[PER];
+  constexpr int VPER = (KB / 2 * CH + 255) / 256;
+  v4u rk[PER], rv0[VPER], rv1[VPER];
   auto gload = [&](int blk) {
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
@@ -222,10 +226,18 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
       const int key = idx / CH, ch = idx % CH;
       const int pos = blk * KB + key;
       rk[r] = v4u{0u, 0u, 0u, 0u};
-      rv[r] = v4u{0u, 0u, 0u, 0u};
-      if (idx < KB * CH && pos < nkeys) {
-        rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)pos * HD + ch * 8);
-        rv[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)pos * HD + ch * 8);
+      if (idx < KB * CH && pos < nkeys) rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)pos * HD + ch * 8);
+    }
+#pragma unroll
+    for (int r = 0; r < VPER; ++r) {
+      const int idx = tid + 256 * r;
+      const int kp = idx % (KB / 2), ch = idx / (KB / 2);
+      const int pos = blk * KB + 2 * kp;
+      rv0[r] = v4u{0u, 0u, 0u, 0u};
+      rv1[r] = v4u{0u, 0u, 0u, 0u};
+      if (idx < KB / 2 * CH) {
+        if (pos < nkeys) rv0[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)pos * HD + ch * 8);
+        if (pos + 1 < nkeys) rv1[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)(pos + 1) * HD + ch * 8);
       }
     }
   };
@@ -236,11 +248,22 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
       if (idx < KB * CH) {
         const int key = idx / CH, ch = idx % CH;
         *reinterpret_cast<v4u*>(&Ks[buf][key * LDK + ch * 8]) = rk[r];
-        const uint32_t w[4] = {rv[r].x, rv[r].y, rv[r].z, rv[r].w};
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < VPER; ++r) {
+      const int idx = tid + 256 * r;
+      if (idx < KB / 2 * CH) {
+        const int kp = idx % (KB / 2), ch = idx / (KB / 2);
+        const uint32_t a[4] = {rv0[r].x, rv0[r].y, rv0[r].z, rv0[r].w};
+        const uint32_t b[4] = {rv1[r].x, rv1[r].y, rv1[r].z, rv1[r].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          Vt[buf][(ch * 8 + 2 * e) * LDV + key] = (uint16_t)(w[e] & 0xffffu);
-          Vt[buf][(ch * 8 + 2 * e + 1) * LDV + key] = (uint16_t)(w[e] >> 16);
+          // d = ch*8 + 2e holds the low halves, d + 1 the high halves
+          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * LDV + 2 * kp]) =
+              (a[e] & 0xffffu) | (b[e] << 16);
+          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * LDV + 2 * kp]) =
+              (a[e] >> 16) | (b[e] & 0xffff0000u);
         }
       }
     }
