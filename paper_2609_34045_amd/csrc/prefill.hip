@@ -164,12 +164,17 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
 // two per CU): split z takes key blocks [z nblk / Z, (z+1) nblk / Z) and, when
 // Z > 1, writes its unnormalised output and (max, sum) per query to part_acc /
 // part_ml for attn_prefill_combine_kernel.
+#ifndef KF_PF_ATTN_KB
+#define KF_PF_ATTN_KB 64
+#endif
 template <int HD>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
+__global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
                                                            const uint16_t* vc, uint16_t* out, float* part_acc,
                                                            float* part_ml, int T, int nq, int nkv, int pos0,
                                                            int max_ctx, float scale_log2) {
-  constexpr int KB = 32;            // keys per block
+  constexpr int KB = KF_PF_ATTN_KB;  // keys per block: KB / 32 tiles of 32 keys
+  constexpr int NT = KB / 32;
+  static_assert(KB == 32 || KB == 64, "32 or 64 keys per block");
   constexpr int LDK = HD + 8;       // K tile row stride (fp16 elements)
   constexpr int LDV = KB + 4;       // V^T tile row stride (fp16 elements), keeps 8-byte alignment
   constexpr int DB = HD / 32;       // 32-row d-blocks of O^T
@@ -278,24 +283,29 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
     const int buf = (blk - blk0) & 1;
     if (blk + 1 < blk1) gload(blk + 1);
 
-    // S^T[key][query] for the 32 keys of this block.
-    f32x16 st;
+    // S^T[key][query] for each 32-key tile of this block.
+    f32x16 st[NT];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) st[v] = 0.f;
+    for (int t = 0; t < NT; ++t) {
 #pragma unroll
-    for (int s = 0; s < HD / 16; ++s) {
-      const v4u kf = *reinterpret_cast<const v4u*>(&Ks[buf][(lane & 31) * LDK + 16 * s + 8 * half_sel]);
-      st = mfma32(kf, qf[s], st);
+      for (int v = 0; v < 16; ++v) st[t][v] = 0.f;
+#pragma unroll
+      for (int s = 0; s < HD / 16; ++s) {
+        const v4u kf = *reinterpret_cast<const v4u*>(&Ks[buf][(32 * t + (lane & 31)) * LDK + 16 * s + 8 * half_sel]);
+        st[t] = mfma32(kf, qf[s], st[t]);
+      }
     }
-    // Lane holds keys kk(v) = 8 (v/4) + 4 half_sel + v%4 of its query.
+    // Lane holds keys 32 t + 8 (v/4) + 4 half_sel + v%4 of its query.
     float mb = -INFINITY;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int key = blk * KB + 8 * (v >> 2) + 4 * half_sel + (v & 3);
-      const float sv = (key <= qpos) ? st[v] * scale_log2 : -INFINITY;
-      st[v] = sv;
-      mb = fmaxf(mb, sv);
-    }
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = blk * KB + 32 * t + 8 * (v >> 2) + 4 * half_sel + (v & 3);
+        const float sv = (key <= qpos) ? st[t][v] * scale_log2 : -INFINITY;
+        st[t][v] = sv;
+        mb = fmaxf(mb, sv);
+      }
     mb = fmaxf(mb, __shfl_xor(mb, 32));
     const float m_new = fmaxf(m_run, mb);
     // Until a visible key has been seen (possible in a later key split) the
@@ -305,11 +315,13 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
     const float alpha = exp2f(m_run - m_ref);  // 0 while m_run = -inf
     float ls = 0.f;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const float pv = exp2f(st[v] - m_ref);
-      st[v] = pv;
-      ls += pv;
-    }
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float pv = exp2f(st[t][v] - m_ref);
+        st[t][v] = pv;
+        ls += pv;
+      }
     ls += __shfl_xor(ls, 32);
     l_run = l_run * alpha + ls;
     m_run = m_new;
@@ -318,27 +330,31 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const uint16_t* q, co
 #pragma unroll
       for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
 
-    // P^T fragments: step 0 takes v = 0..7, step 1 takes v = 8..15 (the MFMA's
-    // k index runs over the keys this lane holds, in that order).
-    v4u pf[2];
+    // P^T fragments of tile t: step 0 takes v = 0..7, step 1 takes v = 8..15 (the
+    // MFMA's k index runs over the keys this lane holds, in that order).
+    v4u pf[NT][2];
 #pragma unroll
-    for (int sidx = 0; sidx < 2; ++sidx) {
-      uint32_t w[4];
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        w[e] = pack_f16(st[8 * sidx + 2 * e], st[8 * sidx + 2 * e + 1]);
-      pf[sidx] = v4u{w[0], w[1], w[2], w[3]};
-    }
-    // V^T fragments with the same key order: keys 16 sidx + 4 half_sel + {0..3} and 16 sidx + 8 + 4 half_sel + {0..3}.
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_f16(st[t][8 * sidx + 2 * e], st[t][8 * sidx + 2 * e + 1]);
+        pf[t][sidx] = v4u{w[0], w[1], w[2], w[3]};
+      }
+    // V^T fragments with the same key order: keys 32 t + 16 sidx + 4 half_sel + {0..3}
+    // and 32 t + 16 sidx + 8 + 4 half_sel + {0..3}.
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
       const uint16_t* vrow = &Vt[buf][(32 * d + (lane & 31)) * LDV];
 #pragma unroll
-      for (int sidx = 0; sidx < 2; ++sidx) {
-        const v2u lo = *reinterpret_cast<const v2u*>(vrow + 16 * sidx + 4 * half_sel);
-        const v2u hi = *reinterpret_cast<const v2u*>(vrow + 16 * sidx + 8 + 4 * half_sel);
-        o[d] = mfma32(v4u{lo.x, lo.y, hi.x, hi.y}, pf[sidx], o[d]);
-      }
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int sidx = 0; sidx < 2; ++sidx) {
+          const v2u lo = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 4 * half_sel);
+          const v2u hi = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 8 + 4 * half_sel);
+          o[d] = mfma32(v4u{lo.x, lo.y, hi.x, hi.y}, pf[t][sidx], o[d]);
+        }
     }
     if (blk + 1 < blk1) lstore(buf ^ 1);
     __syncthreads();
