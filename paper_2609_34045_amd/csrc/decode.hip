@@ -301,8 +301,15 @@ __device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, in
   }
 }
 
+#ifndef KF_GEMV_MIN_WAVES
+#define KF_GEMV_MIN_WAVES 4
+#endif
+// The weight bytes in flight per CU scale with resident waves; at batch 3-4 the
+// input rows and partial sums put the kernel just past 128 VGPRs (3 waves per
+// SIMD), so the register budget is held to 4 waves.
 template <int B, int R, int U, int EPI, bool NORM, bool SRC = false>
-__global__ __launch_bounds__(256) void gemv_kernel(const GemvParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KF_GEMV_MIN_WAVES)))
+void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
   constexpr int NV = R * B + (NORM ? B : 0);
   constexpr int NVP = NV <= 8 ? 8 : NV <= 16 ? 16 : NV <= 32 ? 32 : 64;
@@ -853,13 +860,13 @@ static hipError_t gemv_dispatch_src(int epi, bool norm, const GemvParams& p, int
   return hipGetLastError();
 }
 
-template <int R, int U>
+template <int R, int U, bool SRC>
 static hipError_t gemv_dispatch_b(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
   switch (p.batch) {
-    case 1: return gemv_dispatch_epi<1, R, U>(epi, norm, p, grid, s);
-    case 2: return gemv_dispatch_epi<2, R, U>(epi, norm, p, grid, s);
-    case 3: return gemv_dispatch_epi<3, R, U>(epi, norm, p, grid, s);
-    case 4: return gemv_dispatch_epi<4, R, U>(epi, norm, p, grid, s);
+    case 1: return SRC ? gemv_dispatch_src<1, R, U>(epi, norm, p, grid, s) : gemv_dispatch_epi<1, R, U>(epi, norm, p, grid, s);
+    case 2: return SRC ? gemv_dispatch_src<2, R, U>(epi, norm, p, grid, s) : gemv_dispatch_epi<2, R, U>(epi, norm, p, grid, s);
+    case 3: return SRC ? gemv_dispatch_src<3, R, U>(epi, norm, p, grid, s) : gemv_dispatch_epi<3, R, U>(epi, norm, p, grid, s);
+    case 4: return SRC ? gemv_dispatch_src<4, R, U>(epi, norm, p, grid, s) : gemv_dispatch_epi<4, R, U>(epi, norm, p, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -874,23 +881,14 @@ int gemv_grid(int epi, int R, const GemvParams& p) {
 
 hipError_t launch_gemv_src(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
   if ((p.src == nullptr) == (p.tokens == nullptr)) return hipErrorInvalidValue;
-  if (R != 8 || U != 1) return hipErrorInvalidValue;
   const int grid = gemv_grid(epi, R, p);
-  switch (p.batch) {
-    case 1: return gemv_dispatch_src<1, 8, 1>(epi, norm, p, grid, s);
-    case 2: return gemv_dispatch_src<2, 8, 1>(epi, norm, p, grid, s);
-    case 3: return gemv_dispatch_src<3, 8, 1>(epi, norm, p, grid, s);
-    case 4: return gemv_dispatch_src<4, 8, 1>(epi, norm, p, grid, s);
-    default: return hipErrorInvalidValue;
-  }
+  if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, true>(epi, norm, p, grid, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
   const int grid = gemv_grid(epi, R, p);
-  if (R == 8 && U == 1) return gemv_dispatch_b<8, 1>(epi, norm, p, grid, s);
-  if (R == 8 && U == 2) return gemv_dispatch_b<8, 2>(epi, norm, p, grid, s);
-  if (R == 4 && U == 2) return gemv_dispatch_b<4, 2>(epi, norm, p, grid, s);
-  if (R == 4 && U == 4) return gemv_dispatch_b<4, 4>(epi, norm, p, grid, s);
+  if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
   return hipErrorInvalidValue;
 }
 
