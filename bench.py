@@ -50,6 +50,9 @@ def parse():
                     help="skip the per-launch HIP-event pass (no roofline figure)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB (counter calibration)")
+    ap.add_argument("--cost-model", action="store_true",
+                    help="probe bandwidth and dispatch overhead, then compare eq. (2)'s stage-time prediction with "
+                         "measured batch-1 stage times (8B-shaped stages of 1-16 blocks and with the head, 32B, 70B)")
     ap.add_argument("--prefill", action="store_true",
                     help="time the workload's prefill chunk (matrix cores) instead of decode")
     return ap.parse_args()
@@ -199,6 +202,79 @@ def cpu_baseline(wl, model_layers, kv_inject, hidden_steps, budget_s: float):
 
 
 # ------------------------------------------------------------------ main
+def bench_cost_model(args, torch, kf):
+    """Section V-A's cost model on this GPU: probe b and o, predict stage times by eq. (2), measure them.
+
+    Each stage runs batch-1 decode with a cache of `ctx` keys per layer (zeros:
+    timing does not depend on the values).  Timing follows the paper's rule: five
+    runs of 16 steps, the first discarded, the median of the rest.  Weight
+    values do not affect timing either, so every layer of a stage reuses one
+    seeded layer's tensors (each still gets its own device copy).
+    """
+    from paper_2609_34045_amd import planner
+    bw = planner.probe_bandwidth(4 << 30, reps=5)
+    o = planner.probe_overhead(reps=5)
+    log(f"[cost] probe: bandwidth {bw / 1e9:.1f} GB/s, dispatch overhead {o * 1e6:.2f} us")
+    cases = [("8b", 1, False, 2048), ("8b", 2, False, 2048), ("8b", 4, False, 2048), ("8b", 8, False, 2048),
+             ("8b", 16, False, 2048), ("8b", 4, True, 2048), ("32b", 4, False, 4096), ("32b", 16, False, 4096),
+             ("70b", 2, False, 4096), ("70b", 10, False, 4096)]
+    shapes = {"8b": (synth.SHAPE_8B, 2), "32b": (synth.SHAPE_32B, 4), "70b": (synth.SHAPE_70B, 5)}
+    layer_cache, head_cache, rows = {}, {}, []
+    steps, runs = 16, 5
+    for name, n, has_head, ctx in cases:
+        shape, cfg_id = shapes[name]
+        if name not in layer_cache:
+            layer_cache[name] = synth.layer_weights(shape, cfg_id, 0)
+        if has_head and name not in head_cache:
+            head_cache[name] = synth.head_weights(shape, cfg_id)
+        lo = 0 if has_head else shape.n_layers // 4
+        g = kf.Stage(shape, lo, lo + n, {l: layer_cache[name] for l in range(lo, lo + n)},
+                     head_cache[name] if has_head else None)
+        kv = g.kv(1, ctx + steps + 1)
+        z = torch.zeros((ctx, shape.n_kv_heads, shape.head_dim), dtype=torch.int16, device="cuda")
+        for l in range(lo, lo + n):
+            kv.write(l, 0, 0, z, z)
+        hid = torch.from_numpy(synth.hidden_states(cfg_id, synth.STREAM_DECODE_HIDDEN, 0, 1, shape.hidden)).cuda()
+        out = torch.empty((1, shape.hidden), dtype=torch.float32, device="cuda")
+        tok = torch.zeros(1, dtype=torch.int32, device="cuda")
+        times = []
+        for r in range(runs):
+            kv.set_len(0, ctx)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for i in range(steps):
+                if has_head:
+                    g.decode(kv, [0], [ctx + i], tokens=tok, out=out)
+                    tok = g.head_argmax(out)
+                else:
+                    g.decode(kv, [0], [ctx + i], hidden=hid, out=out)
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e-3 / steps)
+        g.sync()
+        measured = float(np.median(times[1:]))
+        costs = planner.stage_costs(shape, 1, ctx + steps + 1)
+        member = dict(o=o, bw=bw, flops=0.0, room=0)
+        predicted = planner.stage_cost(costs, member, n, has_head)
+        rows.append({"stage": f"{name} x{n}" + (" + head" if has_head else ""), "blocks": n, "head": has_head,
+                     "context": ctx, "predicted_us": round(predicted * 1e6, 1), "measured_us": round(measured * 1e6, 1),
+                     "error": round((predicted - measured) / measured, 4),
+                     "kernel_launches_per_step": 5 * n + (2 if has_head else 0)})
+        log(f"[cost] {rows[-1]}")
+        kv.close()
+        g.close()
+        del z, hid, out
+    errs = sorted(abs(r["error"]) for r in rows)
+    print(json.dumps({
+        "metric": "eq. (2) stage-time prediction vs measured (batch-1 decode)",
+        "probe": {"bandwidth_gbps": round(bw / 1e9, 1), "overhead_us": round(o * 1e6, 3), "bandwidth_buffer_gib": 4},
+        "rows": rows,
+        "median_abs_error": errs[len(errs) // 2] if len(errs) % 2 else 0.5 * (errs[len(errs) // 2 - 1] + errs[len(errs) // 2]),
+        "timing": f"{runs} runs of {steps} steps, first discarded, median",
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -220,6 +296,9 @@ def main():
         torch.cuda.synchronize()
         del a, b
         log(f"[bench] copied {args.copy_calibration_mb} MiB three times (calibration)")
+    if args.cost_model:
+        torch.cuda.set_device(0)
+        return bench_cost_model(args, torch, kf)
     wl = synth.WORKLOADS[args.workload]
     if args.prefill:
         if not wl.prefill_chunk:

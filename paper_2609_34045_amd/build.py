@@ -1,8 +1,8 @@
 """Build ``libkafila_stage.so`` (HIP sources for gfx950) in-tree.
 
-Usage: ``python -m paper_2609_34045_amd.build``.  Each ``csrc/*.hip`` is
-compiled to an object under ``_build/`` with hipcc, then linked into the
-shared library next to this file, where the binding loads it.
+Usage: ``python -m paper_2609_34045_amd.build``.  Each ``csrc/*.hip`` and
+``csrc/*.cpp`` is compiled to an object under ``_build/`` with hipcc, then
+linked into the shared library next to this file, where the binding loads it.
 """
 from __future__ import annotations
 
@@ -30,7 +30,7 @@ FLAGS = [
 
 
 def _compile(src: str, build_dir: str = BUILD, extra=()) -> str:
-    obj = os.path.join(build_dir, os.path.basename(src).replace(".hip", ".o"))
+    obj = os.path.join(build_dir, os.path.splitext(os.path.basename(src))[0] + ".o")
     cmd = [HIPCC, *FLAGS, *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -41,7 +41,8 @@ def _compile(src: str, build_dir: str = BUILD, extra=()) -> str:
 def build(verbose: bool = False, out: str = LIB, extra=(), build_dir: str = BUILD) -> str:
     """Compile and link; ``out``/``extra``/``build_dir`` let a caller build a variant elsewhere."""
     os.makedirs(build_dir, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    # .hip: kernels and the runtime that launches them; .cpp: host-only parts (planner, errors).
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(lambda f: _compile(f, build_dir, extra), srcs))
     tmp = out + ".tmp%d" % os.getpid()

@@ -9,6 +9,8 @@
 #include <string>
 #include <vector>
 
+#include "error.h"
+#include "kafila_planner.h"
 #include "kafila_stage.h"
 #include "kernels.h"
 #include "prefill.h"
@@ -46,18 +48,6 @@ using namespace kf;
 #ifndef KF_ATTN_ALIGN
 #define KF_ATTN_ALIGN 64
 #endif
-
-static thread_local std::string g_err;
-
-static kf_status fail(kf_status code, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_err = buf;
-  return code;
-}
 
 #define KF_HIP(call, what)                                                                  \
   do {                                                                                      \
@@ -205,8 +195,6 @@ extern "C" {
 
 int32_t kf_abi_version(void) { return KF_ABI_VERSION; }
 
-const char* kf_last_error(void) { return g_err.c_str(); }
-
 kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t lo, int32_t hi, int32_t has_head, int32_t max_users,
                          int32_t max_ctx, int64_t* beta_block, int64_t* beta_head, int64_t* resident) {
   kf_status st = check_cfg(cfg, lo, hi);
@@ -218,6 +206,28 @@ kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t lo, int32_t hi, int
   if (resident)
     *resident = (int64_t)(hi - lo) * bb + hb + decode_ws_bytes(*cfg, has_head) +
                 (max_users > 0 && max_ctx > 0 ? kv_bytes(*cfg, hi - lo, max_users, max_ctx) : 0);
+  return KF_OK;
+}
+
+kf_status kf_stage_costs(const kf_model_config* cfg, int32_t max_users, int32_t max_ctx, kf_model_costs* out) {
+  kf_status st = check_cfg(cfg, 0, 1);
+  if (st != KF_OK && st != KF_EUNSUPPORTED) return st;
+  if (!out) return fail(KF_EINVAL, "out is NULL");
+  if (max_users < 0 || max_ctx < 0) return fail(KF_EINVAL, "max_users and max_ctx must be >= 0");
+  const kf_model_config& c = *cfg;
+  const bool kv = max_users > 0 && max_ctx > 0;
+  const int64_t bb = block_bytes(c), hb = head_bytes(c);
+  // kf_stage_bytes' resident for one and two blocks, without and with the head: the
+  // per-block share is the difference (weights + that layer's KV), the rest is per stage.
+  const int64_t r1 = bb + decode_ws_bytes(c, 0) + (kv ? kv_bytes(c, 1, max_users, max_ctx) : 0);
+  const int64_t r2 = 2 * bb + decode_ws_bytes(c, 0) + (kv ? kv_bytes(c, 2, max_users, max_ctx) : 0);
+  const int64_t r1h = r1 + hb + decode_ws_bytes(c, 1) - decode_ws_bytes(c, 0);
+  out->beta_block = bb;
+  out->beta_head = hb;
+  out->block_resident = r2 - r1;
+  out->stage_resident = r1 - (r2 - r1);
+  out->head_resident = r1h - r1;
+  out->flops_block = 2.0 * (double)(bb / 2);  // two flops per bf16 weight at batch 1
   return KF_OK;
 }
 
@@ -356,7 +366,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   }
   s->err_flag = (int*)take(4);
   *out = s;
-  g_err.clear();
+  clear_error();
   return KF_OK;
 }
 

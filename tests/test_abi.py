@@ -12,7 +12,8 @@ import pytest
 import synth
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "kafila_stage.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 
 @pytest.fixture(scope="module")
@@ -22,22 +23,24 @@ def lib():
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kf_[a-z_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(kf_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("kf_stage_init", "kf_stage_prefill", "kf_stage_decode", "kf_head_logits", "kf_head_argmax",
-              "kf_kv_create", "kf_stage_bytes", "kf_last_error"):
+              "kf_kv_create", "kf_stage_bytes", "kf_last_error", "kf_partition", "kf_plan", "kf_probe_bandwidth"):
         assert n in names
 
 
 def test_library_exports_every_declared_symbol(lib):
-    from paper_2609_34045_amd import stage
+    from paper_2609_34045_amd import planner, stage
     names = declared_functions()
-    assert set(names) == set(stage.EXPORTS)
+    assert set(names) == set(stage.EXPORTS) | set(planner.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
 
