@@ -167,6 +167,10 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
 #ifndef KF_PF_ATTN_KB
 #define KF_PF_ATTN_KB 64
 #endif
+#ifndef KF_PF_ATTN_RING
+#define KF_PF_ATTN_RING 4
+#endif
+constexpr int kRing = KF_PF_ATTN_RING;  // LDS fragment reads in flight ahead of the MFMAs
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
                                                            const uint16_t* vc, uint16_t* out, float* part_acc,
@@ -181,9 +185,23 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KB * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = blockIdx.y, g = h / (nq / nkv);
-  const int i0 = blockIdx.x * 128;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // Workgroups go to the 8 XCDs round-robin by linear id.  Numbering the work
+  // XCD-major (logical id = xcd * n / 8 + slot) puts the workgroups of one KV
+  // group on as few XCDs as possible, so that group's K and V stay in one L2.
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  {
+    const int nx = gridDim.x, ny = gridDim.y, n = nx * ny * gridDim.z;
+    const int lin = bx + nx * (by + ny * bz);
+    if (n % 8 == 0) {
+      const int l = (lin % 8) * (n / 8) + lin / 8;  // z slowest within a head, then query tile
+      bz = l % gridDim.z;
+      bx = (l / gridDim.z) % nx;
+      by = l / (gridDim.z * nx);
+    }
+  }
+  const int h = by, g = h / (nq / nkv);
+  const int i0 = bx * 128;
   const int qi = i0 + wave * 32 + (lane & 31);  // this lane's query (chunk index)
   const int half_sel = lane >> 5;
   const bool qok = qi < T;
@@ -191,7 +209,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   const int last_q = min(i0 + 127, T - 1);
   const int nkeys = pos0 + last_q + 1;  // keys visible to the workgroup's last query
   const int nblk_all = (nkeys + KB - 1) / KB;
-  const int Z = gridDim.z, z = blockIdx.z;
+  const int Z = gridDim.z, z = bz;
   const int blk0 = (int)((int64_t)nblk_all * z / Z), blk1 = (int)((int64_t)nblk_all * (z + 1) / Z);
   const uint16_t* kbase = kc + (int64_t)g * max_ctx * HD;
   const uint16_t* vbase = vc + (int64_t)g * max_ctx * HD;
@@ -283,52 +301,83 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     const int buf = (blk - blk0) & 1;
     if (blk + 1 < blk1) gload(blk + 1);
 
-    // S^T[key][query] for each 32-key tile of this block.
+    // S^T[key][query] for each 32-key tile of this block.  The K fragments
+    // go through a ring of kRing registers: the read for MFMA i + kRing is
+    // issued before MFMA i, so LDS latency hides behind the MFMAs in flight.
     f32x16 st[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) st[t][v] = 0.f;
-#pragma unroll
-      for (int s = 0; s < HD / 16; ++s) {
-        const v4u kf = *reinterpret_cast<const v4u*>(&Ks[buf][(32 * t + (lane & 31)) * LDK + 16 * s + 8 * half_sel]);
-        st[t] = mfma32(kf, qf[s], st[t]);
-      }
-    }
-    // Lane holds keys 32 t + 8 (v/4) + 4 half_sel + v%4 of its query.
-    float mb = -INFINITY;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = blk * KB + 32 * t + 8 * (v >> 2) + 4 * half_sel + (v & 3);
-        const float sv = (key <= qpos) ? st[t][v] * scale_log2 : -INFINITY;
-        st[t][v] = sv;
-        mb = fmaxf(mb, sv);
+      for (int v = 0; v < 16; ++v) st[t][v] = 0.f;
+    {
+      constexpr int NS = HD / 16, NI = NT * NS;
+      auto kread = [&](int i) {
+        const int t = i / NS, s = i % NS;
+        return *reinterpret_cast<const v4u*>(&Ks[buf][(32 * t + (lane & 31)) * LDK + 16 * s + 8 * half_sel]);
+      };
+      v4u ring[kRing];
+#pragma unroll
+      for (int i = 0; i < kRing; ++i) ring[i] = kread(i);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const v4u cur = ring[i % kRing];
+        if (i + kRing < NI) ring[i % kRing] = kread(i + kRing);
+        st[i / NS] = mfma32(cur, qf[i % NS], st[i / NS]);
       }
+      // Order: the kRing prologue reads, then MFMA i followed by the read for i + kRing.
+      __builtin_amdgcn_sched_group_barrier(0x100, kRing, 0);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i + kRing < NI) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+    }
+    // Lane holds keys 32 t + 8 (v/4) + 4 half_sel + v%4 of its query.  Scores
+    // stay unscaled here: the scale (> 0) commutes with the maximum and is
+    // folded into the exponent's fma below.  Only blocks that reach past the
+    // wave's first query need the causal mask.
+    float mb = -INFINITY;
+    if (blk * KB + KB - 1 <= pos0 + i0 + wave * 32) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mb = fmaxf(mb, st[t][v]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = blk * KB + 32 * t + 8 * (v >> 2) + 4 * half_sel + (v & 3);
+          const float sv = key <= qpos ? st[t][v] : -INFINITY;
+          st[t][v] = sv;
+          mb = fmaxf(mb, sv);
+        }
+    }
     mb = fmaxf(mb, __shfl_xor(mb, 32));
-    const float m_new = fmaxf(m_run, mb);
+    const float m_new = fmaxf(m_run, mb * scale_log2);
     // Until a visible key has been seen (possible in a later key split) the
     // maximum is -inf; 0 then stands in as reference so that every
     // probability, and the rescale of the empty state, is exactly 0.
     const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_ref);  // 0 while m_run = -inf
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);  // 0 while m_run = -inf
     float ls = 0.f;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float pv = exp2f(st[t][v] - m_ref);
+        const float pv = __builtin_amdgcn_exp2f(fmaf(st[t][v], scale_log2, -m_ref));
         st[t][v] = pv;
         ls += pv;
       }
     ls += __shfl_xor(ls, 32);
     l_run = l_run * alpha + ls;
     m_run = m_new;
+    if (__ballot(alpha != 1.0f)) {  // no lane's maximum moved: nothing to rescale
 #pragma unroll
-    for (int d = 0; d < DB; ++d)
+      for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
+        for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
+    }
 
     // P^T fragments of tile t: step 0 takes v = 0..7, step 1 takes v = 8..15 (the
     // MFMA's k index runs over the keys this lane holds, in that order).
@@ -343,18 +392,31 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
         pf[t][sidx] = v4u{w[0], w[1], w[2], w[3]};
       }
     // V^T fragments with the same key order: keys 32 t + 16 sidx + 4 half_sel + {0..3}
-    // and 32 t + 16 sidx + 8 + 4 half_sel + {0..3}.
+    // and 32 t + 16 sidx + 8 + 4 half_sel + {0..3}; read through the same kind of ring.
+    {
+      constexpr int NP = NT * 2, NI = DB * NP;  // MFMA i: d-block i / NP, (t, sidx) = i % NP
+      auto vread = [&](int i) {
+        const int d = i / NP, t = (i % NP) / 2, sidx = i % 2;
+        const uint16_t* vrow = &Vt[buf][(32 * d + (lane & 31)) * LDV];
+        const v2u lo = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 4 * half_sel);
+        const v2u hi = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 8 + 4 * half_sel);
+        return v4u{lo.x, lo.y, hi.x, hi.y};
+      };
+      v4u ring[kRing];
 #pragma unroll
-    for (int d = 0; d < DB; ++d) {
-      const uint16_t* vrow = &Vt[buf][(32 * d + (lane & 31)) * LDV];
+      for (int i = 0; i < kRing; ++i) ring[i] = vread(i);
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+      for (int i = 0; i < NI; ++i) {
+        const v4u cur = ring[i % kRing];
+        if (i + kRing < NI) ring[i % kRing] = vread(i + kRing);
+        o[i / NP] = mfma32(cur, pf[(i % NP) / 2][i % 2], o[i / NP]);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * kRing, 0);  // two LDS reads per fragment
 #pragma unroll
-        for (int sidx = 0; sidx < 2; ++sidx) {
-          const v2u lo = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 4 * half_sel);
-          const v2u hi = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 8 + 4 * half_sel);
-          o[d] = mfma32(v4u{lo.x, lo.y, hi.x, hi.y}, pf[t][sidx], o[d]);
-        }
+      for (int i = 0; i < NI; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i + kRing < NI) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
     }
     if (blk + 1 < blk1) lstore(buf ^ 1);
     __syncthreads();
