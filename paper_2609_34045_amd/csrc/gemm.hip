@@ -4,17 +4,17 @@
 // staged), both K-contiguous; the product runs on v_mfma_f32_32x32x16_f16 with
 // fp32 accumulation.  At a 512-token chunk the projections are large enough
 // to be bound by the matrix cores, which sets the tile shape:
-//   * 256 x 256 x 32 workgroup tiles, four waves (one per SIMD) of 128 x 128,
-//     16 accumulator blocks each (held in the accumulation registers): per K
-//     step a wave reads 16 KB of fragments from LDS for 32 MFMAs (about half
-//     of the LDS bandwidth at full rate);
+//   * 256 x 256 x 32 workgroup tiles, eight waves (two per SIMD) of 128 x 64,
+//     8 accumulator blocks each: per K step a wave reads 12 KB of fragments
+//     from LDS for 16 MFMAs.  Two waves per SIMD let one issue MFMAs while the
+//     other waits on LDS or the barrier (measured 4% faster than four waves of
+//     128 x 128 with 16 blocks each, which remains selectable);
 //   * operands go from global memory straight into a 4-stage LDS ring with
 //     global_load_lds (no register staging), so loads run three to four K
 //     steps (1.3 - 1.7 us of math at full rate) ahead; chunks are XOR-swizzled
 //     within a row so that fragment reads are free of bank conflicts;
-//   * with one wave per SIMD nothing else hides LDS latency, so each wave
-//     reads the fragments of the next 16-wide K slice while the MFMAs of the
-//     current one run;
+//   * each wave reads the fragments of the next 16-wide K slice while the
+//     MFMAs of the current one run;
 //   * weights stay bf16 in LDS and are converted to fp16 after the fragment
 //     read (exact; 12 ALU operations per 8 values, alongside the MFMAs);
 //   * narrow projections (few 256-wide column tiles) are split along K over
@@ -40,7 +40,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
 constexpr int BM = 256, BN = 256, BK = 32;
-constexpr int NT = 256;                     // threads per workgroup (4 waves, one per SIMD)
+#ifndef KF_GEMM_WN
+#define KF_GEMM_WN 4
+#endif
+// Waves along N: 2 gives four waves of 128 x 128 (one per SIMD), 4 gives eight
+// waves of 128 x 64 (two per SIMD, half the accumulators each).
+constexpr int kGemmWN = KF_GEMM_WN;
+constexpr int kGemmThreads = 128 * kGemmWN;
 #ifndef KF_GEMM_READS_PER_SLOT
 #define KF_GEMM_READS_PER_SLOT 1  // fragment reads issued per MFMA slot
 #endif
@@ -60,7 +66,6 @@ constexpr int STAGES = KF_GEMM_STAGES;      // LDS ring depth: loads run up to S
 static_assert(STAGES >= 3 && STAGES <= 5, "ring depth");
 constexpr int TILE_BYTES = BM * BK * 2;     // one operand's tile per stage (16 KB)
 constexpr int ROW_BYTES = BK * 2;           // 64 B: four 16-byte chunks per tile row
-constexpr int LOADS = TILE_BYTES / 1024 / 4;  // 1 KB direct loads per wave per operand per stage (4)
 
 __device__ __forceinline__ uint32_t pack_f16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, h2));
@@ -108,13 +113,19 @@ struct Params {
 };
 
 template <int EPI>
-__global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
+__global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
+  constexpr int WN = kGemmWN;
+  constexpr int NW = 2 * WN;                 // waves
+  constexpr int JW = 8 / WN;                 // 32-column blocks per wave (128 / 64 columns)
+  constexpr int LOADS = TILE_BYTES / 1024 / NW;  // 1 KB direct loads per wave per operand per stage
+  constexpr int SLOTS = 4 * JW;              // MFMAs per wave per 16-wide K slice
+  static_assert(WN == 2 || WN == 4, "four or eight waves");
   // STAGES x (A tile, W tile), each [256 rows][4 swizzled 16-byte chunks]; W stays bf16 here.
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * 2 * TILE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 128 x 128
+  const int wm = wave / WN, wn = wave % WN;  // 2 x WN waves of 128 x (256 / WN)
   const int mt = (p.M + BM - 1) / BM, nt = (p.N + BN - 1) / BN, ntiles = mt * nt;
   const int nwg = ntiles * p.splitk;
   // Tiles sharing a weight panel (same column tile) go to the same XCD, where
@@ -130,14 +141,14 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
   const int nk = k_end - k_begin;
 
   // Direct global -> LDS loads: load j of this wave fills tile rows
-  // 16 (4 j + wave) .. +15; lane l writes row 16 (4 j + wave) + l/4, slot l%4,
+  // 16 (NW j + wave) .. +15; lane l writes row 16 (NW j + wave) + l/4, slot l%4,
   // so it fetches the chunk that belongs in that slot.
   const int w_rows = EPI == kGemmSwiGLU ? (p.N >> 1) : p.N;
   const uint16_t* asrc[LOADS];
   const uint16_t* wsrc[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int r = 16 * (4 * j + wave) + (lane >> 2);
+    const int r = 16 * (NW * j + wave) + (lane >> 2);
     const int c = swz(r, lane & 3);
     const int ar = m0 + r < p.M ? m0 + r : p.M - 1;  // rows past M load a valid row; they are never stored
     asrc[j] = p.A + (int64_t)ar * K + (int64_t)k_begin * BK + c * 8;
@@ -159,16 +170,16 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
     uint8_t* wbuf = abuf + TILE_BYTES;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      __builtin_amdgcn_global_load_lds(asrc[j] + (int64_t)kt * BK, (lds_ptr)(abuf + 1024 * (4 * j + wave)), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(wsrc[j] + (int64_t)kt * BK, (lds_ptr)(wbuf + 1024 * (4 * j + wave)), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(asrc[j] + (int64_t)kt * BK, (lds_ptr)(abuf + 1024 * (NW * j + wave)), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(wsrc[j] + (int64_t)kt * BK, (lds_ptr)(wbuf + 1024 * (NW * j + wave)), 16, 0, 0);
     }
   };
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][JW];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < JW; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
@@ -177,45 +188,45 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
   // the barrier, one global->LDS load each), the last slots convert the weight
   // fragments read (whose reads have returned by then).
   const int rl = lane & 31, kh = lane >> 5;
-  // fragment read q (0..7) of sub-step s (16 values of K) of a stage: weight
-  // block q (still bf16) for q < 4, then A block q-4, so that the conversions
-  // wait only on the first four reads
-  auto read_frag = [&](int stage, int s, int q, v4u (&fa)[4], v4u (&fw)[4]) {
-    const bool w = q < 4;
+  // fragment read q (0..JW+3) of sub-step s (16 values of K) of a stage: weight
+  // block q (still bf16) for q < JW, then A block q-JW, so that the conversions
+  // wait only on the first JW reads
+  auto read_frag = [&](int stage, int s, int q, v4u (&fa)[4], v4u (&fw)[JW]) {
+    const bool w = q < JW;
     const uint8_t* buf = smem + stage * 2 * TILE_BYTES + (w ? TILE_BYTES : 0);
-    const int r = (w ? wn : wm) * 128 + 32 * (q & 3) + rl;
+    const int r = w ? wn * (32 * JW) + 32 * q + rl : wm * 128 + 32 * (q - JW) + rl;
     const v4u v = *reinterpret_cast<const v4u*>(buf + r * ROW_BYTES + swz(r, 2 * s + kh) * 16);
-    if (w) fw[q & 3] = v;
-    else fa[q & 3] = v;
+    if (w) fw[q] = v;
+    else fa[q - JW] = v;
   };
-  // conversion of dword d (0..15) of the weight fragments (fragment d/4)
-  auto convert_dword = [&](v4u (&fw)[4], int d) {
+  // conversion of dword d (0..4 JW - 1) of the weight fragments (fragment d/4)
+  auto convert_dword = [&](v4u (&fw)[JW], int d) {
     const uint32_t w = fw[d >> 2][d & 3];
     fw[d >> 2][d & 3] = pack_f16(__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u));
   };
-  // global->LDS load q (0..7) of step kt into a stage: A for even q, W for odd q
+  // global->LDS load q (0..2 LOADS - 1) of step kt into a stage: A for even q, W for odd q
   auto load_part = [&](int kt, int stage, int q) {
-    uint8_t* buf = smem + stage * 2 * TILE_BYTES + (q & 1) * TILE_BYTES + 1024 * (4 * (q >> 1) + wave);
+    uint8_t* buf = smem + stage * 2 * TILE_BYTES + (q & 1) * TILE_BYTES + 1024 * (NW * (q >> 1) + wave);
     const uint16_t* src = ((q & 1) ? wsrc[q >> 1] : asrc[q >> 1]) + (int64_t)kt * BK;
     __builtin_amdgcn_global_load_lds(src, (lds_ptr)buf, 16, 0, 0);
   };
-  // One half step: the 16 MFMAs on (fa, fw), the reads of the next fragments
+  // One half step: the SLOTS MFMAs on (fa, fw), the reads of the next fragments
   // into (na, nw) and their conversion, and optionally the loads of step kt.
-  // Reads go out RPS per slot from slot 0; the 16 dword conversions are spread
-  // over slots C0..15.
-  auto half = [&](const v4u (&fa)[4], const v4u (&fw)[4], int rstage, int rs, v4u (&na)[4], v4u (&nw)[4],
+  // Reads go out RPS per slot from slot 0; the 4 JW dword conversions are
+  // spread over slots C0..SLOTS-1.
+  auto half = [&](const v4u (&fa)[4], const v4u (&fw)[JW], int rstage, int rs, v4u (&na)[4], v4u (&nw)[JW],
                   bool load, int kt, int lstage) {
-    constexpr int RPS = KF_GEMM_READS_PER_SLOT, C0 = KF_GEMM_CVT_SLOT;
+    constexpr int RPS = KF_GEMM_READS_PER_SLOT, C0 = KF_GEMM_CVT_SLOT * SLOTS / 16, ND = 4 * JW;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      acc[q >> 2][q & 3] = mfma32(fa[q >> 2], fw[q & 3], acc[q >> 2][q & 3]);
+    for (int q = 0; q < SLOTS; ++q) {
+      acc[q / JW][q % JW] = mfma32(fa[q / JW], fw[q % JW], acc[q / JW][q % JW]);
 #pragma unroll
       for (int r = 0; r < RPS; ++r)
-        if (q * RPS + r < 8) read_frag(rstage, rs, q * RPS + r, na, nw);
-      if (load && q < 8) load_part(kt, lstage, q);
+        if (q * RPS + r < JW + 4) read_frag(rstage, rs, q * RPS + r, na, nw);
+      if (load && q < 2 * LOADS) load_part(kt, lstage, q);
       if (q >= C0) {
 #pragma unroll
-        for (int d = (q - C0) * 16 / (16 - C0); d < (q - C0 + 1) * 16 / (16 - C0); ++d) convert_dword(nw, d);
+        for (int d = (q - C0) * ND / (SLOTS - C0); d < (q - C0 + 1) * ND / (SLOTS - C0); ++d) convert_dword(nw, d);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -231,11 +242,11 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
   for (int s = 0; s < STAGES; ++s) issue(s < nk ? s : nk - 1, s);
   wait_vm<(STAGES - 1) * 2 * LOADS>();  // step 0 has landed
   block_barrier();
-  v4u fa0[4], fw0[4], fa1[4], fw1[4];
+  v4u fa0[4], fw0[JW], fa1[4], fw1[JW];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) read_frag(0, 0, q, fa0, fw0);
+  for (int q = 0; q < JW + 4; ++q) read_frag(0, 0, q, fa0, fw0);
 #pragma unroll
-  for (int d = 0; d < 16; ++d) convert_dword(fw0, d);
+  for (int d = 0; d < 4 * JW; ++d) convert_dword(fw0, d);
   for (int k = 0; k + 1 < nk; ++k) {
     __builtin_amdgcn_sched_barrier(0);
     half(fa0, fw0, k % STAGES, 1, fa1, fw1, false, 0, 0);
@@ -251,7 +262,7 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
     const int k = nk - 1;
     half(fa0, fw0, k % STAGES, 1, fa1, fw1, false, 0, 0);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) acc[q >> 2][q & 3] = mfma32(fa1[q >> 2], fw1[q & 3], acc[q >> 2][q & 3]);
+    for (int q = 0; q < SLOTS; ++q) acc[q / JW][q % JW] = mfma32(fa1[q / JW], fw1[q % JW], acc[q / JW][q % JW]);
   }
   wait_vm<0>();  // no load may still be writing LDS when the workgroup ends
 
@@ -270,8 +281,8 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
           const int row = m0 + wm * 128 + 32 * i + 8 * (v >> 2) + rq + (v & 3);
           if (row >= p.M) continue;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int col = n0 + wn * 128 + 32 * j + rl;
+          for (int j = 0; j < JW; ++j) {
+            const int col = n0 + wn * (32 * JW) + 32 * j + rl;
             if (col < p.N) atomicAdd(p.C + (int64_t)row * p.N + col, acc[i][j][v]);
           }
         }
@@ -297,8 +308,8 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
       if (row >= p.M) continue;
       if (EPI == kGemmSwiGLU) {
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {  // blocks (2jj, 2jj+1) are gate / up of the same outputs
-          const int j = (n0 >> 1) + wn * 64 + 32 * jj + rl;
+        for (int jj = 0; jj < JW / 2; ++jj) {  // blocks (2jj, 2jj+1) are gate / up of the same outputs
+          const int j = (n0 >> 1) + wn * (16 * JW) + 32 * jj + rl;
           if (j < (p.N >> 1)) {
             const float g = acc[i][2 * jj][v], u = acc[i][2 * jj + 1][v];
             p.Cb[(int64_t)row * (p.N >> 1) + j] = to_f16(g / (1.0f + expf(-g)) * u);
@@ -306,8 +317,8 @@ __global__ __launch_bounds__(NT) void gemm256_kernel(const Params p) {
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int col = n0 + wn * 128 + 32 * j + rl;
+        for (int j = 0; j < JW; ++j) {
+          const int col = n0 + wn * (32 * JW) + 32 * j + rl;
           if (col >= p.N) continue;
           float* c = p.C + (int64_t)row * p.N + col;
           if (EPI == kGemmResidF32) *c += acc[i][j][v];
@@ -354,10 +365,10 @@ hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint
   }
   const int grid = ((M + BM - 1) / BM) * ((N + BN - 1) / BN) * p.splitk;
   switch (epi) {
-    case kGemmStoreF32: hipLaunchKernelGGL(gemm256_kernel<kGemmStoreF32>, dim3(grid), dim3(NT), 0, s, p); break;
-    case kGemmResidF32: hipLaunchKernelGGL(gemm256_kernel<kGemmResidF32>, dim3(grid), dim3(NT), 0, s, p); break;
-    case kGemmSwiGLU: hipLaunchKernelGGL(gemm256_kernel<kGemmSwiGLU>, dim3(grid), dim3(NT), 0, s, p); break;
-    case kGemmPartialF32: hipLaunchKernelGGL(gemm256_kernel<kGemmPartialF32>, dim3(grid), dim3(NT), 0, s, p); break;
+    case kGemmStoreF32: hipLaunchKernelGGL(gemm256_kernel<kGemmStoreF32>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
+    case kGemmResidF32: hipLaunchKernelGGL(gemm256_kernel<kGemmResidF32>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
+    case kGemmSwiGLU: hipLaunchKernelGGL(gemm256_kernel<kGemmSwiGLU>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
+    case kGemmPartialF32: hipLaunchKernelGGL(gemm256_kernel<kGemmPartialF32>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
