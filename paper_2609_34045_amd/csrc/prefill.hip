@@ -242,25 +242,28 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   constexpr int PER = (KB * CH + 255) / 256;
   constexpr int VPER = (KB / 2 * CH + 255) / 256;
   v4u rk[PER], rv0[VPER], rv1[VPER];
+  // Keys at or past nkeys come after every query of the workgroup, so the
+  // causal mask gives them weight 0; they are loaded from key nkeys - 1 (a
+  // written, finite row) instead of being branched around.
+  // (Thread chunks past the tile, possible only when 256 does not divide the
+  // chunk count, are skipped; the test folds away otherwise.)
+  constexpr bool kFullK = KB * CH % 256 == 0, kFullV = KB / 2 * CH % 256 == 0;
   auto gload = [&](int blk) {
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
       const int idx = tid + 256 * r;
       const int key = idx / CH, ch = idx % CH;
-      const int pos = blk * KB + key;
-      rk[r] = v4u{0u, 0u, 0u, 0u};
-      if (idx < KB * CH && pos < nkeys) rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)pos * HD + ch * 8);
+      const int pos = min(blk * KB + key, nkeys - 1);
+      if (kFullK || idx < KB * CH) rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)pos * HD + ch * 8);
     }
 #pragma unroll
     for (int r = 0; r < VPER; ++r) {
       const int idx = tid + 256 * r;
       const int kp = idx % (KB / 2), ch = idx / (KB / 2);
       const int pos = blk * KB + 2 * kp;
-      rv0[r] = v4u{0u, 0u, 0u, 0u};
-      rv1[r] = v4u{0u, 0u, 0u, 0u};
-      if (idx < KB / 2 * CH) {
-        if (pos < nkeys) rv0[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)pos * HD + ch * 8);
-        if (pos + 1 < nkeys) rv1[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)(pos + 1) * HD + ch * 8);
+      if (kFullV || idx < KB / 2 * CH) {
+        rv0[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(pos, nkeys - 1) * HD + ch * 8);
+        rv1[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(pos + 1, nkeys - 1) * HD + ch * 8);
       }
     }
   };
@@ -268,7 +271,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
       const int idx = tid + 256 * r;
-      if (idx < KB * CH) {
+      if (kFullK || idx < KB * CH) {
         const int key = idx / CH, ch = idx % CH;
         *reinterpret_cast<v4u*>(&Ks[buf][key * LDK + ch * 8]) = rk[r];
       }
@@ -276,7 +279,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
 #pragma unroll
     for (int r = 0; r < VPER; ++r) {
       const int idx = tid + 256 * r;
-      if (idx < KB / 2 * CH) {
+      if (kFullV || idx < KB / 2 * CH) {
         const int kp = idx % (KB / 2), ch = idx / (KB / 2);
         const uint32_t a[4] = {rv0[r].x, rv0[r].y, rv0[r].z, rv0[r].w};
         const uint32_t b[4] = {rv1[r].x, rv1[r].y, rv1[r].z, rv1[r].w};
