@@ -306,9 +306,10 @@ __device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, in
 #endif
 // The weight bytes in flight per CU scale with resident waves; at batch 3-4 the
 // input rows and partial sums put the kernel just past 128 VGPRs (3 waves per
-// SIMD), so the register budget is held to 4 waves.
+// SIMD), so the register budget is held to 4 waves there.  Smaller batches are
+// left to the compiler (a cap costs the batch-1 gate/up kernel a wave).
 template <int B, int R, int U, int EPI, bool NORM, bool SRC = false>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KF_GEMV_MIN_WAVES)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(B >= 3 ? KF_GEMV_MIN_WAVES : 1)))
 void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
   constexpr int NV = R * B + (NORM ? B : 0);
