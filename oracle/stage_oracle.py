@@ -22,13 +22,18 @@ head, with every reading of the unstated details listed here:
   also the cache slot (append-only).
 * Head: untied embedding and output projection; greedy argmax, lowest index on
   ties.
+* Qwen3-style blocks (the family the paper serves) add an RMSNorm over each q
+  and each k head vector (gains of length head_dim, the layer's eps) after the
+  projections and before RoPE; their query width nq * head_dim may differ from
+  the hidden size.  Pinned against transformers' Qwen3 model in float64.
 * Rows of a batch are independent users with their own cache and position.
 
 Everything is float64.  Weights arrive as bf16 bit patterns and are widened
 exactly.  There is no blocking, fusion or reordering beyond the definition.
 Parity pins: each function is checked in ``tests/test_oracle_pins.py`` against
 closed forms, invariants, library routines (torch CPU, transformers' Llama
-layer) and a separately written scalar brute force.
+layer, and its Qwen3 model for the q/k-norm variant) and a separately
+written scalar brute force.
 """
 from __future__ import annotations
 
@@ -158,6 +163,9 @@ def decoder_layer(x, w, shape, kv: OracleKV, layer: int, users, positions):
     q = (xn @ w["wq"].T).reshape(N, nq, hd)
     k = (xn @ w["wk"].T).reshape(N, nkv, hd)
     v = (xn @ w["wv"].T).reshape(N, nkv, hd)
+    if "q_norm" in w:  # Qwen3-style: each q and k head is RMS-normalised (gain over head_dim) before RoPE
+        q = rms_norm(q, w["q_norm"], shape.rms_eps)
+        k = rms_norm(k, w["k_norm"], shape.rms_eps)
     q = rope(q, pos, shape.rope_theta)
     k = rope(k, pos, shape.rope_theta)
     for n in range(N):

@@ -81,8 +81,9 @@ STREAM_WEIGHTS, STREAM_PREFILL_HIDDEN, STREAM_DECODE_HIDDEN, STREAM_TOKENS, STRE
 # Tensor kinds (generator coordinate); names follow the decoder-layer notation.
 LAYER_KINDS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")
 HEAD_KINDS = ("embed", "final_norm", "lm_head")
-KIND_ID = {n: i for i, n in enumerate(LAYER_KINDS + HEAD_KINDS)}
-GAIN_KINDS = ("attn_norm", "mlp_norm", "final_norm")
+QK_NORM_KINDS = ("q_norm", "k_norm")  # per-head RMSNorm gains of q and k (Qwen3-style blocks)
+KIND_ID = {n: i for i, n in enumerate(LAYER_KINDS + HEAD_KINDS + QK_NORM_KINDS)}
+GAIN_KINDS = ("attn_norm", "mlp_norm", "final_norm", "q_norm", "k_norm")
 
 
 @dataclass(frozen=True)
@@ -96,18 +97,22 @@ class ModelShape:
     vocab: int
     rms_eps: float = 1e-5
     rope_theta: float = 1e4
+    qk_norm: bool = False  # RMSNorm over each q and k head (gains [head_dim]) before RoPE, as in Qwen3
+
+    def layer_kinds(self):
+        return LAYER_KINDS + (QK_NORM_KINDS if self.qk_norm else ())
 
     def tensor_shape(self, kind: str):
         H, hd, F = self.hidden, self.head_dim, self.ffn
         return {
-            "attn_norm": (H,), "mlp_norm": (H,), "final_norm": (H,),
+            "attn_norm": (H,), "mlp_norm": (H,), "final_norm": (H,), "q_norm": (hd,), "k_norm": (hd,),
             "wq": (self.n_q_heads * hd, H), "wk": (self.n_kv_heads * hd, H), "wv": (self.n_kv_heads * hd, H),
             "wo": (H, self.n_q_heads * hd), "wg": (F, H), "wu": (F, H), "wd": (H, F),
             "embed": (self.vocab, H), "lm_head": (self.vocab, H),
         }[kind]
 
     def block_bytes(self) -> int:
-        return sum(2 * int(np.prod(self.tensor_shape(k))) for k in LAYER_KINDS)
+        return sum(2 * int(np.prod(self.tensor_shape(k))) for k in self.layer_kinds())
 
 
 @dataclass(frozen=True)
@@ -132,6 +137,11 @@ SHAPE_TINY = ModelShape(2, 512, 8, 2, 64, 1408, 1000, 1e-5, 1e4)
 SHAPE_8B = ModelShape(32, 4096, 32, 8, 128, 14336, 128256, 1e-5, 5e5)
 SHAPE_32B = ModelShape(64, 5120, 40, 8, 128, 27648, 152064, 1e-5, 1e6)
 SHAPE_70B = ModelShape(80, 8192, 64, 8, 128, 28672, 128256, 1e-5, 5e5)
+# Qwen3-style blocks (per-head q/k RMSNorm; query width nq*hd may differ from H), the
+# family the paper serves.  The tiny shape keeps nq*hd (512) != H (384) on purpose.
+SHAPE_QWEN3_TINY = ModelShape(2, 384, 8, 2, 64, 1024, 1000, 1e-6, 1e6, qk_norm=True)
+SHAPE_QWEN3_8B = ModelShape(36, 4096, 32, 8, 128, 12288, 151936, 1e-6, 1e6, qk_norm=True)
+SHAPE_QWEN3_32B = ModelShape(64, 5120, 64, 8, 128, 25600, 151936, 1e-6, 1e6, qk_norm=True)
 
 WORKLOADS = {
     "tiny": Workload(1, "tiny", SHAPE_TINY, 0, 2, False, 1, (128,), 16, prefill_chunk=128,
@@ -156,7 +166,7 @@ def layer_weights(shape: ModelShape, cfg_id: int, layer: int, seed: int = 0) -> 
     global layer index, so a layer has the same weights in every stage that holds it.
     """
     out = {}
-    for kind in LAYER_KINDS:
+    for kind in shape.layer_kinds():
         k = key(seed, cfg_id, STREAM_WEIGHTS, layer, KIND_ID[kind])
         mean = 1.0 if kind in GAIN_KINDS else 0.0
         out[kind] = normal_bf16(k, shape.tensor_shape(kind), mean, 0.02)

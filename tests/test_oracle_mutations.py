@@ -100,3 +100,33 @@ def test_mutation_is_caught(name, monkeypatch):
     attr, fn = MUTATIONS[name]
     monkeypatch.setattr(so, attr, fn)
     assert _max_rel_gap() > 1e-6, name
+
+
+def _decoder_layer_qk_norm_after_rope(x, w, shape, kv, layer, users, positions):
+    """Planted mistake: the per-head q/k norms applied after RoPE instead of before."""
+    x = np.asarray(x, dtype=np.float64)
+    N, H = x.shape
+    nq, nkv, hd = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    pos = np.asarray(positions, dtype=np.int64)
+    xn = so.rms_norm(x, w["attn_norm"], shape.rms_eps)
+    q = so.rope((xn @ w["wq"].T).reshape(N, nq, hd), pos, shape.rope_theta)
+    k = so.rope((xn @ w["wk"].T).reshape(N, nkv, hd), pos, shape.rope_theta)
+    v = (xn @ w["wv"].T).reshape(N, nkv, hd)
+    q = so.rms_norm(q, w["q_norm"], shape.rms_eps)
+    k = so.rms_norm(k, w["k_norm"], shape.rms_eps)
+    for n in range(N):
+        kv.k[layer][users[n], pos[n]] = k[n]
+        kv.v[layer][users[n], pos[n]] = v[n]
+    keys = [kv.k[layer][users[n], : pos[n] + 1] for n in range(N)]
+    vals = [kv.v[layer][users[n], : pos[n] + 1] for n in range(N)]
+    x = x + so.attention_rows(q, keys, vals, nkv) @ w["wo"].T
+    z = so.rms_norm(x, w["mlp_norm"], shape.rms_eps)
+    return x + so.mlp_swiglu(z, w["wg"], w["wu"], w["wd"])
+
+
+def test_qwen3_pin_catches_qk_norm_after_rope(monkeypatch):
+    from tests import test_oracle_pins as pins
+    pytest.importorskip("transformers")
+    monkeypatch.setattr(so, "decoder_layer", _decoder_layer_qk_norm_after_rope)
+    with pytest.raises(AssertionError):
+        pins.test_qk_norm_stage_matches_transformers_qwen3_in_float64()

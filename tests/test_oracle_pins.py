@@ -248,6 +248,53 @@ def test_stage_matches_transformers_llama_in_float64():
         nxt = int(orc.argmax(y)[0])
 
 
+# ---------------------------------------------------------------- Qwen3-style block vs transformers' Qwen3
+def test_qk_norm_stage_matches_transformers_qwen3_in_float64():
+    """Per-head q/k RMSNorm before RoPE, query width nq*hd != hidden, against Qwen3ForCausalLM."""
+    transformers = pytest.importorskip("transformers")
+    if not hasattr(transformers, "Qwen3ForCausalLM"):
+        pytest.skip("transformers without Qwen3")
+    shape = synth.ModelShape(n_layers=3, hidden=24, n_q_heads=4, n_kv_heads=2, head_dim=8, ffn=40, vocab=64,
+                             rms_eps=1e-6, rope_theta=1000.0, qk_norm=True)
+    assert shape.n_q_heads * shape.head_dim != shape.hidden
+    Wbits = _tiny_weights(shape, 0, 3, cfg=97)
+    assert set(Wbits[0]) == set(synth.LAYER_KINDS) | {"q_norm", "k_norm"}
+    hb = synth.head_weights(shape, 97)
+    cfg = transformers.Qwen3Config(hidden_size=24, intermediate_size=40, num_attention_heads=4,
+                                   num_key_value_heads=2, head_dim=8, num_hidden_layers=3, vocab_size=64,
+                                   rms_norm_eps=1e-6, tie_word_embeddings=False,
+                                   rope_parameters={"rope_type": "default", "rope_theta": 1000.0},
+                                   max_position_embeddings=64, attention_bias=False, use_sliding_window=False)
+    torch.manual_seed(0)
+    m = transformers.Qwen3ForCausalLM(cfg).to(torch.float64).eval()
+    names = {"attn_norm": "input_layernorm", "mlp_norm": "post_attention_layernorm", "wq": "self_attn.q_proj",
+             "wk": "self_attn.k_proj", "wv": "self_attn.v_proj", "wo": "self_attn.o_proj", "wg": "mlp.gate_proj",
+             "wu": "mlp.up_proj", "wd": "mlp.down_proj", "q_norm": "self_attn.q_norm", "k_norm": "self_attn.k_norm"}
+    sd = {}
+    for l, w in Wbits.items():
+        for k, v in w.items():
+            sd[f"model.layers.{l}.{names[k]}.weight"] = torch.from_numpy(bf16_to_f64(v))
+    sd["model.embed_tokens.weight"] = torch.from_numpy(bf16_to_f64(hb["embed"]))
+    sd["model.norm.weight"] = torch.from_numpy(bf16_to_f64(hb["final_norm"]))
+    sd["lm_head.weight"] = torch.from_numpy(bf16_to_f64(hb["lm_head"]))
+    m.load_state_dict(sd, strict=True)
+    toks = [3, 40, 63, 1, 22, 7]
+    orc = OracleStage(shape, 0, 3, lambda l: Wbits[l], hb, max_users=1, max_ctx=16)
+    with torch.no_grad():
+        out = m(torch.tensor([toks]), use_cache=True)
+    x = orc.prefill(0, 0, tokens=np.array(toks))
+    np.testing.assert_allclose(orc.logits(x), out.logits[0].numpy(), rtol=2e-5, atol=2e-6)
+    past = out.past_key_values
+    nxt = int(np.argmax(out.logits[0, -1].numpy()))
+    for step in range(3):
+        with torch.no_grad():
+            o2 = m(torch.tensor([[nxt]]), past_key_values=past, use_cache=True)
+        past = o2.past_key_values
+        y = orc.decode([0], [len(toks) + step], tokens=np.array([nxt]))
+        np.testing.assert_allclose(orc.logits(y), o2.logits[0].numpy(), rtol=2e-5, atol=2e-6)
+        nxt = int(orc.argmax(y)[0])
+
+
 # ---------------------------------------------------------------- structural invariants
 def test_prefill_equals_sequential_decode_and_chunking():
     shape = TINY
