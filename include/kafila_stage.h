@@ -29,7 +29,8 @@
  *    failure on the calling thread.
  *  - Requirements checked at init: head_dim in {64, 128}; n_q_heads a multiple
  *    of n_kv_heads with at most 8 query heads per KV head; hidden and ffn
- *    multiples of 64.  Anything else is KF_EUNSUPPORTED.
+ *    multiples of 64.  Anything else is KF_EUNSUPPORTED.  The query width
+ *    n_q_heads * head_dim need not equal hidden.
  */
 #ifndef KAFILA_STAGE_H
 #define KAFILA_STAGE_H
@@ -40,7 +41,7 @@
 extern "C" {
 #endif
 
-#define KF_ABI_VERSION 1
+#define KF_ABI_VERSION 2  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds */
 #define KF_MAX_BATCH 4
 
 typedef struct kf_stage kf_stage;
@@ -68,6 +69,8 @@ typedef struct {
   int32_t vocab;      /* V (used only with the head) */
   float rms_eps;      /* RMSNorm epsilon, added to mean(x^2) inside the square root */
   float rope_theta;   /* RoPE base: pair (i, i + hd/2) turns by pos * theta^(-2i/hd) */
+  int32_t qk_norm;    /* 1: each q and k head vector is RMS-normalised (gains KF_W_Q_NORM / KF_W_K_NORM,
+                         eps rms_eps) before RoPE, as in the Qwen3 models the paper serves; 0: no such norm */
 } kf_model_config;
 
 typedef enum {
@@ -82,7 +85,9 @@ typedef enum {
   KF_W_DOWN = 8,      /* [H, F] */
   KF_W_EMBED = 9,     /* [V, H]         head only */
   KF_W_FINAL_NORM = 10, /* [H]          head only */
-  KF_W_LM_HEAD = 11   /* [V, H]         head only (not tied to the embedding) */
+  KF_W_LM_HEAD = 11,  /* [V, H]         head only (not tied to the embedding) */
+  KF_W_Q_NORM = 12,   /* [hd]           gain of the per-head q norm (only when qk_norm) */
+  KF_W_K_NORM = 13    /* [hd]           gain of the per-head k norm (only when qk_norm) */
 } kf_tensor_kind;
 
 typedef struct {
@@ -120,8 +125,9 @@ kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t layer_lo, int32_t l
  * Create a stage holding layers [layer_lo, layer_hi) of the model and, if has_head,
  * the head.  Weight tensors are copied to the current HIP device (the stage's
  * device) before the call returns, so the caller may free them afterwards.  Every
- * layer tensor of every held layer must be present exactly once, plus the three
- * head tensors when has_head; anything else is KF_EINVAL.  hip_stream (a
+ * layer tensor of every held layer must be present exactly once (kinds 0..8, plus
+ * KF_W_Q_NORM and KF_W_K_NORM when qk_norm), plus the three head tensors when
+ * has_head; anything else is KF_EINVAL.  hip_stream (a
  * hipStream_t, NULL for the default stream) is where all later work is enqueued.
  */
 kf_status kf_stage_init(const kf_model_config* cfg, int32_t layer_lo, int32_t layer_hi, int32_t has_head,
@@ -233,9 +239,10 @@ typedef enum {
   KF_K_PF_GATEUP = 13, /* prefill: gate/up GEMM + SwiGLU */
   KF_K_PF_DOWN = 14,   /* prefill: down GEMM + residual */
   KF_K_PF_STORE = 15,  /* prefill: hidden output store */
-  KF_K_COUNT = 16
+  KF_K_QKNORM = 16,    /* decode: per-head q/k RMSNorm + RoPE + K append (qk_norm blocks) */
+  KF_K_COUNT = 17
 } kf_kernel_class;
-#define KF_K_ALL 0xffff
+#define KF_K_ALL 0x1ffff
 
 kf_status kf_stage_profile(kf_stage* stage, int32_t mask);
 kf_status kf_stage_profile_read(kf_stage* stage, int32_t kernel_class, int64_t* launches, double* total_ms);

@@ -208,7 +208,12 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       const float y1 = fin[r * B + b] * rs[b];
       const float y2 = fin[(r + R / 2) * B + b] * rs[b];
       const int hd = p.hd, half = hd / 2, i = i0 + r, pos = p.pos[b];
-      if (head < p.nq + p.nkv) {
+      if (p.kraw && head < p.nq + p.nkv) {  // raw q / k: their norm and RoPE follow in another kernel
+        float* dst = head < p.nq ? p.q + (int64_t)b * p.nq * hd + head * hd
+                                 : p.kraw + ((int64_t)b * p.nkv + head - p.nq) * hd;
+        dst[i] = y1;
+        dst[i + half] = y2;
+      } else if (head < p.nq + p.nkv) {
         const float c = pre.a, s = pre.b;
         const float z1 = y1 * c - y2 * s, z2 = y2 * c + y1 * s;
         if (head < p.nq) {
@@ -836,6 +841,35 @@ __global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, float* dk
   dv[i] = (float)__builtin_bit_cast(_Float16, sv[at]);
 }
 
+// ------------------------------------------------------------------ q / k head norms
+// One wave per (head, batch row): lane l holds elements l and l + HD/2 of the
+// head vector, which are also the pair RoPE rotates together.
+template <int HD>
+__global__ __launch_bounds__(64) void qk_norm_rope_kernel(const QkNormParams p) {
+  constexpr int HALF = HD / 2;
+  const int h = blockIdx.x, b = blockIdx.y, l = threadIdx.x;
+  const bool isq = h < p.nq;
+  const float* src = isq ? p.q + ((int64_t)b * p.nq + h) * HD : p.kraw + ((int64_t)b * p.nkv + h - p.nq) * HD;
+  const bool act = l < HALF;
+  const float a = act ? src[l] : 0.f, c = act ? src[l + HALF] : 0.f;
+  const float rs = 1.0f / sqrtf(wave_sum(a * a + c * c) / (float)HD + p.eps);
+  if (!act) return;
+  const uint16_t* g = isq ? p.gq : p.gk;
+  const float x1 = a * rs * bf16_to_f32(g[l]), x2 = c * rs * bf16_to_f32(g[l + HALF]);
+  const int pos = p.pos[b];
+  const float cs = p.rope_cos[(int64_t)pos * HALF + l], sn = p.rope_sin[(int64_t)pos * HALF + l];
+  const float z1 = x1 * cs - x2 * sn, z2 = x2 * cs + x1 * sn;
+  if (isq) {
+    float* dst = p.q + ((int64_t)b * p.nq + h) * HD;
+    dst[l] = z1;
+    dst[l + HALF] = z2;
+  } else {
+    uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(h - p.nq) * p.max_ctx + pos) * HD;
+    k[l] = f32_to_f16(z1);
+    k[l + HALF] = f32_to_f16(z2);
+  }
+}
+
 // ------------------------------------------------------------------ launchers
 template <int B, int R, int U>
 static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
@@ -891,6 +925,15 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   const int grid = gemv_grid(epi, R, p);
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_qk_norm_rope(const QkNormParams& p, int batch, hipStream_t s) {
+  if (batch < 1 || batch > kMaxBatch) return hipErrorInvalidValue;
+  const dim3 grid(p.nq + p.nkv, batch);
+  if (p.hd == 128) hipLaunchKernelGGL(qk_norm_rope_kernel<128>, grid, dim3(64), 0, s, p);
+  else if (p.hd == 64) hipLaunchKernelGGL(qk_norm_rope_kernel<64>, grid, dim3(64), 0, s, p);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 template <int HD, int G>

@@ -59,6 +59,10 @@ struct GemvParams {
   const float* rope_sin;
   int users[kMaxBatch];
   int pos[kMaxBatch];
+  // Blocks with per-head q/k norms: when set, q goes to `q` and k to kraw
+  // ([B][nkv][hd] fp32) as projected (after the attention RMSNorm), without
+  // RoPE; launch_qk_norm_rope finishes both.  v goes to the cache as usual.
+  float* kraw;
 
   // kEpiSwiGLU
   float* act;          // [B][N] with N = F
@@ -96,6 +100,23 @@ struct AttnParams {
   int len[kMaxBatch];  // keys visible to row b: position + 1
 };
 
+// Per-head RMSNorm + RoPE of the raw q and k rows (Qwen3-style blocks); k is
+// appended to the cache at each row's position, q is rotated in place.
+struct QkNormParams {
+  float* q;             // [B][nq][hd]
+  const float* kraw;    // [B][nkv][hd]
+  uint16_t* kc;         // layer base of the K cache (fp16 bits)
+  const uint16_t* gq;   // [hd] bf16 gains
+  const uint16_t* gk;
+  const float* rope_cos;
+  const float* rope_sin;
+  int64_t user_stride;
+  int max_ctx, nq, nkv, hd;
+  float eps;
+  int users[kMaxBatch];
+  int pos[kMaxBatch];
+};
+
 // Launchers (return hipGetLastError() of the launch).
 int gemv_grid(int epi, int rows_per_wg, const GemvParams& p);
 hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p, hipStream_t s);
@@ -103,6 +124,7 @@ hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
+hipError_t launch_qk_norm_rope(const QkNormParams& p, int batch, hipStream_t s);
 // x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] bf16).
 hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,

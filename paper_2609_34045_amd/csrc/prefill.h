@@ -21,6 +21,7 @@ struct PrefillArgs {
 
 struct PrefillLayer {
   const uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
+  const uint16_t *g_qn, *g_kn;  // per-head q / k norm gains (qk_norm blocks), else NULL
   uint16_t* kc;  // K cache of this layer and user (fp16 bits): [kv_head][pos][hd]
   uint16_t* vc;
   void* out;     // hidden output after this layer (last layer only), else NULL

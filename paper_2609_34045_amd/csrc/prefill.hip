@@ -109,10 +109,14 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const f
 // QKV [T][(nq+2nkv) hd] fp32, the sum of nsplit split-K slices of `qkv` (slice
 // stride `stride`) -> q [T][nq][hd] fp16 (rotated), K/V cache at pos0 + i (fp16).
 // A thread takes 4 consecutive rotation pairs (j .. j+3, j+hd/2 .. j+hd/2+3).
+// With gq / gk set (blocks with per-head q / k norms), each q and k head is
+// RMS-normalised over its hd values first: the hd/8 consecutive threads that
+// hold a head add their squares with lane shuffles.
 __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nsplit, int64_t stride, uint16_t* q,
                                                       uint16_t* kc, uint16_t* vc, const float* cosT,
                                                       const float* sinT, int nq, int nkv, int hd, int pos0,
-                                                      int max_ctx) {
+                                                      int max_ctx, const uint16_t* gq, const uint16_t* gk,
+                                                      float eps) {
   const int i = blockIdx.x, half = hd / 2, q4 = half / 4, pos = pos0 + i;
   const int nh = nq + 2 * nkv;
   const float* src = qkv + (int64_t)i * nh * hd;
@@ -136,6 +140,17 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
     }
     uint16_t* dst;
     v4f z1, z2;
+    if (gq && h < nq + nkv) {  // the q4 threads of a head are consecutive lanes of one wave
+      float ss = a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
+      for (int o = 1; o < q4; o <<= 1) ss += __shfl_xor(ss, o);
+      const float rs = 1.0f / sqrtf(ss / (float)hd + eps);
+      const uint16_t* g = h < nq ? gq : gk;
+      const v4f ga = {from_bf16(g[j]), from_bf16(g[j + 1]), from_bf16(g[j + 2]), from_bf16(g[j + 3])};
+      const v4f gb = {from_bf16(g[j + half]), from_bf16(g[j + half + 1]), from_bf16(g[j + half + 2]),
+                      from_bf16(g[j + half + 3])};
+      a = a * rs * ga;
+      b = b * rs * gb;
+    }
     if (h < nq + nkv) {
       const v4f c = *reinterpret_cast<const v4f*>(cosT + (int64_t)pos * half + j);
       const v4f s = *reinterpret_cast<const v4f*>(sinT + (int64_t)pos * half + j);
@@ -560,7 +575,7 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   if (e != hipSuccess) return e;
   tr.begin(ROPE);
   hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.part, s_qkv, (int64_t)T * nqkv, ws.q, l.kc, l.vc,
-                     a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, a.max_ctx);
+                     a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, a.max_ctx, l.g_qn, l.g_kn, a.eps);
   tr.end(ROPE);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));

@@ -59,6 +59,7 @@ static int64_t align256(int64_t n) { return (n + 255) & ~(int64_t)255; }
 
 struct LayerW {
   uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
+  uint16_t *g_qn = nullptr, *g_kn = nullptr;  // per-head q / k norm gains (qk_norm blocks)
 };
 
 struct kf_stage {
@@ -72,6 +73,7 @@ struct kf_stage {
   // decode workspace
   char* ws = nullptr;
   float *x = nullptr, *q = nullptr, *act = nullptr;
+  float* kraw = nullptr;  // [B][nkv][hd] new keys before their norm and RoPE (qk_norm blocks)
   float* part_val = nullptr;
   int* part_idx = nullptr;
   int lm_wg = 0;       // capacity of the argmax partials per batch row
@@ -138,6 +140,7 @@ static kf_status check_cfg(const kf_model_config* c, int lo, int hi) {
   if (c->n_q_heads / c->n_kv_heads > kMaxGroup)
     return fail(KF_EUNSUPPORTED, "more than %d query heads per KV head", kMaxGroup);
   if (c->hidden % 64 || c->ffn % 64) return fail(KF_EUNSUPPORTED, "hidden and ffn must be multiples of 64");
+  if (c->qk_norm != 0 && c->qk_norm != 1) return fail(KF_EINVAL, "qk_norm must be 0 or 1");
   return KF_OK;
 }
 
@@ -150,13 +153,20 @@ static int64_t tensor_numel(const kf_model_config& c, int kind) {
     case KF_W_O: return H * c.n_q_heads * hd;
     case KF_W_GATE: case KF_W_UP: case KF_W_DOWN: return F * H;
     case KF_W_EMBED: case KF_W_LM_HEAD: return V * H;
+    case KF_W_Q_NORM: case KF_W_K_NORM: return c.qk_norm ? hd : -1;
     default: return -1;
   }
 }
 
+// Layer tensors: kinds 0..8, then the q / k norm gains of qk_norm blocks.
+constexpr int kLayerSlots = 11;
+static int layer_slot(int kind) { return kind <= KF_W_DOWN ? kind : kind - KF_W_Q_NORM + KF_W_DOWN + 1; }
+static bool is_layer_kind(int kind) { return (kind >= KF_W_ATTN_NORM && kind <= KF_W_DOWN) || kind == KF_W_Q_NORM || kind == KF_W_K_NORM; }
+
 static int64_t block_bytes(const kf_model_config& c) {
   int64_t n = 0;
   for (int k = KF_W_ATTN_NORM; k <= KF_W_DOWN; ++k) n += tensor_numel(c, k);
+  if (c.qk_norm) n += tensor_numel(c, KF_W_Q_NORM) + tensor_numel(c, KF_W_K_NORM);
   return 2 * n;
 }
 
@@ -183,6 +193,7 @@ static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
   n += align256(B * H * 4);                           // x
   n += align256(B * c.n_q_heads * c.head_dim * 4);    // q
   n += align256(B * (int64_t)c.ffn * 4);              // act
+  if (c.qk_norm) n += align256(B * (int64_t)c.n_kv_heads * c.head_dim * 4);  // kraw
   if (has_head) {
     const int64_t wgs = (c.vocab + 3) / 4;  // enough for any rows-per-workgroup choice
     n += 2 * align256(B * wgs * 4);
@@ -242,30 +253,34 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
 
   const int nl = hi - lo;
   // Locate every tensor exactly once.
-  std::vector<const kf_tensor*> slot((size_t)nl * 9, nullptr);
+  std::vector<const kf_tensor*> slot((size_t)nl * kLayerSlots, nullptr);
   const kf_tensor* hslot[3] = {nullptr, nullptr, nullptr};
   for (int i = 0; i < weights->count; ++i) {
     const kf_tensor& t = weights->tensors[i];
-    if (t.kind < KF_W_ATTN_NORM || t.kind > KF_W_LM_HEAD) return fail(KF_EINVAL, "tensor %d: unknown kind %d", i, t.kind);
+    if (t.kind < KF_W_ATTN_NORM || t.kind > KF_W_K_NORM) return fail(KF_EINVAL, "tensor %d: unknown kind %d", i, t.kind);
     if (!t.bf16) return fail(KF_EINVAL, "tensor %d: NULL data", i);
+    if ((t.kind == KF_W_Q_NORM || t.kind == KF_W_K_NORM) && !cfg->qk_norm)
+      return fail(KF_EINVAL, "tensor %d: q/k norm gain given for a config without qk_norm", i);
     if (t.numel != tensor_numel(*cfg, t.kind))
       return fail(KF_EINVAL, "tensor %d (layer %d kind %d): numel %lld, expected %lld", i, t.layer, t.kind,
                   (long long)t.numel, (long long)tensor_numel(*cfg, t.kind));
     const kf_tensor** dst;
-    if (t.kind >= KF_W_EMBED) {
+    if (!is_layer_kind(t.kind)) {
       if (!has_head) return fail(KF_EINVAL, "tensor %d: head tensor given to a stage without the head", i);
       if (t.layer != -1) return fail(KF_EINVAL, "tensor %d: head tensors take layer -1", i);
       dst = &hslot[t.kind - KF_W_EMBED];
     } else {
       if (t.layer < lo || t.layer >= hi) return fail(KF_EINVAL, "tensor %d: layer %d outside [%d, %d)", i, t.layer, lo, hi);
-      dst = &slot[(size_t)(t.layer - lo) * 9 + t.kind];
+      dst = &slot[(size_t)(t.layer - lo) * kLayerSlots + layer_slot(t.kind)];
     }
     if (*dst) return fail(KF_EINVAL, "tensor %d (layer %d kind %d) given twice", i, t.layer, t.kind);
     *dst = &t;
   }
+  const int need = cfg->qk_norm ? kLayerSlots : KF_W_DOWN + 1;
   for (int l = 0; l < nl; ++l)
-    for (int k = 0; k < 9; ++k)
-      if (!slot[(size_t)l * 9 + k]) return fail(KF_EINVAL, "missing tensor: layer %d kind %d", lo + l, k);
+    for (int k = 0; k < need; ++k)
+      if (!slot[(size_t)l * kLayerSlots + k])
+        return fail(KF_EINVAL, "missing tensor: layer %d kind %d", lo + l, k <= KF_W_DOWN ? k : k - KF_W_DOWN - 1 + KF_W_Q_NORM);
   if (has_head)
     for (int k = 0; k < 3; ++k)
       if (!hslot[k]) return fail(KF_EINVAL, "missing head tensor kind %d", KF_W_EMBED + k);
@@ -288,7 +303,9 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   // Per-layer arena: wqkv | wo | wg | wu | wd | g_attn | g_mlp, each 256-byte aligned.
   const int64_t off_qkv = 0, off_o = align256(off_qkv + nqkv * H * 2), off_g = align256(off_o + H * c.n_q_heads * hd * 2),
                 off_u = align256(off_g + F * H * 2), off_d = align256(off_u + F * H * 2),
-                off_na = align256(off_d + H * F * 2), off_nm = align256(off_na + H * 2), lsz = align256(off_nm + H * 2);
+                off_na = align256(off_d + H * F * 2), off_nm = align256(off_na + H * 2),
+                off_qn = align256(off_nm + H * 2), off_kn = align256(off_qn + (c.qk_norm ? hd * 2 : 0)),
+                lsz = align256(off_kn + (c.qk_norm ? hd * 2 : 0));
   const int64_t V = c.vocab;
   const int64_t off_e = lsz * nl, off_lm = align256(off_e + (has_head ? V * H * 2 : 0)),
                 off_gf = align256(off_lm + (has_head ? V * H * 2 : 0)), total = align256(off_gf + H * 2);
@@ -310,7 +327,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->layers.resize(nl);
   for (int l = 0; l < nl; ++l) {
     char* base = s->arena + lsz * l;
-    const kf_tensor** w = &slot[(size_t)l * 9];
+    const kf_tensor** w = &slot[(size_t)l * kLayerSlots];
     LayerW& L = s->layers[l];
     L.wqkv = (uint16_t*)(base + off_qkv);
     L.wo = (uint16_t*)(base + off_o);
@@ -330,6 +347,12 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
     if (e == hipSuccess) e = up(base + off_d, w[KF_W_DOWN]);
     if (e == hipSuccess) e = up(base + off_na, w[KF_W_ATTN_NORM]);
     if (e == hipSuccess) e = up(base + off_nm, w[KF_W_MLP_NORM]);
+    if (c.qk_norm) {
+      L.g_qn = (uint16_t*)(base + off_qn);
+      L.g_kn = (uint16_t*)(base + off_kn);
+      if (e == hipSuccess) e = up(base + off_qn, w[layer_slot(KF_W_Q_NORM)]);
+      if (e == hipSuccess) e = up(base + off_kn, w[layer_slot(KF_W_K_NORM)]);
+    }
     if (e != hipSuccess) return cleanup(fail(KF_EDEVICE, "weight upload: %s", hipGetErrorString(e)));
   }
   if (has_head) {
@@ -359,6 +382,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->x = (float*)take(B * H * 4);
   s->q = (float*)take(B * c.n_q_heads * hd * 4);
   s->act = (float*)take(B * F * 4);
+  if (c.qk_norm) s->kraw = (float*)take(B * c.n_kv_heads * hd * 4);
   if (has_head) {
     s->lm_wg = (int)((V + KF_R_LMHEAD - 1) / KF_R_LMHEAD);
     s->part_val = (float*)take(B * s->lm_wg * 4);
@@ -600,6 +624,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     g.hd = hd;
     g.rope_cos = kv->rcos;
     g.rope_sin = kv->rsin;
+    g.kraw = s->kraw;  // set for qk_norm blocks: q and k are normalised and rotated below
     for (int b = 0; b < kMaxBatch; ++b) {
       g.users[b] = b < batch ? users[b] : 0;
       g.pos[b] = b < batch ? positions[b] : 0;
@@ -620,6 +645,30 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
     tr.end(KF_K_QKV);
     KF_HIP(le, "qkv launch");
+    if (c.qk_norm) {
+      QkNormParams qn{};
+      qn.q = s->q;
+      qn.kraw = s->kraw;
+      qn.kc = kv->k + loff;
+      qn.gq = L.g_qn;
+      qn.gk = L.g_kn;
+      qn.rope_cos = kv->rcos;
+      qn.rope_sin = kv->rsin;
+      qn.user_stride = kv->user_stride;
+      qn.max_ctx = kv->max_ctx;
+      qn.nq = c.n_q_heads;
+      qn.nkv = c.n_kv_heads;
+      qn.hd = hd;
+      qn.eps = c.rms_eps;
+      for (int b = 0; b < kMaxBatch; ++b) {
+        qn.users[b] = g.users[b];
+        qn.pos[b] = g.pos[b];
+      }
+      tr.begin(KF_K_QKNORM);
+      const hipError_t qe = launch_qk_norm_rope(qn, batch, st);
+      tr.end(KF_K_QKNORM);
+      KF_HIP(qe, "q/k norm launch");
+    }
 
     AttnParams a{};
     a.q = s->q;
@@ -808,6 +857,8 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
     pl.wd = L.wd;
     pl.g_attn = L.g_attn;
     pl.g_mlp = L.g_mlp;
+    pl.g_qn = L.g_qn;
+    pl.g_kn = L.g_kn;
     pl.kc = kv->k + loff;
     pl.vc = kv->v + loff;
     pl.out = l == s->hi - 1 ? hidden_out_dev : nullptr;

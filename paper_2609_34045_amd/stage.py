@@ -24,6 +24,7 @@ KF_F32, KF_BF16, KF_F16 = 0, 1, 2
 MAX_BATCH = 4
 
 LAYER_KINDS = {"attn_norm": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4, "mlp_norm": 5, "wg": 6, "wu": 7, "wd": 8}
+QK_NORM_KINDS = {"q_norm": 12, "k_norm": 13}  # per-head q / k RMSNorm gains of qk_norm blocks
 HEAD_KINDS = {"embed": 9, "final_norm": 10, "lm_head": 11}
 
 EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init", "kf_stage_destroy",
@@ -33,7 +34,7 @@ EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init",
 
 # kf_kernel_class
 KERNEL_CLASSES = ("prep", "qkv", "attn", "oproj", "gateup", "down", "lmhead", "argmax", "pf_norm", "pf_qkv", "pf_rope",
-                  "pf_attn", "pf_oproj", "pf_gateup", "pf_down", "pf_store")
+                  "pf_attn", "pf_oproj", "pf_gateup", "pf_down", "pf_store", "qknorm")
 
 
 class KFError(RuntimeError):
@@ -46,12 +47,13 @@ class KFError(RuntimeError):
 class ModelConfig(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
-                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("qk_norm", ctypes.c_int32)]
 
     @classmethod
     def of(cls, shape) -> "ModelConfig":
         return cls(shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
-                   shape.vocab, shape.rms_eps, shape.rope_theta)
+                   shape.vocab, shape.rms_eps, shape.rope_theta, int(getattr(shape, "qk_norm", False)))
 
 
 class Tensor(ctypes.Structure):
@@ -147,7 +149,8 @@ class Stage:
 
     ``layer_weights`` maps each held layer index to a dict of bf16 bit arrays
     (numpy uint16, row-major [out, in]) named attn_norm, wq, wk, wv, wo, mlp_norm,
-    wg, wu, wd; ``head_weights`` holds embed, final_norm and lm_head.
+    wg, wu, wd (plus q_norm and k_norm when the shape has qk_norm);
+    ``head_weights`` holds embed, final_norm and lm_head.
     """
 
     def __init__(self, shape, lo: int, hi: int, layer_weights, head_weights=None, stream=None):
@@ -159,7 +162,8 @@ class Stage:
         keep, items = [], []
         for l in range(lo, hi):
             w = layer_weights[l] if not callable(layer_weights) else layer_weights(l)
-            for name, kind in LAYER_KINDS.items():
+            kinds = dict(LAYER_KINDS, **(QK_NORM_KINDS if self._cfg.qk_norm else {}))
+            for name, kind in kinds.items():
                 a = np.ascontiguousarray(w[name], dtype=np.uint16)
                 keep.append(a)
                 items.append(Tensor(l, kind, a.ctypes.data, a.size))

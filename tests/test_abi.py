@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.kf_abi_version() == 1
+    assert lib.kf_abi_version() == 2
 
 
 def test_stage_bytes_matches_shape_arithmetic():
@@ -107,6 +107,62 @@ def test_init_reports_missing_and_misshapen_tensors(lib):
     t = (stage.Tensor * 1)(stage.Tensor(-1, 9, a.ctypes.data, 100 * 512))
     st = lib.kf_stage_init(ctypes.byref(cfg), 0, 1, 0, ctypes.byref(stage.Weights(t, 1)), None, ctypes.byref(out))
     assert st == 1 and b"head" in lib.kf_last_error()
+
+
+def _layer_tensors(stage, shape, layer, keep):
+    import numpy as np
+    items = []
+    kinds = dict(stage.LAYER_KINDS, **(stage.QK_NORM_KINDS if shape.qk_norm else {}))
+    for name, kind in kinds.items():
+        a = np.zeros(int(np.prod(shape.tensor_shape(name))), dtype=np.uint16)
+        keep.append(a)
+        items.append(stage.Tensor(layer, kind, a.ctypes.data, a.size))
+    return items
+
+
+def test_qk_norm_tensors_are_checked_before_touching_the_device(lib):
+    """q/k norm gains are required exactly when the config sets qk_norm (host-side checks only)."""
+    from paper_2609_34045_amd import stage
+    import numpy as np
+    shape = synth.SHAPE_QWEN3_TINY
+    keep = []
+    full = _layer_tensors(stage, shape, 0, keep)
+    out = ctypes.c_void_p()
+    cfg = stage.ModelConfig.of(shape)
+    # a Qwen3-style config without its two gains: missing tensor (kind 12)
+    no_gains = [t for t in full if t.kind < 12]
+    st = lib.kf_stage_init(ctypes.byref(cfg), 0, 1, 0, ctypes.byref(stage.Weights((stage.Tensor * 9)(*no_gains), 9)),
+                           None, ctypes.byref(out))
+    assert st == 1 and b"missing tensor: layer 0 kind 12" in lib.kf_last_error()
+    # gains given to a config without qk_norm
+    plain = stage.ModelConfig.of(shape)
+    plain.qk_norm = 0
+    st = lib.kf_stage_init(ctypes.byref(plain), 0, 1, 0, ctypes.byref(stage.Weights((stage.Tensor * 11)(*full), 11)),
+                           None, ctypes.byref(out))
+    assert st == 1 and b"without qk_norm" in lib.kf_last_error()
+    # a gain of the wrong length
+    bad = list(full)
+    a = np.zeros(shape.head_dim + 1, dtype=np.uint16)
+    bad[-1] = stage.Tensor(0, 13, a.ctypes.data, a.size)
+    st = lib.kf_stage_init(ctypes.byref(cfg), 0, 1, 0, ctypes.byref(stage.Weights((stage.Tensor * 11)(*bad), 11)),
+                           None, ctypes.byref(out))
+    assert st == 1 and b"numel" in lib.kf_last_error()
+    # qk_norm must be 0 or 1
+    odd = stage.ModelConfig.of(shape)
+    odd.qk_norm = 2
+    st = lib.kf_stage_init(ctypes.byref(odd), 0, 1, 0, ctypes.byref(stage.Weights(None, 0)), None, ctypes.byref(out))
+    assert st == 1 and b"qk_norm" in lib.kf_last_error()
+
+
+def test_qk_norm_block_bytes_include_the_gains():
+    from paper_2609_34045_amd import stage
+    for shape in (synth.SHAPE_QWEN3_TINY, synth.SHAPE_QWEN3_8B, synth.SHAPE_QWEN3_32B):
+        bb = stage.stage_bytes(shape, 0, 1, False, 1, 64)[0]
+        assert bb == shape.block_bytes()
+        plain = synth.ModelShape(**{**shape.__dict__, "qk_norm": False})
+        assert bb == plain.block_bytes() + 2 * 2 * shape.head_dim
+    # Qwen3-8B-shaped block: q 4096x4096, k and v 1024x4096, o 4096x4096, three 12288x4096, gains
+    assert synth.SHAPE_QWEN3_8B.block_bytes() == 2 * (2 * 4096 * 4096 + 2 * 1024 * 4096 + 3 * 12288 * 4096 + 2 * 4096 + 2 * 128)
 
 
 def test_null_handles_are_rejected(lib):
