@@ -209,7 +209,8 @@ class Stage:
         """
         mask = 0
         if enable:
-            mask = 0xFFFF if classes is None else sum(1 << KERNEL_CLASSES.index(c) for c in classes)
+            all_classes = (1 << len(KERNEL_CLASSES)) - 1
+            mask = all_classes if classes is None else sum(1 << KERNEL_CLASSES.index(c) for c in classes)
         _check(self._lib.kf_stage_profile(self.handle, mask), "kf_stage_profile")
 
     def profile_read(self) -> dict:

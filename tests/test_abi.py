@@ -173,3 +173,14 @@ def test_null_handles_are_rejected(lib):
     assert lib.kf_kv_destroy(None) == 1
     assert lib.kf_stage_decode(None, None, 1, None, None, None, None, None, 0) == 1
     assert lib.kf_head_argmax(None, 1, None, 0, None, None) == 1
+
+
+def test_kernel_classes_match_the_header():
+    from paper_2609_34045_amd import stage
+    text = open(os.path.join(ROOT, "include", "kafila_stage.h")).read()
+    count = int(re.search(r"KF_K_COUNT\s*=\s*(\d+)", text).group(1))
+    assert len(stage.KERNEL_CLASSES) == count
+    assert int(re.search(r"#define KF_K_ALL (0x[0-9a-fA-F]+)", text).group(1), 16) == (1 << count) - 1
+    names = re.findall(r"KF_K_([A-Z_]+)\s*=\s*(\d+),", text)
+    for name, idx in names:
+        assert stage.KERNEL_CLASSES[int(idx)] == name.lower(), name
