@@ -559,9 +559,17 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
 // about KF_ATTN_TARGET_WGS workgroups carry keys however ragged the contexts
 // are (a row shorter than the longest has idle trailing splits, which exit at
 // once).  The split never exceeds the partial-buffer capacity per row.
+// Keys per split-KV workgroup: about KF_ATTN_TARGET_WGS workgroups for the whole
+// batch (few, long splits keep the merge cheap at short contexts), but no more
+// than KF_ATTN_KEYS_PER_WG keys each, so that long contexts spread over more
+// workgroups (a workgroup streams its keys with only one chunk in flight).
+#ifndef KF_ATTN_KEYS_PER_WG
+#define KF_ATTN_KEYS_PER_WG 512
+#endif
 static void attn_split(int nkv, int64_t total_len, int max_len, int max_split, int* split, int* n_split) {
   auto up = [](int64_t v) { return (int)((v + KF_ATTN_ALIGN - 1) / KF_ATTN_ALIGN * KF_ATTN_ALIGN); };
   int sp = up((total_len * nkv + KF_ATTN_TARGET_WGS - 1) / KF_ATTN_TARGET_WGS);
+  if (sp > KF_ATTN_KEYS_PER_WG) sp = KF_ATTN_KEYS_PER_WG;
   const int need = up((max_len + max_split - 1) / max_split);
   if (sp < need) sp = need;
   if (sp < kAttnMinSplit) sp = kAttnMinSplit;

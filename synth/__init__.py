@@ -156,6 +156,11 @@ WORKLOADS = {
                        notes="layers [16,32) of 64, four users at context 4096"),
     "70b": Workload(5, "70b", SHAPE_70B, 40, 50, False, 1, (4096,), 64, prefill_chunk=512,
                     notes="layers [40,50) of 80; prefill chunks of 512 into 4096, then 64 decode steps"),
+    # long declared context: the KV reads (134 MB per layer) are a quarter of the step
+    "8b_mid_32k": Workload(8, "8b_mid_32k", SHAPE_8B, 8, 16, False, 1, (32768,), 64,
+                           notes="layers [8,16) of 32, KV injected for [0,32768)"),
+    "8b_b4_32k": Workload(9, "8b_b4_32k", SHAPE_8B, 8, 16, False, 4, (32768, 16384, 8192, 1024), 32,
+                          notes="layers [8,16) of 32, four users up to 32768 keys"),
     # Qwen3-style blocks (the paper's served family), same roles as 8b_mid / 32b_b1
     "qwen3_8b_mid": Workload(6, "qwen3_8b_mid", SHAPE_QWEN3_8B, 9, 18, False, 1, (2048,), 64,
                              notes="layers [9,18) of 36, KV injected for [0,2048)"),

@@ -185,3 +185,14 @@ def test_70b_stage_decode(torch, kf):
     decode_steps(torch, g, kv, o, wl, [0], 1)
     kv.close()
     g.close()
+
+
+def test_8b_long_context_decode(torch, kf):
+    """Ragged contexts up to 32768 keys (64 splits of 512 keys per head) on one 8B-shaped layer."""
+    wl = synth.WORKLOADS["8b_b4_32k"]
+    g, kv, o, _ = build(torch, kf, wl, 8, 9, 4, 32800, wl.contexts, cache_weights=True)
+    worst = decode_steps(torch, g, kv, o, wl, [0, 1, 2, 3], 2)
+    worst = max(worst, decode_steps(torch, g, kv, o, wl, [0], 1, first_step=5))
+    print("long-context max row rel err", worst)
+    kv.close()
+    g.close()
