@@ -17,31 +17,10 @@
 
 using namespace kf;
 
-// Launch-shape tunables (compile-time; the defaults are the measured best on MI355X).
-#ifndef KF_R_QKV
-#define KF_R_QKV 8
-#endif
-#ifndef KF_R_GATEUP
-#define KF_R_GATEUP 8
-#endif
-#ifndef KF_R_DOWN
-#define KF_R_DOWN 8
-#endif
-#ifndef KF_R_LMHEAD
-#define KF_R_LMHEAD 8
-#endif
-#ifndef KF_U_QKV
-#define KF_U_QKV 1
-#endif
-#ifndef KF_U_GATEUP
-#define KF_U_GATEUP 1
-#endif
-#ifndef KF_U_DOWN
-#define KF_U_DOWN 1
-#endif
-#ifndef KF_U_LMHEAD
-#define KF_U_LMHEAD 1
-#endif
+// Launch shapes (compile-time; the defaults are the measured best on MI355X).
+// Decode GEMVs take 8 output rows per workgroup and one 16-byte chunk per row in
+// flight per thread (other shapes were measured slower at every batch).
+constexpr int kGemvRows = 8, kGemvChunks = 1;
 #ifndef KF_ATTN_TARGET_WGS
 #define KF_ATTN_TARGET_WGS 256
 #endif
@@ -384,7 +363,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->act = (float*)take(B * F * 4);
   if (c.qk_norm) s->kraw = (float*)take(B * c.n_kv_heads * hd * 4);
   if (has_head) {
-    s->lm_wg = (int)((V + KF_R_LMHEAD - 1) / KF_R_LMHEAD);
+    s->lm_wg = (int)((V + kGemvRows - 1) / kGemvRows);
     s->part_val = (float*)take(B * s->lm_wg * 4);
     s->part_idx = (int*)take(B * s->lm_wg * 4);
   }
@@ -647,9 +626,9 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.vocab = c.vocab;
       g.x_init = s->x;
       g.err_flag = s->err_flag;
-      le = launch_gemv_src(kEpiQKV, KF_R_QKV, KF_U_QKV, true, g, st);
+      le = launch_gemv_src(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
     } else {
-      le = launch_gemv(kEpiQKV, KF_R_QKV, KF_U_QKV, true, g, st);
+      le = launch_gemv(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
     }
     tr.end(KF_K_QKV);
     KF_HIP(le, "qkv launch");
@@ -723,7 +702,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.act = s->act;
     {
       tr.begin(KF_K_GATEUP);
-      const hipError_t le = launch_gemv(kEpiSwiGLU, KF_R_GATEUP, KF_U_GATEUP, true, gu, st);
+      const hipError_t le = launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
       tr.end(KF_K_GATEUP);
       KF_HIP(le, "gate/up launch");
     }
@@ -741,7 +720,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
     {
       tr.begin(KF_K_DOWN);
-      const hipError_t le = launch_gemv(kEpiResid, KF_R_DOWN, KF_U_DOWN, false, d, st);
+      const hipError_t le = launch_gemv(kEpiResid, kGemvRows, kGemvChunks, false, d, st);
       tr.end(KF_K_DOWN);
       KF_HIP(le, "down launch");
     }
@@ -775,10 +754,10 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.logits = logits;
   g.part_val = s->part_val;
   g.part_idx = s->part_idx;
-  g.n_wg = gemv_grid(kEpiLMHead, KF_R_LMHEAD, g);
+  g.n_wg = gemv_grid(kEpiLMHead, kGemvRows, g);
   s->lm_wg_used = g.n_wg;
   tr.begin(KF_K_LMHEAD);
-  const hipError_t e = launch_gemv_src(kEpiLMHead, KF_R_LMHEAD, KF_U_LMHEAD, true, g, s->stream);
+  const hipError_t e = launch_gemv_src(kEpiLMHead, kGemvRows, kGemvChunks, true, g, s->stream);
   tr.end(KF_K_LMHEAD);
   KF_HIP(e, "lm-head launch");
   return KF_OK;
