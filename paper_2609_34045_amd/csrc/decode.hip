@@ -51,7 +51,9 @@ __device__ __forceinline__ void bf16x8(const v4u w, float (&f)[8]) {
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f8 __attribute__((ext_vector_type(8)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 
 // 8 fp16 (16 bytes) to fp32.
 __device__ __forceinline__ void f16x8(const v4u w, float (&f)[8]) {
@@ -490,34 +492,53 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   };
   if (c0 < nk) load_chunk(c0);
 
-  float qv[G][8];
+  // The scaled query as fp16 pairs: a score is then 4 packed fp16 dot products
+  // (fp32 accumulation) against the key's fp16 values as stored in the cache.
+  h2 qh[G][4];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const v4f* src = reinterpret_cast<const v4f*>(p.q + (int64_t)b * p.nq * HD + (hq0 + h) * HD + d0);
-    const v4f lo = src[0], hi = src[1];
-    qv[h][0] = lo.x * p.scale_log2; qv[h][1] = lo.y * p.scale_log2;
-    qv[h][2] = lo.z * p.scale_log2; qv[h][3] = lo.w * p.scale_log2;
-    qv[h][4] = hi.x * p.scale_log2; qv[h][5] = hi.y * p.scale_log2;
-    qv[h][6] = hi.z * p.scale_log2; qv[h][7] = hi.w * p.scale_log2;
+    const v4f lo = src[0] * p.scale_log2, hi = src[1] * p.scale_log2;
+    qh[h][0] = __builtin_convertvector(f2{lo.x, lo.y}, h2);
+    qh[h][1] = __builtin_convertvector(f2{lo.z, lo.w}, h2);
+    qh[h][2] = __builtin_convertvector(f2{hi.x, hi.y}, h2);
+    qh[h][3] = __builtin_convertvector(f2{hi.z, hi.w}, h2);
   }
 
   for (; c0 < nk; c0 += 4 * CH) {
     float sc[J][G];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      float kf[8];
-      f16x8(kw[j], kf);
+      // Pairs are taken from the whole 8-half vector by shuffles (a bit cast of a
+      // single dword element of the loaded vector is lowered to element 0).
+      const h8 k8 = __builtin_bit_cast(h8, kw[j]);
+      const h2 k0 = __builtin_shufflevector(k8, k8, 0, 1), k1 = __builtin_shufflevector(k8, k8, 2, 3),
+               k2 = __builtin_shufflevector(k8, k8, 4, 5), k3 = __builtin_shufflevector(k8, k8, 6, 7);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        float a = 0.f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) a += qv[h][i] * kf[i];
+        float a = __builtin_amdgcn_fdot2(k0, qh[h][0], 0.f, false);
+        a = __builtin_amdgcn_fdot2(k1, qh[h][1], a, false);
+        a = __builtin_amdgcn_fdot2(k2, qh[h][2], a, false);
+        a = __builtin_amdgcn_fdot2(k3, qh[h][3], a, false);
         sc[j][h] = group_sum<LPK>(a);
       }
     }
-    float vf[J][8];
+    // V of key pairs (2m, 2m+1) regrouped per dimension: vp[m][i] = (v_2m[i], v_2m+1[i]),
+    // so P.V is a packed fp16 dot product per dimension and key pair.
+    static_assert(J % 2 == 0, "keys come in pairs");
+    h2 vp[J / 2][8];
 #pragma unroll
-    for (int j = 0; j < J; ++j) f16x8(vw[j], vf[j]);
+    for (int m = 0; m < J / 2; ++m) {
+      const h8 a = __builtin_bit_cast(h8, vw[2 * m]), c = __builtin_bit_cast(h8, vw[2 * m + 1]);
+      vp[m][0] = __builtin_shufflevector(a, c, 0, 8);
+      vp[m][1] = __builtin_shufflevector(a, c, 1, 9);
+      vp[m][2] = __builtin_shufflevector(a, c, 2, 10);
+      vp[m][3] = __builtin_shufflevector(a, c, 3, 11);
+      vp[m][4] = __builtin_shufflevector(a, c, 4, 12);
+      vp[m][5] = __builtin_shufflevector(a, c, 5, 13);
+      vp[m][6] = __builtin_shufflevector(a, c, 6, 14);
+      vp[m][7] = __builtin_shufflevector(a, c, 7, 15);
+    }
     bool okc[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) okc[j] = ok[j];
@@ -532,17 +553,22 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
       mc = fmaxf(mc, __shfl_xor(mc, 16));
       mc = fmaxf(mc, __shfl_xor(mc, 32));
       const float m_new = fmaxf(m_run[h], mc);
-      const float alpha = exp2f(m_run[h] - m_new);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[h] - m_new);  // 0 while m_run is -inf
       m_run[h] = m_new;
       l_run[h] *= alpha;
 #pragma unroll
       for (int i = 0; i < 8; ++i) acc[h][i] *= alpha;
+      float pj[J];
 #pragma unroll
       for (int j = 0; j < J; ++j) {
-        const float pj = okc[j] ? exp2f(sc[j][h] - m_new) : 0.f;
-        l_run[h] += pj;
+        pj[j] = okc[j] ? __builtin_amdgcn_exp2f(sc[j][h] - m_new) : 0.f;
+        l_run[h] += pj[j];
+      }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[h][i] += pj * vf[j][i];
+      for (int m = 0; m < J / 2; ++m) {
+        const h2 pp = __builtin_convertvector(f2{pj[2 * m], pj[2 * m + 1]}, h2);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[h][i] = __builtin_amdgcn_fdot2(vp[m][i], pp, acc[h][i], false);
       }
     }
   }
