@@ -142,6 +142,12 @@ kf_status kf_stage_set_stream(kf_stage* stage, void* hip_stream);
 /* Wait for all enqueued work; KF_EDEVICE (with the HIP error text) if any of it failed. */
 kf_status kf_stage_sync(kf_stage* stage);
 
+/* What a stage holds: its config, layer range [layer_lo, layer_hi), whether it holds
+ * the head, the stream it enqueues on (a hipStream_t) and its device ordinal.  Any
+ * output pointer may be NULL.  Host-only. */
+kf_status kf_stage_describe(const kf_stage* stage, kf_model_config* cfg, int32_t* layer_lo, int32_t* layer_hi,
+                            int32_t* has_head, void** hip_stream, int32_t* device);
+
 /*
  * Reserve a KV cache for max_users concurrent users of context up to max_ctx tokens
  * each, for every layer the stage holds (the declared concurrency x context of
@@ -152,6 +158,9 @@ kf_status kf_stage_sync(kf_stage* stage);
  */
 kf_status kf_kv_create(kf_stage* stage, int32_t max_users, int32_t max_ctx, kf_kv** out);
 kf_status kf_kv_destroy(kf_kv* kv);
+
+/* The stage a cache was created on, and its capacity.  Any output pointer may be NULL.  Host-only. */
+kf_status kf_kv_describe(const kf_kv* kv, kf_stage** stage, int32_t* max_users, int32_t* max_ctx);
 
 /* Number of cached positions of a user (a host-side value; no device sync). */
 kf_status kf_kv_len(const kf_kv* kv, int32_t user, int32_t* len);

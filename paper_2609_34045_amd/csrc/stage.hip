@@ -391,6 +391,18 @@ kf_status kf_stage_set_stream(kf_stage* s, void* hip_stream) {
   return KF_OK;
 }
 
+kf_status kf_stage_describe(const kf_stage* s, kf_model_config* cfg, int32_t* lo, int32_t* hi, int32_t* has_head,
+                            void** hip_stream, int32_t* device) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  if (cfg) *cfg = s->cfg;
+  if (lo) *lo = s->lo;
+  if (hi) *hi = s->hi;
+  if (has_head) *has_head = s->has_head;
+  if (hip_stream) *hip_stream = (void*)s->stream;
+  if (device) *device = s->device;
+  return KF_OK;
+}
+
 kf_status kf_stage_sync(kf_stage* s) {
   if (!s) return fail(KF_EINVAL, "stage is NULL");
   KF_HIP(hipStreamSynchronize(s->stream), "stream synchronize");
@@ -475,6 +487,14 @@ kf_status kf_kv_destroy(kf_kv* kv) {
   for (void* m : mem) hipFree(m);
   kv->st->live_kv--;
   delete kv;
+  return KF_OK;
+}
+
+kf_status kf_kv_describe(const kf_kv* kv, kf_stage** stage, int32_t* max_users, int32_t* max_ctx) {
+  if (!kv) return fail(KF_EINVAL, "kv is NULL");
+  if (stage) *stage = kv->st;
+  if (max_users) *max_users = kv->max_users;
+  if (max_ctx) *max_ctx = kv->max_ctx;
   return KF_OK;
 }
 

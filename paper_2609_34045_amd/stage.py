@@ -30,7 +30,7 @@ HEAD_KINDS = {"embed": 9, "final_norm": 10, "lm_head": 11}
 EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init", "kf_stage_destroy",
            "kf_stage_set_stream", "kf_stage_sync", "kf_kv_create", "kf_kv_destroy", "kf_kv_len", "kf_kv_set_len",
            "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax",
-           "kf_stage_profile", "kf_stage_profile_read")
+           "kf_stage_profile", "kf_stage_profile_read", "kf_stage_describe", "kf_kv_describe")
 
 # kf_kernel_class
 KERNEL_CLASSES = ("prep", "qkv", "attn", "oproj", "gateup", "down", "lmhead", "argmax", "pf_norm", "pf_qkv", "pf_rope",
@@ -98,6 +98,8 @@ def load_library(path: str = LIB_PATH):
         "kf_head_argmax": (I32, [P, I32, VP, I32, VP, VP]),
         "kf_stage_profile": (I32, [P, I32]),
         "kf_stage_profile_read": (I32, [P, I32, I64P, ctypes.POINTER(ctypes.c_double)]),
+        "kf_stage_describe": (I32, [P, ctypes.POINTER(ModelConfig), I32P, I32P, I32P, ctypes.POINTER(VP), I32P]),
+        "kf_kv_describe": (I32, [P, ctypes.POINTER(P), I32P, I32P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -201,6 +203,15 @@ class Stage:
 
     def sync(self):
         _check(self._lib.kf_stage_sync(self.handle), "kf_stage_sync")
+
+    def describe(self) -> dict:
+        """The library's own record of the stage (kf_stage_describe)."""
+        cfg, lo, hi, head, dev = ModelConfig(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        st = ctypes.c_void_p()
+        _check(self._lib.kf_stage_describe(self.handle, ctypes.byref(cfg), ctypes.byref(lo), ctypes.byref(hi),
+                                           ctypes.byref(head), ctypes.byref(st), ctypes.byref(dev)), "kf_stage_describe")
+        return {"config": cfg, "lo": lo.value, "hi": hi.value, "has_head": bool(head.value), "stream": st.value or 0,
+                "device": dev.value}
 
     def profile(self, enable, classes=None):
         """Start (clearing earlier records) or stop per-kernel HIP-event timing.
@@ -324,6 +335,12 @@ class KV:
 
     def set_len(self, user: int, n: int):
         _check(self._lib.kf_kv_set_len(self.handle, user, n), "kf_kv_set_len")
+
+    def describe(self) -> dict:
+        owner, mu, mc = ctypes.c_void_p(), ctypes.c_int32(), ctypes.c_int32()
+        _check(self._lib.kf_kv_describe(self.handle, ctypes.byref(owner), ctypes.byref(mu), ctypes.byref(mc)),
+               "kf_kv_describe")
+        return {"stage": owner.value, "max_users": mu.value, "max_ctx": mc.value}
 
     def write(self, layer: int, user: int, pos0: int, k, v):
         """k, v: device tensors [n, nkv, hd]: float32, float16, bfloat16, or int16 holding bf16 bits."""

@@ -38,9 +38,9 @@ def test_header_declares_the_boundary():
 
 
 def test_library_exports_every_declared_symbol(lib):
-    from paper_2609_34045_amd import planner, stage
+    from paper_2609_34045_amd import planner, ring, stage
     names = declared_functions()
-    assert set(names) == set(stage.EXPORTS) | set(planner.EXPORTS)
+    assert set(names) == set(stage.EXPORTS) | set(planner.EXPORTS) | set(ring.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -173,6 +173,33 @@ def test_null_handles_are_rejected(lib):
     assert lib.kf_kv_destroy(None) == 1
     assert lib.kf_stage_decode(None, None, 1, None, None, None, None, None, 0) == 1
     assert lib.kf_head_argmax(None, 1, None, 0, None, None) == 1
+
+
+def test_ring_rejects_before_touching_the_device(lib):
+    """Ring argument checks that return before any stage or device is touched."""
+    from paper_2609_34045_amd import ring
+    r = ring._lib()
+    out = ctypes.c_void_p(123)
+    P = ctypes.c_void_p
+    assert r.kf_ring_create(0, (P * 1)(), (P * 1)(), 1, 1, 0, ctypes.byref(out)) == 1
+    assert out.value is None and b"n_members" in lib.kf_last_error()
+    assert r.kf_ring_create(1, None, None, 1, 1, 0, ctypes.byref(out)) == 1
+    assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 0, 1, 0, ctypes.byref(out)) == 1
+    assert b"max_groups" in lib.kf_last_error()
+    assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 65, 1, 0, ctypes.byref(out)) == 1
+    assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 4, 0, 0, ctypes.byref(out)) == 1
+    assert b"max_prefill" in lib.kf_last_error()
+    assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 4, 8, 2, ctypes.byref(out)) == 1  # fp16 hand-off
+    assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 4, 8, 0, ctypes.byref(out)) == 1  # NULL stage
+    assert b"stages[0]" in lib.kf_last_error()
+    assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 4, 8, 0, None) == 1
+    one = (ctypes.c_int32 * 1)(1)
+    assert r.kf_ring_generate(None, 1, one, one, P(8), 1, P(8)) == 1
+    assert r.kf_ring_prefill(None, 0, 1, P(8), P(8)) == 1
+    assert r.kf_ring_sync(None) == 1
+    assert r.kf_ring_destroy(None) == 1
+    assert lib.kf_stage_describe(None, None, None, None, None, None, None) == 1
+    assert lib.kf_kv_describe(None, None, None, None) == 1
 
 
 def test_kernel_classes_match_the_header():

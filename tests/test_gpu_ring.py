@@ -1,0 +1,167 @@
+"""The ring (include/kafila_ring.h) on the GPU against the float64 oracle of the whole model.
+
+Stages chained head first, each on its own stream, prefill prompts of ragged
+lengths and then generate for several request groups at once.  The oracle runs
+the whole model as one stage, teacher-forced on the ring's own tokens: every
+sampled token must be the oracle's greedy choice, or a near tie (oracle logit
+gap within NEAR_TIE of the largest |logit|; at most one per case).  Every call
+goes through the C ABI.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleStage
+from tests.helpers import SeededModel
+
+pytestmark = pytest.mark.gpu
+
+NEAR_TIE = 5e-3
+TINY4 = synth.ModelShape(**{**synth.SHAPE_TINY.__dict__, "n_layers": 4})
+QWEN3_TINY3 = synth.ModelShape(**{**synth.SHAPE_QWEN3_TINY.__dict__, "n_layers": 3})
+BLOCKS_8B = synth.ModelShape(**{**synth.SHAPE_8B.__dict__, "n_layers": 2})
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+@pytest.fixture(scope="module")
+def kf():
+    from paper_2609_34045_amd import ring, stage
+    return stage, ring
+
+
+def token_ok(t_gpu: int, logits: np.ndarray):
+    """(accepted, near tie) for a sampled token against the oracle's logits."""
+    t_ref = int(np.argmax(logits))  # lowest index on ties
+    if t_gpu == t_ref:
+        return True, False
+    gap = float(logits[t_ref] - logits[t_gpu])
+    return gap <= NEAR_TIE * float(np.max(np.abs(logits))), True
+
+
+def build(torch, kf, shape, model, bounds, n_users, ctx, shared_stream=False, io=None, max_groups=4):
+    st, rg = kf
+    one = torch.cuda.Stream()
+    stages, kvs = [], []
+    for i, (lo, hi) in enumerate(bounds):
+        s = one if shared_stream else torch.cuda.Stream()
+        g = st.Stage(shape, lo, hi, model.layer, model.head() if i == 0 else None, stream=s)
+        stages.append(g)
+        kvs.append(g.kv(n_users, ctx))
+    return rg.Ring(stages, kvs, max_groups=max_groups, max_prefill=64, io=io), stages, kvs
+
+
+def close(ring, stages, kvs):
+    ring.close()
+    for kv in kvs:
+        kv.close()
+    for g in stages:
+        g.close()
+
+
+def run_case(torch, kf, shape, cfg_id, bounds, prompt_lens, groups, steps, **kw):
+    model = SeededModel(shape, cfg_id)
+    prompts = [synth.tokens(cfg_id, 100 + u, n, shape.vocab) for u, n in enumerate(prompt_lens)]
+    ctx = max(prompt_lens) + steps + 4
+    ring, stages, kvs = build(torch, kf, shape, model, bounds, len(prompts), ctx, **kw)
+    oracle = OracleStage(shape, 0, shape.n_layers, model.layer, model.head(), max_users=len(prompts), max_ctx=ctx)
+    near = 0
+    firsts = []
+    for u, p in enumerate(prompts):
+        tok = torch.from_numpy(p.astype(np.int32)).cuda()
+        torch.cuda.synchronize()  # the ring's streams read it
+        firsts.append(ring.prefill(u, tok))
+    ring.sync()
+    prev = {}
+    for u, p in enumerate(prompts):
+        t_gpu = int(firsts[u].cpu()[0])
+        ok, tie = token_ok(t_gpu, oracle.logits(oracle.prefill(u, 0, tokens=p)[-1:])[0])
+        assert ok, f"prefill of user {u}: token {t_gpu}"
+        near += tie
+        prev[u] = t_gpu
+    order = [u for g in groups for u in g]
+    tin = torch.tensor([prev[u] for u in order], dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    out = ring.generate(groups, tin, steps)
+    ring.sync()
+    toks = out.cpu().numpy()
+    assert toks.shape == (steps, len(order))
+    for t in range(steps):
+        for g in groups:
+            h = oracle.decode(g, [oracle.kv.len[u] for u in g], tokens=np.array([prev[u] for u in g], dtype=np.int64))
+            lr = oracle.logits(h)
+            for b, u in enumerate(g):
+                t_gpu = int(toks[t, order.index(u)])
+                ok, tie = token_ok(t_gpu, lr[b])
+                assert ok, f"step {t} user {u}: token {t_gpu}"
+                near += tie
+                prev[u] = t_gpu
+    for i, kv in enumerate(kvs):
+        for u in order:
+            assert kv.len(u) == prompt_lens[u] + steps, (i, u)
+    assert near <= 1, f"{near} near ties"
+    print(shape, bounds, "near ties", near)
+    close(ring, stages, kvs)
+
+
+def test_tiny_three_members_three_groups(torch, kf):
+    """Ragged prompts, groups of 2, 1 and 3 users, more groups than members."""
+    run_case(torch, kf, TINY4, 21, [(0, 1), (1, 3), (3, 4)], (5, 17, 9, 30, 1, 12), [[0, 1], [2], [3, 4, 5]], 6)
+
+
+@pytest.mark.parametrize("variant", ["one_member", "shared_stream", "bf16_handoff", "fewer_groups_than_members"])
+def test_tiny_ring_variants(torch, kf, variant):
+    if variant == "one_member":
+        run_case(torch, kf, TINY4, 22, [(0, 4)], (6, 3), [[0], [1]], 5)
+    elif variant == "shared_stream":
+        run_case(torch, kf, TINY4, 23, [(0, 2), (2, 4)], (4, 8, 2), [[0, 2], [1]], 5, shared_stream=True)
+    elif variant == "bf16_handoff":
+        run_case(torch, kf, TINY4, 24, [(0, 1), (1, 4)], (7, 11), [[1, 0]], 5, io=torch.bfloat16)
+    else:
+        run_case(torch, kf, TINY4, 25, [(0, 1), (1, 2), (2, 3), (3, 4)], (3, 5, 2, 4), [[0, 1, 2, 3]], 4)
+
+
+def test_qwen3_tiny_ring(torch, kf):
+    run_case(torch, kf, QWEN3_TINY3, 26, [(0, 1), (1, 3)], (9, 4, 14), [[2], [0, 1]], 5)
+
+
+def test_8b_blocks_two_members(torch, kf):
+    """Full 8B block and head shapes (vocab 128256), two members of one block each."""
+    run_case(torch, kf, BLOCKS_8B, 27, [(0, 1), (1, 2)], (7, 12, 3), [[0, 2], [1]], 3)
+
+
+def test_ring_checks_run_before_anything_is_enqueued(torch, kf):
+    st, rg = kf
+    model = SeededModel(TINY4, 28)
+    ring, stages, kvs = build(torch, kf, TINY4, model, [(0, 2), (2, 4)], 3, 16)
+    tok = torch.zeros(4, dtype=torch.int32, device="cuda")
+    kvs[1].set_len(0, 3)  # user 0 now disagrees between the members
+    with pytest.raises(st.KFError) as e:
+        ring.generate([[0], [1]], tok[:2], 2)
+    assert e.value.status == st.KF_EINVAL and "member 1" in e.value.message
+    with pytest.raises(st.KFError):
+        ring.prefill(0, tok)
+    with pytest.raises(st.KFError) as e:  # 14 + 3 positions exceed max_ctx 16
+        kvs[0].set_len(1, 14)
+        kvs[1].set_len(1, 14)
+        ring.generate([[1]], tok[:1], 3)
+    assert e.value.status == st.KF_ERANGE
+    with pytest.raises(st.KFError):  # a user twice
+        ring.generate([[2], [2]], tok[:2], 1)
+    with pytest.raises(st.KFError):  # five users in one group
+        ring.generate([[0, 1, 2, 0, 1]], torch.zeros(5, dtype=torch.int32, device="cuda"), 1)
+    assert [kv.len(u) for kv in kvs for u in range(3)] == [0, 14, 0, 3, 14, 0]
+    # chains that are not a ring of this model
+    with pytest.raises(st.KFError):
+        rg.Ring(stages[::-1], kvs[::-1])  # head stage not first
+    with pytest.raises(st.KFError):
+        rg.Ring(stages[:1], kvs[:1])  # does not reach the last layer
+    with pytest.raises(st.KFError):
+        rg.Ring(stages, kvs[::-1])  # a cache of another stage
+    close(ring, stages, kvs)
