@@ -55,6 +55,9 @@ def parse():
                          "measured batch-1 stage times (8B-shaped stages of 1-16 blocks and with the head, 32B, 70B)")
     ap.add_argument("--prefill", action="store_true",
                     help="time the workload's prefill chunk (matrix cores) instead of decode")
+    ap.add_argument("--ring", action="store_true",
+                    help="the whole 8B-shaped model as a ring of stages on this GPU: four concurrent users "
+                         "against one user, in turn, batched, and over 2 and 4 members on their own streams")
     return ap.parse_args()
 
 
@@ -275,6 +278,77 @@ def bench_cost_model(args, torch, kf):
     }), flush=True)
 
 
+def bench_ring(args, torch, kf):
+    """Section VII-C's concurrency on one GPU: the ring's members overlap on their own streams.
+
+    The whole 32-layer 8B-shaped model plus its head, divided into 1, 2 or 4
+    members of equal block ranges (the head on member 0).  Four users each hold
+    a 2048-token prompt, prefilled through the ring; then every configuration
+    generates `steps` tokens per user.  Timing depends on shapes only, so every
+    layer reuses one seeded layer's tensors (each member gets its own device
+    copy).  On one GPU the members share the HBM: the ring can only gain what
+    one stream leaves idle between its kernels.
+    """
+    from paper_2609_34045_amd import ring as kr
+    shape, cfg_id, prompt, n_users = synth.SHAPE_8B, 2, 2048, 4
+    steps, warmup = max(args.steps // 4, 8), max(args.warmup // 2, 2)
+    t0 = time.perf_counter()
+    lw = synth.layer_weights(shape, cfg_id, 0)
+    head = synth.head_weights(shape, cfg_id)
+    log(f"[ring] weights generated in {time.perf_counter() - t0:.1f} s")
+    prompts = [synth.tokens(cfg_id, 200 + u, prompt, shape.vocab) for u in range(n_users)]
+    cases = [("one user", 1, [[0]]), ("4 users in turn, 1 member", 1, [[0], [1], [2], [3]]),
+             ("4 users batched, 1 member", 1, [[0, 1, 2, 3]]), ("4 users, 2 members", 2, [[0], [1], [2], [3]]),
+             ("4 users, 4 members", 4, [[0], [1], [2], [3]]), ("4 users batched, 2 members", 2, [[0, 1, 2, 3]]),
+             ("2 groups of 2, 2 members", 2, [[0, 1], [2, 3]])]
+    rows = []
+    for name, m, groups in cases:
+        per = shape.n_layers // m
+        streams = [torch.cuda.Stream() for _ in range(m)]
+        stages = [kf.Stage(shape, i * per, (i + 1) * per, {l: lw for l in range(i * per, (i + 1) * per)},
+                           head if i == 0 else None, stream=streams[i]) for i in range(m)]
+        kvs = [g.kv(n_users, prompt + steps + warmup + 2) for g in stages]
+        ring = kr.Ring(stages, kvs, max_groups=4, max_prefill=512)
+        users = [u for g in groups for u in g]
+        first = {}
+        for u in users:
+            for c0 in range(0, prompt, 512):
+                t = torch.from_numpy(prompts[u][c0:c0 + 512].astype(np.int32)).cuda()
+                torch.cuda.synchronize()
+                first[u] = ring.prefill(u, t)
+        ring.sync()
+        tin = torch.cat([first[u] for u in users])
+        torch.cuda.synchronize()
+        out = ring.generate(groups, tin, warmup)
+        ring.sync()
+        tin = out[-1].clone()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        out = ring.generate(groups, tin, steps)
+        ring.sync()
+        dt = time.perf_counter() - t0
+        toks = steps * len(users)
+        rows.append({"case": name, "members": m, "groups": [len(g) for g in groups], "tokens": toks,
+                     "ms": round(dt * 1e3, 2), "tokens_per_s": round(toks / dt, 1),
+                     "per_user_tokens_per_s": round(steps / dt, 1)})
+        log(f"[ring] {rows[-1]}")
+        ring.close()
+        for kv in kvs:
+            kv.close()
+        for g in stages:
+            g.close()
+        del stages, kvs, ring, out, tin
+        torch.cuda.empty_cache()
+    base = rows[0]["tokens_per_s"]
+    for r in rows:
+        r["vs_one_user"] = round(r["tokens_per_s"] / base, 3)
+    print(json.dumps({
+        "metric": "ring decode tokens/s on one GPU (whole 8B-shaped model + head, 2048-token prompts)",
+        "unit": "tokens/s", "steps_per_user": steps, "warmup": warmup, "rows": rows,
+        "data": "synthetic (one seeded layer's weights in every block; seeded prompts prefilled through the ring)",
+    }), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -299,6 +373,9 @@ def main():
     if args.cost_model:
         torch.cuda.set_device(0)
         return bench_cost_model(args, torch, kf)
+    if args.ring:
+        torch.cuda.set_device(0)
+        return bench_ring(args, torch, kf)
     wl = synth.WORKLOADS[args.workload]
     if args.prefill:
         if not wl.prefill_chunk:
