@@ -55,6 +55,9 @@ def parse():
                          "measured batch-1 stage times (8B-shaped stages of 1-16 blocks and with the head, 32B, 70B)")
     ap.add_argument("--prefill", action="store_true",
                     help="time the workload's prefill chunk (matrix cores) instead of decode")
+    ap.add_argument("--paged", action="store_true",
+                    help="decode over a paged KV cache (a pool of 64-position pages shared by the users, the "
+                         "contexts injected page by page in turn so that every user's pages are scattered)")
     ap.add_argument("--ring", action="store_true",
                     help="the whole 8B-shaped model as a ring of stages on this GPU: four concurrent users "
                          "against one user, in turn, batched, and over 2 and 4 members on their own streams")
@@ -392,13 +395,26 @@ def main():
     t0 = time.perf_counter()
     g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, head)
     span = max(args.steps, args.warmup)
-    kv = g.kv(B, max(ctx) + span + 1)
+    cap = max(ctx) + span + 1
+    page = 64
+    n_pages = sum((c + span + 1 + page - 1) // page for c in ctx) if args.paged else None
+    kv = g.kv(B, cap, pages=n_pages)
     inject = {}
     for l in range(wl.layer_lo, wl.layer_hi):
         for u in range(B):
-            kb, vb = synth.injected_kv(s, wl.cfg_id, l, u, ctx[u], wl.seed)
-            inject[(l, u)] = (kb, vb)
-            kv.write(l, u, 0, torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+            inject[(l, u)] = synth.injected_kv(s, wl.cfg_id, l, u, ctx[u], wl.seed)
+    # A paged cache gets its contexts one page per user in turn, so that each user's pages are scattered.
+    step_pos = page if args.paged else max(ctx)
+    for p0 in range(0, max(ctx), step_pos):
+        for u in range(B):
+            m = min(step_pos, ctx[u] - p0)
+            if m <= 0:
+                continue
+            for l in range(wl.layer_lo, wl.layer_hi):
+                kb, vb = inject[(l, u)]
+                kv.write(l, u, p0, torch.from_numpy(kb[p0:p0 + m].view(np.int16)).cuda(),
+                         torch.from_numpy(vb[p0:p0 + m].view(np.int16)).cuda())
+            kv.set_len(u, p0 + m)
     for u in range(B):
         kv.set_len(u, ctx[u])
     torch.cuda.synchronize()
@@ -497,6 +513,7 @@ def main():
             "contexts": ctx,
             "layers": wl.layer_hi - wl.layer_lo,
             "has_head": wl.has_head,
+            "kv_cache": "paged: 64-position pages from a shared pool, scattered" if args.paged else "reserved per user",
             "parallelism": "single GPU (one stage)",
         },
         "hbm": {"algorithmic_bytes_per_step": sb, "achieved_gbps": round(hbm, 1),

@@ -41,7 +41,9 @@
 extern "C" {
 #endif
 
-#define KF_ABI_VERSION 2  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds */
+#define KF_ABI_VERSION 3  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds;
+                            3: paged KV caches, kf_stage_describe, kf_kv_describe */
+#define KF_KV_PAGE 64     /* positions per KV cache page */
 #define KF_MAX_BATCH 4
 
 typedef struct kf_stage kf_stage;
@@ -151,13 +153,31 @@ kf_status kf_stage_describe(const kf_stage* stage, kf_model_config* cfg, int32_t
 /*
  * Reserve a KV cache for max_users concurrent users of context up to max_ctx tokens
  * each, for every layer the stage holds (the declared concurrency x context of
- * Section V-C).  Layout on the device: fp16 K and V, [layer][user][kv_head][pos][hd]
- * (fp16 keeps 8x the mantissa of bf16 in the same bytes; keys and values must stay
- * below 65504 in magnitude).
+ * Section V-C).  Layout on the device: fp16 K and V in pages of KF_KV_PAGE
+ * positions, [layer][page][kv_head][KF_KV_PAGE][hd]; user u holds pages
+ * u * P .. u * P + P - 1 with P = ceil(max_ctx / KF_KV_PAGE) (fp16 keeps 8x the
+ * mantissa of bf16 in the same bytes; keys and values must stay below 65504 in
+ * magnitude).
  * All user lengths start at 0.  KF_ENOMEM if the device cannot hold it.
  */
 kf_status kf_kv_create(kf_stage* stage, int32_t max_users, int32_t max_ctx, kf_kv** out);
+
+/*
+ * A paged KV cache: the same users and context limits, but only n_pages pages
+ * (>= 1) of KF_KV_PAGE positions for all users together, so that cache is held by
+ * the prompts that arrive rather than reserved for every declared user (the
+ * reservation the paper leaves as future work, Section VIII).  A user is lent
+ * pages from the pool as its length grows (decode, prefill, kf_kv_write,
+ * kf_kv_set_len) and gives back the pages past its new length when
+ * kf_kv_set_len shortens it (0 frees them all).  A call that needs more pages
+ * than are free fails with KF_ENOMEM before anything is enqueued.  A device
+ * table [max_users][P] maps each user's page index to a pool page.
+ */
+kf_status kf_kv_create_paged(kf_stage* stage, int32_t max_users, int32_t max_ctx, int32_t n_pages, kf_kv** out);
 kf_status kf_kv_destroy(kf_kv* kv);
+
+/* Pages of the cache and, for a paged cache, how many are free (0 for a reserved cache).  Host-only. */
+kf_status kf_kv_pages(const kf_kv* kv, int32_t* total, int32_t* free_pages);
 
 /* The stage a cache was created on, and its capacity.  Any output pointer may be NULL.  Host-only. */
 kf_status kf_kv_describe(const kf_kv* kv, kf_stage** stage, int32_t* max_users, int32_t* max_ctx);
@@ -166,20 +186,23 @@ kf_status kf_kv_describe(const kf_kv* kv, kf_stage** stage, int32_t* max_users, 
 kf_status kf_kv_len(const kf_kv* kv, int32_t user, int32_t* len);
 
 /* Set a user's length to any value in [0, max_ctx]: 0 resets the user; positions below
- * len are from then on taken as valid in every layer (e.g. after kf_kv_write). */
+ * len are from then on taken as valid in every layer (e.g. after kf_kv_write).  In a
+ * paged cache the user holds exactly the pages its length needs afterwards
+ * (KF_ENOMEM, with nothing changed, if the pool cannot lend them). */
 kf_status kf_kv_set_len(kf_kv* kv, int32_t user, int32_t len);
 
 /*
  * Copy n positions of keys (already rotated) and values for one held layer and user,
  * from k_dev / v_dev laid out [n, nkv, hd] in dtype (KF_F16 or KF_BF16 bits, or KF_F32),
  * stored as fp16 rounded to nearest even, into positions [pos0, pos0 + n).  Does not
- * change lengths.
+ * change lengths (a paged cache lends the pages up to pos0 + n; KF_ENOMEM if it cannot).
  * KF_ERANGE if pos0 + n > max_ctx.  Enqueued on the stage's stream.
  */
 kf_status kf_kv_write(kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, const void* k_dev,
                       const void* v_dev, kf_dtype dtype);
 
-/* Copy positions [pos0, pos0 + n) of one layer and user out as fp32 (exact), [n, nkv, hd]. */
+/* Copy positions [pos0, pos0 + n) of one layer and user out as fp32 (exact), [n, nkv, hd].
+ * KF_ERANGE for positions on pages the user does not hold (paged caches). */
 kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int32_t n, float* k_dev,
                      float* v_dev);
 
@@ -193,7 +216,9 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
  *   hidden_out_dev : [batch, H] in `io`; may alias hidden_in_dev
  * Row b's token is at positions[b]: its key and value are written at that slot of
  * the user's cache in every held layer, and it attends slots 0..positions[b].
- * On success every user's length advances by one.
+ * On success every user's length advances by one.  A paged cache lends a page to
+ * each user whose position starts one (KF_ENOMEM, nothing enqueued, if the pool
+ * is short for the batch).
  */
 kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32_t* users,
                           const int32_t* positions, const int32_t* tokens_dev, const void* hidden_in_dev,
@@ -203,6 +228,7 @@ kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32
  * Forward a chunk of n_tokens consecutive tokens of one user starting at pos0 (prefill).
  * pos0 must equal the user's length and pos0 + n_tokens <= max_ctx.  Token i attends
  * slots 0..pos0+i.  tokens_dev int32 [n] or hidden_in_dev [n, H]; hidden_out_dev [n, H].
+ * A paged cache lends the pages up to pos0 + n (KF_ENOMEM if it cannot).
  * Dense products run on the matrix cores with fp16 operands (bf16 weights converted
  * exactly while staged) and fp32 accumulation.
  * On success the user's length advances by n_tokens.

@@ -223,12 +223,12 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
           q[i] = z1;
           q[i + half] = z2;
         } else {
-          uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq) * p.max_ctx + pos) * hd;
+          uint16_t* k = p.kc + kv_offset(p.kv, p.users[b], head - p.nq, pos, hd);
           k[i] = f32_to_f16(z1);
           k[i + half] = f32_to_f16(z2);
         }
       } else {
-        uint16_t* v = p.vc + p.users[b] * p.user_stride + ((int64_t)(head - p.nq - p.nkv) * p.max_ctx + pos) * hd;
+        uint16_t* v = p.vc + kv_offset(p.kv, p.users[b], head - p.nq - p.nkv, pos, hd);
         v[i] = f32_to_f16(y1);
         v[i + half] = f32_to_f16(y2);
       }
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   constexpr int CH = KPW * J;      // keys per wave chunk
   constexpr int SUB = 4 * KPW;     // (wave, key group) partial states per workgroup
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int len = p.len[b];
   const int s0 = split * p.split;
   const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
@@ -460,11 +460,22 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   __shared__ float sl[SUB][G];
   __shared__ float sm[4][G];
 
-  const int64_t head_off = (int64_t)p.users[b] * p.user_stride + (int64_t)g * p.max_ctx * HD;
-  const uint16_t* kb = p.kc + head_off + (int64_t)s0 * HD;
-  const uint16_t* vb = p.vc + head_off + (int64_t)s0 * HD;
   const int d0 = (lane % LPK) * 8;
   const int kgrp = lane / LPK;
+  // The split starts on a page boundary (split sizes are multiples of kKvPage)
+  // and a wave's chunk of CH keys, which starts at a multiple of CH, lies in one
+  // page.  A paged cache's page ids for the split (at most kAttnMaxSplit /
+  // kKvPage) are loaded once, lane i holding the split's page i.
+  static_assert(kKvPage % CH == 0 && kAttnMaxSplit / kKvPage <= 64, "chunks within pages");
+  const int u = p.users[b], pg0 = s0 / kKvPage;
+  int pid = 0;
+  if (p.kv.table && lane * kKvPage < nk) pid = p.kv.table[u * p.kv.ppu + pg0 + lane];
+  const int64_t goff = (int64_t)g * kKvPage * HD + d0;
+  auto chunk_base = [&](int c) -> int64_t {  // c: the wave's chunk start, relative to s0
+    const int i = c / kKvPage;
+    const int page = p.kv.table ? __builtin_amdgcn_readlane(pid, i) : u * p.kv.ppu + pg0 + i;
+    return (int64_t)page * p.kv.page_stride + goff + (int64_t)(c % kKvPage) * HD;
+  };
 
   float acc[G][8], m_run[G], l_run[G];
 #pragma unroll
@@ -480,14 +491,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   int c0 = wave * CH;
   v4u kw[J], vw[J];
   bool ok[J];
-  auto load_chunk = [&](int c) {
+  auto load_chunk = [&](int c) {  // keys past nk re-read the chunk's first key (c < nk)
+    const int64_t base = chunk_base(c);
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      const int t = c + j * KPW + kgrp;
-      ok[j] = t < nk;
-      const int tt = ok[j] ? t : 0;
-      kw[j] = *reinterpret_cast<const v4u*>(kb + (int64_t)tt * HD + d0);
-      vw[j] = *reinterpret_cast<const v4u*>(vb + (int64_t)tt * HD + d0);
+      const int r = j * KPW + kgrp;
+      ok[j] = c + r < nk;
+      const int64_t at = base + (int64_t)(ok[j] ? r : 0) * HD;
+      kw[j] = *reinterpret_cast<const v4u*>(p.kc + at);
+      vw[j] = *reinterpret_cast<const v4u*>(p.vc + at);
     }
   };
   if (c0 < nk) load_chunk(c0);
@@ -832,16 +844,16 @@ __global__ void store_hidden_kernel(const float* x, void* out, int out_bf16, int
   else reinterpret_cast<float*>(out)[i] = x[i];
 }
 
-// src [n][nkv][hd] -> dst [kv_head][max_ctx][hd] (dst already offset to the first position), stored as fp16.
-__global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const void* sk, const void* sv, int src_type, int n,
-                                int nkv, int hd, int max_ctx) {
+// src [n][nkv][hd] -> the cache at positions pos0 .. pos0 + n - 1 of one user, stored as fp16.
+__global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const KvPages kp, int user, int pos0, const void* sk,
+                                const void* sv, int src_type, int n, int nkv, int hd) {
   const int64_t total = (int64_t)n * nkv * hd;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= total) return;
   const int d = (int)(i % hd);
   const int g = (int)((i / hd) % nkv);
   const int t = (int)(i / ((int64_t)hd * nkv));
-  const int64_t at = ((int64_t)g * max_ctx + t) * hd + d;
+  const int64_t at = kv_offset(kp, user, g, pos0 + t, hd) + d;
   if (src_type == 2) {
     dk[at] = reinterpret_cast<const uint16_t*>(sk)[i];
     dv[at] = reinterpret_cast<const uint16_t*>(sv)[i];
@@ -854,17 +866,22 @@ __global__ void kv_write_kernel(uint16_t* dk, uint16_t* dv, const void* sk, cons
   }
 }
 
-__global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, float* dk, float* dv, int n, int nkv, int hd,
-                               int max_ctx) {
+__global__ void kv_read_kernel(const uint16_t* sk, const uint16_t* sv, const KvPages kp, int user, int pos0, float* dk,
+                               float* dv, int n, int nkv, int hd) {
   const int64_t total = (int64_t)n * nkv * hd;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= total) return;
   const int d = (int)(i % hd);
   const int g = (int)((i / hd) % nkv);
   const int t = (int)(i / ((int64_t)hd * nkv));
-  const int64_t at = ((int64_t)g * max_ctx + t) * hd + d;
+  const int64_t at = kv_offset(kp, user, g, pos0 + t, hd) + d;
   dk[i] = (float)__builtin_bit_cast(_Float16, sk[at]);
   dv[i] = (float)__builtin_bit_cast(_Float16, sv[at]);
+}
+
+__global__ void kv_table_update_kernel(int* table, const KvTableUpdate u) {
+  const int i = threadIdx.x;
+  if (i < u.n) table[u.idx[i]] = u.val[i];
 }
 
 // ------------------------------------------------------------------ q / k head norms
@@ -890,7 +907,7 @@ __global__ __launch_bounds__(64) void qk_norm_rope_kernel(const QkNormParams p) 
     dst[l] = z1;
     dst[l + HALF] = z2;
   } else {
-    uint16_t* k = p.kc + p.users[b] * p.user_stride + ((int64_t)(h - p.nq) * p.max_ctx + pos) * HD;
+    uint16_t* k = p.kc + kv_offset(p.kv, p.users[b], h - p.nq, pos, HD);
     k[l] = f32_to_f16(z1);
     k[l + HALF] = f32_to_f16(z2);
   }
@@ -1028,19 +1045,25 @@ hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t 
   return hipGetLastError();
 }
 
-hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_type,
-                           int n, int nkv, int hd, int max_ctx, hipStream_t s) {
+hipError_t launch_kv_write(uint16_t* k, uint16_t* v, const KvPages& kp, int user, int pos0, const void* src_k,
+                           const void* src_v, int src_type, int n, int nkv, int hd, hipStream_t s) {
   const int64_t total = (int64_t)n * nkv * hd;
-  hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, dst_k, dst_v, src_k,
-                     src_v, src_type, n, nkv, hd, max_ctx);
+  hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, k, v, kp, user, pos0,
+                     src_k, src_v, src_type, n, nkv, hd);
   return hipGetLastError();
 }
 
-hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, float* dst_k, float* dst_v, int n, int nkv,
-                          int hd, int max_ctx, hipStream_t s) {
+hipError_t launch_kv_read(const uint16_t* k, const uint16_t* v, const KvPages& kp, int user, int pos0, float* dst_k,
+                          float* dst_v, int n, int nkv, int hd, hipStream_t s) {
   const int64_t total = (int64_t)n * nkv * hd;
-  hipLaunchKernelGGL(kv_read_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, src_k, src_v, dst_k,
-                     dst_v, n, nkv, hd, max_ctx);
+  hipLaunchKernelGGL(kv_read_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, k, v, kp, user, pos0,
+                     dst_k, dst_v, n, nkv, hd);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_table_update(int* table, const KvTableUpdate& u, hipStream_t s) {
+  if (u.n < 1 || u.n > kKvTableBatch) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kv_table_update_kernel, dim3(1), dim3(kKvTableBatch), 0, s, table, u);
   return hipGetLastError();
 }
 

@@ -13,6 +13,25 @@ constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound
 constexpr int kOprojRows = 256;     // output rows per workgroup of the head-split output projection
 constexpr int kAttnMaxSplitCount = 1024;  // split-KV workgroups per (row, KV head), upper bound
 
+// KV cache pages.  One layer's K (and, alike, V) is an array of pages of kKvPage
+// positions, each page [kv_head][kKvPage][hd] fp16.  Position t of user u lies
+// at slot t % kKvPage of the page with id table[u * ppu + t / kKvPage] (a paged
+// cache, whose pages come from a shared pool), or u * ppu + t / kKvPage (a
+// cache without a table: each user's ppu pages reserved in order).
+constexpr int kKvPage = 64;
+struct KvPages {
+  const int* table;     // [max_users][ppu] page ids, or NULL
+  int ppu;              // pages per user
+  int64_t page_stride;  // elements per page: nkv * kKvPage * hd
+};
+__device__ __forceinline__ int kv_page(const KvPages& kp, int user, int i) {
+  return kp.table ? kp.table[user * kp.ppu + i] : user * kp.ppu + i;
+}
+// Element offset of (user, kv head g, position t) in a layer's K or V.
+__device__ __forceinline__ int64_t kv_offset(const KvPages& kp, int user, int g, int t, int hd) {
+  return (int64_t)kv_page(kp, user, t / kKvPage) * kp.page_stride + ((int64_t)g * kKvPage + t % kKvPage) * hd;
+}
+
 // Optional per-launch marker around each kernel (instrumentation hook of the runtime).
 struct Tracer {
   void* ctx = nullptr;
@@ -50,10 +69,9 @@ struct GemvParams {
 
   // kEpiQKV
   float* q;            // [B][nq*hd]
-  uint16_t* kc;        // K cache of this layer (fp16 bits): [user][kv_head][pos][hd]
+  uint16_t* kc;        // K cache of this layer (fp16 bits), pages as in KvPages
   uint16_t* vc;
-  int64_t user_stride; // elements between users in kc / vc
-  int max_ctx;
+  KvPages kv;
   int nq, nkv, hd;
   const float* rope_cos;  // [max_ctx][hd/2]
   const float* rope_sin;
@@ -86,12 +104,12 @@ struct GemvParams {
 
 struct AttnParams {
   const float* q;      // [B][nq*hd] rotated queries
-  const uint16_t* kc;  // layer base (fp16 bits), [user][kv_head][pos][hd]
+  const uint16_t* kc;  // layer base (fp16 bits), pages as in KvPages
   const uint16_t* vc;
   float* part_acc;     // [B][nq][max_split][hd]
   float* part_ml;      // [B][nq][max_split][2]
-  int64_t user_stride;
-  int max_ctx, nq, nkv, hd;
+  KvPages kv;
+  int nq, nkv, hd;
   int split;           // keys per workgroup
   int n_split;         // workgroups per (row, kv head)
   int max_split;       // allocated split capacity
@@ -105,13 +123,13 @@ struct AttnParams {
 struct QkNormParams {
   float* q;             // [B][nq][hd]
   const float* kraw;    // [B][nkv][hd]
-  uint16_t* kc;         // layer base of the K cache (fp16 bits)
+  uint16_t* kc;         // layer base of the K cache (fp16 bits), pages as in KvPages
   const uint16_t* gq;   // [hd] bf16 gains
   const uint16_t* gk;
   const float* rope_cos;
   const float* rope_sin;
-  int64_t user_stride;
-  int max_ctx, nq, nkv, hd;
+  KvPages kv;
+  int nq, nkv, hd;
   float eps;
   int users[kMaxBatch];
   int pos[kMaxBatch];
@@ -132,10 +150,19 @@ hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
                                float* max_logit, hipStream_t s);
 hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t n, hipStream_t s);
-// src_type: 0 fp32, 1 bf16, 2 fp16 (the kf_dtype values)
-hipError_t launch_kv_write(uint16_t* dst_k, uint16_t* dst_v, const void* src_k, const void* src_v, int src_type,
-                           int n, int nkv, int hd, int max_ctx, hipStream_t s);
-hipError_t launch_kv_read(const uint16_t* src_k, const uint16_t* src_v, float* dst_k, float* dst_v, int n, int nkv,
-                          int hd, int max_ctx, hipStream_t s);
+// Positions [pos0, pos0 + n) of one user in one layer (k, v: the layer's base)
+// from / to [n][nkv][hd] rows.  src_type: 0 fp32, 1 bf16, 2 fp16 (the kf_dtype values).
+hipError_t launch_kv_write(uint16_t* k, uint16_t* v, const KvPages& kp, int user, int pos0, const void* src_k,
+                           const void* src_v, int src_type, int n, int nkv, int hd, hipStream_t s);
+hipError_t launch_kv_read(const uint16_t* k, const uint16_t* v, const KvPages& kp, int user, int pos0, float* dst_k,
+                          float* dst_v, int n, int nkv, int hd, hipStream_t s);
+// table[idx[i]] = val[i] for i < n (n <= kKvTableBatch): page assignments of a paged cache.
+constexpr int kKvTableBatch = 32;
+struct KvTableUpdate {
+  int n;
+  int idx[kKvTableBatch];
+  int val[kKvTableBatch];
+};
+hipError_t launch_kv_table_update(int* table, const KvTableUpdate& u, hipStream_t s);
 
 }  // namespace kf

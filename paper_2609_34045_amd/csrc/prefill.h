@@ -12,8 +12,8 @@ struct PrefillArgs {
   float eps;
   int T;          // tokens in the chunk
   int pos0;       // position of the first token
-  int max_ctx;
-  int64_t user_stride;
+  int user;       // the user's row of the KV cache
+  KvPages kv;
   const float* rope_cos;  // [max_ctx][hd/2]
   const float* rope_sin;
   hipStream_t stream;
@@ -22,7 +22,7 @@ struct PrefillArgs {
 struct PrefillLayer {
   const uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
   const uint16_t *g_qn, *g_kn;  // per-head q / k norm gains (qk_norm blocks), else NULL
-  uint16_t* kc;  // K cache of this layer and user (fp16 bits): [kv_head][pos][hd]
+  uint16_t* kc;  // K cache of this layer (fp16 bits), pages as in KvPages
   uint16_t* vc;
   void* out;     // hidden output after this layer (last layer only), else NULL
   int out_bf16;

@@ -113,10 +113,9 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const f
 // RMS-normalised over its hd values first: the hd/8 consecutive threads that
 // hold a head add their squares with lane shuffles.
 __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nsplit, int64_t stride, uint16_t* q,
-                                                      uint16_t* kc, uint16_t* vc, const float* cosT,
-                                                      const float* sinT, int nq, int nkv, int hd, int pos0,
-                                                      int max_ctx, const uint16_t* gq, const uint16_t* gk,
-                                                      float eps) {
+                                                      uint16_t* kc, uint16_t* vc, const KvPages kp, int user,
+                                                      const float* cosT, const float* sinT, int nq, int nkv, int hd,
+                                                      int pos0, const uint16_t* gq, const uint16_t* gk, float eps) {
   const int i = blockIdx.x, half = hd / 2, q4 = half / 4, pos = pos0 + i;
   const int nh = nq + 2 * nkv;
   const float* src = qkv + (int64_t)i * nh * hd;
@@ -156,11 +155,11 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
       const v4f s = *reinterpret_cast<const v4f*>(sinT + (int64_t)pos * half + j);
       z1 = a * c - b * s;
       z2 = b * c + a * s;
-      dst = h < nq ? q + ((int64_t)i * nq + h) * hd : kc + ((int64_t)(h - nq) * max_ctx + pos) * hd;
+      dst = h < nq ? q + ((int64_t)i * nq + h) * hd : kc + kv_offset(kp, user, h - nq, pos, hd);
     } else {
       z1 = a;
       z2 = b;
-      dst = vc + ((int64_t)(h - nq - nkv) * max_ctx + pos) * hd;
+      dst = vc + kv_offset(kp, user, h - nq - nkv, pos, hd);
     }
     *reinterpret_cast<uint2*>(dst + j) = uint2{pack_f16(z1.x, z1.y), pack_f16(z1.z, z1.w)};
     *reinterpret_cast<uint2*>(dst + j + half) = uint2{pack_f16(z2.x, z2.y), pack_f16(z2.z, z2.w)};
@@ -188,9 +187,9 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
 constexpr int kRing = KF_PF_ATTN_RING;  // LDS fragment reads in flight ahead of the MFMAs
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
-                                                           const uint16_t* vc, uint16_t* out, float* part_acc,
-                                                           float* part_ml, int T, int nq, int nkv, int pos0,
-                                                           int max_ctx, float scale_log2) {
+                                                           const uint16_t* vc, const KvPages kp, int user,
+                                                           uint16_t* out, float* part_acc, float* part_ml, int T,
+                                                           int nq, int nkv, int pos0, float scale_log2) {
   constexpr int KB = KF_PF_ATTN_KB;  // keys per block: KB / 32 tiles of 32 keys
   constexpr int NT = KB / 32;
   static_assert(KB == 32 || KB == 64, "32 or 64 keys per block");
@@ -226,8 +225,12 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   const int nblk_all = (nkeys + KB - 1) / KB;
   const int Z = gridDim.z, z = bz;
   const int blk0 = (int)((int64_t)nblk_all * z / Z), blk1 = (int)((int64_t)nblk_all * (z + 1) / Z);
-  const uint16_t* kbase = kc + (int64_t)g * max_ctx * HD;
-  const uint16_t* vbase = vc + (int64_t)g * max_ctx * HD;
+  // A block of KB keys lies in one cache page (KB divides kKvPage, blocks start at multiples of KB).
+  static_assert(kKvPage % KF_PF_ATTN_KB == 0, "key blocks within pages");
+  auto block_off = [&](int blk) -> int64_t {
+    const int k0 = blk * KF_PF_ATTN_KB;
+    return (int64_t)kv_page(kp, user, k0 / kKvPage) * kp.page_stride + ((int64_t)g * kKvPage + k0 % kKvPage) * HD;
+  };
 
   // Q^T fragments: lane holds query qi, d = 16 s + 8 half_sel .. +7.
   v4u qf[HD / 16];
@@ -263,22 +266,26 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   // (Thread chunks past the tile, possible only when 256 does not divide the
   // chunk count, are skipped; the test folds away otherwise.)
   constexpr bool kFullK = KB * CH % 256 == 0, kFullV = KB / 2 * CH % 256 == 0;
+  // (nkeys - 1 is in block blk whenever a key of blk is clamped to it, so every
+  // load stays in the block's page.)
   auto gload = [&](int blk) {
+    const int kb0 = blk * KB, last = nkeys - 1 - kb0;  // keys of the block relative to kb0
+    const int64_t boff = block_off(blk);
+    const uint16_t* kbase = kc + boff;
+    const uint16_t* vbase = vc + boff;
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
       const int idx = tid + 256 * r;
       const int key = idx / CH, ch = idx % CH;
-      const int pos = min(blk * KB + key, nkeys - 1);
-      if (kFullK || idx < KB * CH) rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)pos * HD + ch * 8);
+      if (kFullK || idx < KB * CH) rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)min(key, last) * HD + ch * 8);
     }
 #pragma unroll
     for (int r = 0; r < VPER; ++r) {
       const int idx = tid + 256 * r;
-      const int kp = idx % (KB / 2), ch = idx / (KB / 2);
-      const int pos = blk * KB + 2 * kp;
+      const int kp2 = idx % (KB / 2), ch = idx / (KB / 2);
       if (kFullV || idx < KB / 2 * CH) {
-        rv0[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(pos, nkeys - 1) * HD + ch * 8);
-        rv1[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(pos + 1, nkeys - 1) * HD + ch * 8);
+        rv0[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(2 * kp2, last) * HD + ch * 8);
+        rv1[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(2 * kp2 + 1, last) * HD + ch * 8);
       }
     }
   };
@@ -295,15 +302,15 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     for (int r = 0; r < VPER; ++r) {
       const int idx = tid + 256 * r;
       if (kFullV || idx < KB / 2 * CH) {
-        const int kp = idx % (KB / 2), ch = idx / (KB / 2);
+        const int kp2 = idx % (KB / 2), ch = idx / (KB / 2);
         const uint32_t a[4] = {rv0[r].x, rv0[r].y, rv0[r].z, rv0[r].w};
         const uint32_t b[4] = {rv1[r].x, rv1[r].y, rv1[r].z, rv1[r].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           // d = ch*8 + 2e holds the low halves, d + 1 the high halves
-          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * LDV + 2 * kp]) =
+          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * LDV + 2 * kp2]) =
               (a[e] & 0xffffu) | (b[e] << 16);
-          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * LDV + 2 * kp]) =
+          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * LDV + 2 * kp2]) =
               (a[e] >> 16) | (b[e] & 0xffff0000u);
         }
       }
@@ -575,7 +582,7 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   if (e != hipSuccess) return e;
   tr.begin(ROPE);
   hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.part, s_qkv, (int64_t)T * nqkv, ws.q, l.kc, l.vc,
-                     a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, a.max_ctx, l.g_qn, l.g_kn, a.eps);
+                     a.kv, a.user, a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, l.g_qn, l.g_kn, a.eps);
   tr.end(ROPE);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));
@@ -587,11 +594,11 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   float* pml = ws.part + (int64_t)Z * T * a.nq * a.hd;
   tr.begin(ATTN);
   if (a.hd == 128)
-    hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, pacc, pml, T, a.nq,
-                       a.nkv, a.pos0, a.max_ctx, sl2);
+    hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, a.kv, a.user, ws.o, pacc,
+                       pml, T, a.nq, a.nkv, a.pos0, sl2);
   else if (a.hd == 64)
-    hipLaunchKernelGGL(attn_prefill_kernel<64>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, ws.o, pacc, pml, T, a.nq,
-                       a.nkv, a.pos0, a.max_ctx, sl2);
+    hipLaunchKernelGGL(attn_prefill_kernel<64>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, a.kv, a.user, ws.o, pacc,
+                       pml, T, a.nq, a.nkv, a.pos0, sl2);
   else
     return hipErrorInvalidValue;
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -98,12 +98,69 @@ void kf_stage::mark(void* ctx, int cls, int begin) {
 struct kf_kv {
   kf_stage* st;
   int max_users, max_ctx, max_split;
+  // Pages of kKvPage positions, [layer][page][kv_head][kKvPage][hd] fp16 for K and V.
+  // A reserved cache holds ppu pages per user in user order (no table); a paged
+  // cache lends pages from a pool, recorded in a device table with a host mirror.
+  int ppu = 0, n_pages = 0;
+  int* table = nullptr;        // device [max_users][ppu] page ids (paged caches only)
+  std::vector<int> host_table; // mirror of the table (-1: not held)
+  std::vector<int> held;       // pages each user holds
+  std::vector<int> free_pages; // the pool's free pages (paged caches only), next page last
   uint16_t *k = nullptr, *v = nullptr;
   float *rcos = nullptr, *rsin = nullptr;
   float *part_acc = nullptr, *part_ml = nullptr;
-  int64_t user_stride, layer_stride;  // elements
+  int64_t page_stride, layer_stride;  // elements
   std::vector<int> len;
+  KvPages pages() const { return KvPages{table, ppu, page_stride}; }
 };
+
+static int pages_for(int64_t len) { return (int)((len + kKvPage - 1) / kKvPage); }
+
+// Lend each user of `users` the pages it needs to hold `upto[i]` positions, or
+// change nothing and fail when the pool is short.  New table entries are written
+// on the stage's stream before any later work there reads them.
+static kf_status kv_grant(kf_kv* kv, int n, const int* users, const int64_t* upto) {
+  if (!kv->table) return KF_OK;  // reserved cache: every page is held from the start
+  int64_t want = 0;
+  for (int i = 0; i < n; ++i) {
+    int need = pages_for(upto[i]) - kv->held[users[i]];
+    for (int j = 0; j < i; ++j)
+      if (users[j] == users[i]) need = 0;  // counted once (the larger request comes first)
+    if (need > 0) want += need;
+  }
+  if (want > (int64_t)kv->free_pages.size())
+    return fail(KF_ENOMEM, "KV pool: %lld more pages needed, %zu free of %d", (long long)want, kv->free_pages.size(),
+                kv->n_pages);
+  KvTableUpdate up{};
+  for (int i = 0; i < n; ++i) {
+    const int u = users[i];
+    for (int pg = kv->held[u]; pg < pages_for(upto[i]); ++pg) {
+      const int id = kv->free_pages.back();
+      kv->free_pages.pop_back();
+      kv->host_table[(size_t)u * kv->ppu + pg] = id;
+      up.idx[up.n] = u * kv->ppu + pg;
+      up.val[up.n] = id;
+      if (++up.n == kKvTableBatch) {
+        KF_HIP(launch_kv_table_update(kv->table, up, kv->st->stream), "page table update");
+        up.n = 0;
+      }
+    }
+    if (pages_for(upto[i]) > kv->held[u]) kv->held[u] = pages_for(upto[i]);
+  }
+  if (up.n) KF_HIP(launch_kv_table_update(kv->table, up, kv->st->stream), "page table update");
+  return KF_OK;
+}
+
+// Return a user's pages past the first `keep` to the pool (paged caches).
+static void kv_release(kf_kv* kv, int u, int keep) {
+  if (!kv->table) return;
+  for (int pg = kv->held[u] - 1; pg >= keep; --pg) {
+    int& id = kv->host_table[(size_t)u * kv->ppu + pg];
+    kv->free_pages.push_back(id);
+    id = -1;
+  }
+  if (kv->held[u] > keep) kv->held[u] = keep;
+}
 
 // ------------------------------------------------------------------ config checks
 static kf_status check_cfg(const kf_model_config* c, int lo, int hi) {
@@ -159,7 +216,7 @@ static int max_split_for(int max_ctx) {
 }
 
 static int64_t kv_bytes(const kf_model_config& c, int layers, int max_users, int max_ctx) {
-  const int64_t cache = 2LL * layers * max_users * c.n_kv_heads * (int64_t)max_ctx * c.head_dim * 2;
+  const int64_t cache = 2LL * layers * max_users * c.n_kv_heads * (int64_t)pages_for(max_ctx) * kKvPage * c.head_dim * 2;
   const int64_t rope = 2LL * max_ctx * (c.head_dim / 2) * 4;
   const int64_t ms = max_split_for(max_ctx);
   const int64_t part = (int64_t)kMaxBatch * c.n_q_heads * ms * (c.head_dim + 2) * 4;
@@ -418,7 +475,8 @@ kf_status kf_stage_sync(kf_stage* s) {
 }
 
 // ------------------------------------------------------------------ KV cache
-kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** out) {
+// n_pages == 0: a reserved cache (every user's pages in user order); else a pool of n_pages.
+static kf_status kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, int32_t n_pages, kf_kv** out) {
   if (!out) return fail(KF_EINVAL, "out is NULL");
   *out = nullptr;
   if (!s) return fail(KF_EINVAL, "stage is NULL");
@@ -426,26 +484,40 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   if ((int64_t)max_ctx > (int64_t)kAttnMaxSplit * 1024) return fail(KF_ERANGE, "max_ctx above %d", kAttnMaxSplit * 1024);
   const kf_model_config& c = s->cfg;
   const int nl = s->hi - s->lo;
+  const int ppu = pages_for(max_ctx);
+  if ((int64_t)max_users * ppu > (1LL << 30)) return fail(KF_ERANGE, "max_users x max_ctx too large");
+  const bool paged = n_pages > 0;
   kf_kv* kv = new (std::nothrow) kf_kv();
   if (!kv) return fail(KF_ENOMEM, "host allocation");
   kv->st = s;
   kv->max_users = max_users;
   kv->max_ctx = max_ctx;
   kv->max_split = max_split_for(max_ctx);
-  kv->user_stride = (int64_t)c.n_kv_heads * max_ctx * c.head_dim;
-  kv->layer_stride = kv->user_stride * max_users;
+  kv->ppu = ppu;
+  kv->n_pages = paged ? n_pages : max_users * ppu;
+  kv->page_stride = (int64_t)c.n_kv_heads * kKvPage * c.head_dim;
+  kv->layer_stride = kv->page_stride * kv->n_pages;
   kv->len.assign(max_users, 0);
+  kv->held.assign(max_users, paged ? 0 : ppu);
+  if (paged) {
+    kv->host_table.assign((size_t)max_users * ppu, -1);
+    kv->free_pages.reserve(n_pages);
+    for (int i = n_pages - 1; i >= 0; --i) kv->free_pages.push_back(i);  // page 0 lent first
+  }
   const int64_t cache = kv->layer_stride * nl * 2;
   const int64_t half = c.head_dim / 2;
   const int64_t rope = (int64_t)max_ctx * half * 4;
   const int64_t pacc = (int64_t)kMaxBatch * c.n_q_heads * kv->max_split * c.head_dim * 4;
   const int64_t pml = (int64_t)kMaxBatch * c.n_q_heads * kv->max_split * 2 * 4;
-  char* mem[6] = {nullptr};
-  const int64_t sz[6] = {cache, cache, rope, rope, pacc, pml};
-  for (int i = 0; i < 6; ++i) {
+  const int64_t tab = paged ? (int64_t)max_users * ppu * 4 : 0;
+  char* mem[7] = {nullptr};
+  const int64_t sz[7] = {cache, cache, rope, rope, pacc, pml, tab};
+  for (int i = 0; i < 7; ++i) {
+    if (sz[i] == 0) continue;
     if (hipMalloc((void**)&mem[i], sz[i]) != hipSuccess) {
       hipGetLastError();
-      for (int j = 0; j < i; ++j) hipFree(mem[j]);
+      for (int j = 0; j < i; ++j)
+        if (mem[j]) hipFree(mem[j]);
       delete kv;
       return fail(KF_ENOMEM, "device allocation of %lld KV bytes", (long long)sz[i]);
     }
@@ -456,6 +528,7 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   kv->rsin = (float*)mem[3];
   kv->part_acc = (float*)mem[4];
   kv->part_ml = (float*)mem[5];
+  kv->table = (int*)mem[6];
   // RoPE table from float64 angles: pos * theta^(-2i/hd).
   std::vector<float> tc((size_t)max_ctx * half), ts((size_t)max_ctx * half);
   for (int64_t i = 0; i < half; ++i) {
@@ -468,10 +541,12 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   }
   hipError_t e = hipMemset(kv->k, 0, cache);
   if (e == hipSuccess) e = hipMemset(kv->v, 0, cache);
+  if (e == hipSuccess && kv->table) e = hipMemset(kv->table, 0, tab);
   if (e == hipSuccess) e = hipMemcpy(kv->rcos, tc.data(), rope, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(kv->rsin, ts.data(), rope, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
-    for (int j = 0; j < 6; ++j) hipFree(mem[j]);
+    for (int j = 0; j < 7; ++j)
+      if (mem[j]) hipFree(mem[j]);
     delete kv;
     return fail(KF_EDEVICE, "KV init: %s", hipGetErrorString(e));
   }
@@ -480,11 +555,31 @@ kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** 
   return KF_OK;
 }
 
+kf_status kf_kv_create(kf_stage* s, int32_t max_users, int32_t max_ctx, kf_kv** out) {
+  return kv_create(s, max_users, max_ctx, 0, out);
+}
+
+kf_status kf_kv_create_paged(kf_stage* s, int32_t max_users, int32_t max_ctx, int32_t n_pages, kf_kv** out) {
+  if (n_pages < 1) {
+    if (out) *out = nullptr;
+    return fail(KF_EINVAL, "n_pages %d < 1", n_pages);
+  }
+  return kv_create(s, max_users, max_ctx, n_pages, out);
+}
+
+kf_status kf_kv_pages(const kf_kv* kv, int32_t* total, int32_t* free_pages) {
+  if (!kv) return fail(KF_EINVAL, "kv is NULL");
+  if (total) *total = kv->n_pages;
+  if (free_pages) *free_pages = kv->table ? (int32_t)kv->free_pages.size() : 0;
+  return KF_OK;
+}
+
 kf_status kf_kv_destroy(kf_kv* kv) {
   if (!kv) return fail(KF_EINVAL, "kv is NULL");
   hipStreamSynchronize(kv->st->stream);
-  void* mem[6] = {kv->k, kv->v, kv->rcos, kv->rsin, kv->part_acc, kv->part_ml};
-  for (void* m : mem) hipFree(m);
+  void* mem[7] = {kv->k, kv->v, kv->rcos, kv->rsin, kv->part_acc, kv->part_ml, kv->table};
+  for (void* m : mem)
+    if (m) hipFree(m);
   kv->st->live_kv--;
   delete kv;
   return KF_OK;
@@ -509,6 +604,10 @@ kf_status kf_kv_set_len(kf_kv* kv, int32_t user, int32_t len) {
   if (!kv) return fail(KF_EINVAL, "kv is NULL");
   if (user < 0 || user >= kv->max_users) return fail(KF_EINVAL, "user %d outside [0, %d)", user, kv->max_users);
   if (len < 0 || len > kv->max_ctx) return fail(KF_ERANGE, "length %d outside [0, %d]", len, kv->max_ctx);
+  const int64_t upto = len;
+  kf_status st = kv_grant(kv, 1, &user, &upto);
+  if (st != KF_OK) return st;
+  kv_release(kv, user, pages_for(len));
   kv->len[user] = len;
   return KF_OK;
 }
@@ -531,9 +630,12 @@ kf_status kf_kv_write(kf_kv* kv, int32_t layer, int32_t user, int32_t pos0, int3
   if (!k_dev || !v_dev) return fail(KF_EINVAL, "NULL source");
   if (dtype != KF_F32 && dtype != KF_BF16 && dtype != KF_F16) return fail(KF_EINVAL, "dtype");
   const kf_model_config& c = kv->st->cfg;
-  const int64_t off = (layer - kv->st->lo) * kv->layer_stride + user * kv->user_stride + (int64_t)pos0 * c.head_dim;
-  KF_HIP(launch_kv_write(kv->k + off, kv->v + off, k_dev, v_dev, (int)dtype, n, c.n_kv_heads, c.head_dim,
-                         kv->max_ctx, kv->st->stream),
+  const int64_t upto = (int64_t)pos0 + n;
+  st = kv_grant(kv, 1, &user, &upto);
+  if (st != KF_OK) return st;
+  const int64_t off = (layer - kv->st->lo) * kv->layer_stride;
+  KF_HIP(launch_kv_write(kv->k + off, kv->v + off, kv->pages(), user, pos0, k_dev, v_dev, (int)dtype, n,
+                         c.n_kv_heads, c.head_dim, kv->st->stream),
          "kv_write launch");
   return KF_OK;
 }
@@ -546,8 +648,11 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
   if (n == 0) return KF_OK;
   if (!k_dev || !v_dev) return fail(KF_EINVAL, "NULL destination");
   const kf_model_config& c = kv->st->cfg;
-  const int64_t off = (layer - kv->st->lo) * kv->layer_stride + user * kv->user_stride + (int64_t)pos0 * c.head_dim;
-  KF_HIP(launch_kv_read(kv->k + off, kv->v + off, k_dev, v_dev, n, c.n_kv_heads, c.head_dim, kv->max_ctx,
+  if ((int64_t)pos0 + n > (int64_t)kv->held[user] * kKvPage)
+    return fail(KF_ERANGE, "positions up to %d of user %d are not in the cache (it holds %d pages)", pos0 + n, user,
+                kv->held[user]);
+  const int64_t off = (layer - kv->st->lo) * kv->layer_stride;
+  KF_HIP(launch_kv_read(kv->k + off, kv->v + off, kv->pages(), user, pos0, k_dev, v_dev, n, c.n_kv_heads, c.head_dim,
                         kv->st->stream),
          "kv_read launch");
   return KF_OK;
@@ -567,6 +672,7 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
 #ifndef KF_ATTN_KEYS_PER_WG
 #define KF_ATTN_KEYS_PER_WG 512
 #endif
+static_assert(KF_ATTN_ALIGN % kKvPage == 0, "splits start on page boundaries");
 static void attn_split(int nkv, int batch, int64_t total_len, int max_len, int max_split, int* split, int* n_split) {
   auto up = [](int64_t v) { return (int)((v + KF_ATTN_ALIGN - 1) / KF_ATTN_ALIGN * KF_ATTN_ALIGN); };
   const int64_t target = batch > 1 ? 2 * KF_ATTN_TARGET_WGS : KF_ATTN_TARGET_WGS;
@@ -607,9 +713,15 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   const int H = c.hidden, hd = c.head_dim;
   hipStream_t st = s->stream;
 
+  int64_t upto[kMaxBatch];
+  for (int b = 0; b < batch; ++b) upto[b] = (int64_t)positions[b] + 1;
+  kf_status gst = kv_grant(kv, batch, users, upto);
+  if (gst != KF_OK) return gst;
+
   const Tracer tr = s->tracer();
   int split, n_split;
   attn_split(c.n_kv_heads, batch, total_len, max_len, kv->max_split, &split, &n_split);
+  if (split % kKvPage) return fail(KF_EINVAL, "split of %d keys is not a whole number of pages", split);
 
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];
@@ -627,8 +739,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     g.q = s->q;
     g.kc = kv->k + loff;
     g.vc = kv->v + loff;
-    g.user_stride = kv->user_stride;
-    g.max_ctx = kv->max_ctx;
+    g.kv = kv->pages();
     g.nq = c.n_q_heads;
     g.nkv = c.n_kv_heads;
     g.hd = hd;
@@ -664,8 +775,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       qn.gk = L.g_kn;
       qn.rope_cos = kv->rcos;
       qn.rope_sin = kv->rsin;
-      qn.user_stride = kv->user_stride;
-      qn.max_ctx = kv->max_ctx;
+      qn.kv = kv->pages();
       qn.nq = c.n_q_heads;
       qn.nkv = c.n_kv_heads;
       qn.hd = hd;
@@ -686,8 +796,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     a.vc = kv->v + loff;
     a.part_acc = kv->part_acc;
     a.part_ml = kv->part_ml;
-    a.user_stride = kv->user_stride;
-    a.max_ctx = kv->max_ctx;
+    a.kv = kv->pages();
     a.nq = c.n_q_heads;
     a.nkv = c.n_kv_heads;
     a.hd = hd;
@@ -841,14 +950,17 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
   pa.eps = c.rms_eps;
   pa.T = n;
   pa.pos0 = pos0;
-  pa.max_ctx = kv->max_ctx;
-  pa.user_stride = kv->user_stride;
+  pa.user = user;
+  pa.kv = kv->pages();
   pa.rope_cos = kv->rcos;
   pa.rope_sin = kv->rsin;
   pa.stream = s->stream;
   hipError_t e = prefill_reserve(s->pf, pa);
   if (e == hipErrorOutOfMemory) return fail(KF_ENOMEM, "device allocation of the prefill workspace");
   KF_HIP(e, "prefill workspace");
+  const int64_t upto = (int64_t)pos0 + n;
+  const kf_status gst = kv_grant(kv, 1, &user, &upto);
+  if (gst != KF_OK) return gst;
   const Tracer tr = s->tracer();
   tr.begin(KF_K_PREP);
   e = launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->pf.x, n, c.hidden, s->err_flag,
@@ -858,7 +970,7 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
   s->pf.pending = 0;  // x now holds the whole input; no split-K slices are pending
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];
-    const int64_t loff = (l - s->lo) * kv->layer_stride + user * kv->user_stride;
+    const int64_t loff = (l - s->lo) * kv->layer_stride;
     PrefillLayer pl{};
     pl.wqkv = L.wqkv;
     pl.wo = L.wo;

@@ -30,7 +30,8 @@ HEAD_KINDS = {"embed": 9, "final_norm": 10, "lm_head": 11}
 EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init", "kf_stage_destroy",
            "kf_stage_set_stream", "kf_stage_sync", "kf_kv_create", "kf_kv_destroy", "kf_kv_len", "kf_kv_set_len",
            "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax",
-           "kf_stage_profile", "kf_stage_profile_read", "kf_stage_describe", "kf_kv_describe")
+           "kf_stage_profile", "kf_stage_profile_read", "kf_stage_describe", "kf_kv_describe",
+           "kf_kv_create_paged", "kf_kv_pages")
 
 # kf_kernel_class
 KERNEL_CLASSES = ("prep", "qkv", "attn", "oproj", "gateup", "down", "lmhead", "argmax", "pf_norm", "pf_qkv", "pf_rope",
@@ -100,6 +101,8 @@ def load_library(path: str = LIB_PATH):
         "kf_stage_profile_read": (I32, [P, I32, I64P, ctypes.POINTER(ctypes.c_double)]),
         "kf_stage_describe": (I32, [P, ctypes.POINTER(ModelConfig), I32P, I32P, I32P, ctypes.POINTER(VP), I32P]),
         "kf_kv_describe": (I32, [P, ctypes.POINTER(P), I32P, I32P]),
+        "kf_kv_create_paged": (I32, [P, I32, I32, I32, ctypes.POINTER(P)]),
+        "kf_kv_pages": (I32, [P, I32P, I32P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -235,8 +238,9 @@ class Stage:
                 out[name] = (n.value, t.value)
         return out
 
-    def kv(self, max_users: int, max_ctx: int) -> "KV":
-        return KV(self, max_users, max_ctx)
+    def kv(self, max_users: int, max_ctx: int, pages: int | None = None) -> "KV":
+        """A KV cache; with ``pages`` a paged cache of that many 64-position pages shared by the users."""
+        return KV(self, max_users, max_ctx, pages)
 
     # -- compute
     def decode(self, kv: "KV", users, positions, tokens=None, hidden=None, out=None):
@@ -310,11 +314,15 @@ class Stage:
 class KV:
     """A KV reservation of ``max_users`` users x ``max_ctx`` positions for every layer of a stage."""
 
-    def __init__(self, stage: Stage, max_users: int, max_ctx: int):
+    def __init__(self, stage: Stage, max_users: int, max_ctx: int, pages: int | None = None):
         self.stage, self.max_users, self.max_ctx = stage, max_users, max_ctx
         self._lib = stage._lib
         h = ctypes.c_void_p()
-        _check(self._lib.kf_kv_create(stage.handle, max_users, max_ctx, ctypes.byref(h)), "kf_kv_create")
+        if pages is None:
+            _check(self._lib.kf_kv_create(stage.handle, max_users, max_ctx, ctypes.byref(h)), "kf_kv_create")
+        else:
+            _check(self._lib.kf_kv_create_paged(stage.handle, max_users, max_ctx, pages, ctypes.byref(h)),
+                   "kf_kv_create_paged")
         self.handle = h
 
     def close(self):
@@ -335,6 +343,12 @@ class KV:
 
     def set_len(self, user: int, n: int):
         _check(self._lib.kf_kv_set_len(self.handle, user, n), "kf_kv_set_len")
+
+    def pages(self):
+        """(pages in the cache, free pages); a reserved cache reports no free pages."""
+        t, f = ctypes.c_int32(), ctypes.c_int32()
+        _check(self._lib.kf_kv_pages(self.handle, ctypes.byref(t), ctypes.byref(f)), "kf_kv_pages")
+        return t.value, f.value
 
     def describe(self) -> dict:
         owner, mu, mc = ctypes.c_void_p(), ctypes.c_int32(), ctypes.c_int32()

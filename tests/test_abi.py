@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.kf_abi_version() == 2
+    assert lib.kf_abi_version() == 3
 
 
 def test_stage_bytes_matches_shape_arithmetic():
@@ -200,6 +200,15 @@ def test_ring_rejects_before_touching_the_device(lib):
     assert r.kf_ring_destroy(None) == 1
     assert lib.kf_stage_describe(None, None, None, None, None, None, None) == 1
     assert lib.kf_kv_describe(None, None, None, None) == 1
+
+
+def test_paged_kv_rejects_before_touching_the_device(lib):
+    out = ctypes.c_void_p(123)
+    assert lib.kf_kv_create_paged(None, 1, 64, 4, ctypes.byref(out)) == 1
+    assert out.value is None
+    assert lib.kf_kv_create_paged(ctypes.c_void_p(8), 1, 64, 0, ctypes.byref(out)) == 1  # no pages
+    assert b"n_pages" in lib.kf_last_error() and out.value is None
+    assert lib.kf_kv_pages(None, None, None) == 1
 
 
 def test_kernel_classes_match_the_header():
