@@ -1,0 +1,96 @@
+"""Edge cases at the largest sizes the library accepts, against the float64 oracle.
+
+A cache of max_ctx = 1,048,576 positions (the maximum) decoded at its last
+slot: the attention then runs the largest split (1024 keys per workgroup) and
+the most splits per row (1024), so the output projection's merge takes its
+longest loops.  Over a million random keys the softmax is nearly flat and the
+attention output nearly zero, which would hide a lost split; so two "needle"
+keys, at positions 3 and 700,001 (different splits and pages), are aligned
+with the token's own rotated queries (computed on the host from the oracle's
+definitions) and dominate every head.  The output is then the mean of the
+needles' values, which moves the hidden row by tens of percent: a wrong page,
+split or merge weight exceeds the tolerance.  Both the reserved and the paged
+cache are checked; one position more is refused.  Every call goes through the
+C ABI.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleStage
+from oracle.stage_oracle import bf16_to_f64, rms_norm, rope
+from tests.helpers import SeededModel, assert_hidden_close
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.SHAPE_TINY
+MAX_CTX = 1 << 20
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+@pytest.fixture(scope="module")
+def st():
+    from paper_2609_34045_amd import stage
+    return stage
+
+
+def to_bf16(a: np.ndarray) -> np.ndarray:
+    """float64 -> bf16 bit patterns, round to nearest even (finite values)."""
+    b = np.asarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("paged", [False, True], ids=["reserved", "paged"])
+def test_decode_at_the_last_slot_of_the_largest_cache(torch, st, paged):
+    cfg_id = 41
+    model = SeededModel(TINY, cfg_id)
+    g = st.Stage(TINY, 0, 1, model.layer, None)
+    n = MAX_CTX - 1
+    kv = g.kv(1, MAX_CTX, pages=MAX_CTX // 64 if paged else None)
+    kb, vb = synth.injected_kv(TINY, cfg_id, 0, 0, n)
+    x = synth.hidden_states(cfg_id, synth.STREAM_DECODE_HIDDEN, 0, 1, TINY.hidden)
+    # needles: key = 400 x the unit mean direction of each KV group's rotated queries at position n
+    w = {k: bf16_to_f64(v) for k, v in model.layer(0).items()}
+    nq, nkv, hd = TINY.n_q_heads, TINY.n_kv_heads, TINY.head_dim
+    q = rope((rms_norm(x, w["attn_norm"], TINY.rms_eps) @ w["wq"].T).reshape(1, nq, hd), np.array([n]),
+             TINY.rope_theta)[0]
+    grp = nq // nkv
+    rng = np.random.default_rng(7)
+    for j in (3, 700_001):
+        for kh in range(nkv):
+            qg = q[kh * grp:(kh + 1) * grp]
+            u = (qg / np.linalg.norm(qg, axis=1, keepdims=True)).sum(0)
+            kb[j, kh] = to_bf16(400.0 * u / np.linalg.norm(u))
+            vb[j, kh] = to_bf16(2.0 * rng.standard_normal(hd))
+    # what the needles alone add to the row: W_o times the mean of their values, per head's KV group
+    o = np.concatenate([(bf16_to_f64(vb[3, h // grp]) + bf16_to_f64(vb[700_001, h // grp])) / 2 for h in range(nq)])
+    share = np.max(np.abs(o @ w["wo"].T)) / np.max(np.abs(x))
+    assert share > 0.2  # large enough that a lost or misweighted needle breaks the 1e-2 bound
+    kv.write(0, 0, 0, torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+    kv.set_len(0, n)
+    o = OracleStage(TINY, 0, 1, model.layer, None, max_users=1, max_ctx=MAX_CTX)
+    o.kv.inject(0, 0, 0, kb, vb)
+    o.kv.set_len(0, n)
+    del kb, vb
+    y = g.decode(kv, [0], [n], hidden=torch.from_numpy(x).cuda())
+    err = assert_hidden_close(y.float().cpu().numpy().astype(np.float64), o.decode([0], [n], hidden=x),
+                              what="decode over 1,048,576 keys")
+    print("max-context row rel err", err, "needle share of the row", share)
+    assert kv.len(0) == MAX_CTX
+    with pytest.raises(st.KFError) as e:  # the cache is full
+        g.decode(kv, [0], [MAX_CTX], hidden=torch.from_numpy(x).cuda())
+    assert e.value.status == st.KF_ERANGE
+    if paged:
+        assert kv.pages() == (MAX_CTX // 64, 0)
+    kv.close()
+    with pytest.raises(st.KFError) as e:
+        g.kv(1, MAX_CTX + 1)
+    assert e.value.status == st.KF_ERANGE
+    g.close()

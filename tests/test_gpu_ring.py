@@ -45,7 +45,7 @@ def token_ok(t_gpu: int, logits: np.ndarray):
     return gap <= NEAR_TIE * float(np.max(np.abs(logits))), True
 
 
-def build(torch, kf, shape, model, bounds, n_users, ctx, shared_stream=False, io=None, max_groups=4):
+def build(torch, kf, shape, model, bounds, n_users, ctx, shared_stream=False, io=None, max_groups=4, pages=None):
     st, rg = kf
     one = torch.cuda.Stream()
     stages, kvs = [], []
@@ -53,7 +53,7 @@ def build(torch, kf, shape, model, bounds, n_users, ctx, shared_stream=False, io
         s = one if shared_stream else torch.cuda.Stream()
         g = st.Stage(shape, lo, hi, model.layer, model.head() if i == 0 else None, stream=s)
         stages.append(g)
-        kvs.append(g.kv(n_users, ctx))
+        kvs.append(g.kv(n_users, ctx, pages=pages))
     return rg.Ring(stages, kvs, max_groups=max_groups, max_prefill=64, io=io), stages, kvs
 
 
@@ -69,14 +69,18 @@ def run_case(torch, kf, shape, cfg_id, bounds, prompt_lens, groups, steps, **kw)
     model = SeededModel(shape, cfg_id)
     prompts = [synth.tokens(cfg_id, 100 + u, n, shape.vocab) for u, n in enumerate(prompt_lens)]
     ctx = max(prompt_lens) + steps + 4
+    if kw.pop("paged", False):  # a pool with exactly the pages the users will hold
+        kw["pages"] = sum((n + steps + 63) // 64 for n in prompt_lens)
     ring, stages, kvs = build(torch, kf, shape, model, bounds, len(prompts), ctx, **kw)
     oracle = OracleStage(shape, 0, shape.n_layers, model.layer, model.head(), max_users=len(prompts), max_ctx=ctx)
     near = 0
     firsts = []
     for u, p in enumerate(prompts):
-        tok = torch.from_numpy(p.astype(np.int32)).cuda()
-        torch.cuda.synchronize()  # the ring's streams read it
-        firsts.append(ring.prefill(u, tok))
+        for c0 in range(0, len(p), 64):  # chunks of at most max_prefill tokens
+            tok = torch.from_numpy(p[c0:c0 + 64].astype(np.int32)).cuda()
+            torch.cuda.synchronize()  # the ring's streams read it
+            nxt = ring.prefill(u, tok)
+        firsts.append(nxt)
     ring.sync()
     prev = {}
     for u, p in enumerate(prompts):
@@ -115,7 +119,8 @@ def test_tiny_three_members_three_groups(torch, kf):
     run_case(torch, kf, TINY4, 21, [(0, 1), (1, 3), (3, 4)], (5, 17, 9, 30, 1, 12), [[0, 1], [2], [3, 4, 5]], 6)
 
 
-@pytest.mark.parametrize("variant", ["one_member", "shared_stream", "bf16_handoff", "fewer_groups_than_members"])
+@pytest.mark.parametrize("variant", ["one_member", "shared_stream", "bf16_handoff", "fewer_groups_than_members",
+                                     "paged_caches"])
 def test_tiny_ring_variants(torch, kf, variant):
     if variant == "one_member":
         run_case(torch, kf, TINY4, 22, [(0, 4)], (6, 3), [[0], [1]], 5)
@@ -123,8 +128,10 @@ def test_tiny_ring_variants(torch, kf, variant):
         run_case(torch, kf, TINY4, 23, [(0, 2), (2, 4)], (4, 8, 2), [[0, 2], [1]], 5, shared_stream=True)
     elif variant == "bf16_handoff":
         run_case(torch, kf, TINY4, 24, [(0, 1), (1, 4)], (7, 11), [[1, 0]], 5, io=torch.bfloat16)
-    else:
+    elif variant == "fewer_groups_than_members":
         run_case(torch, kf, TINY4, 25, [(0, 1), (1, 2), (2, 3), (3, 4)], (3, 5, 2, 4), [[0, 1, 2, 3]], 4)
+    else:  # every member's cache a pool just large enough; prompts cross pages
+        run_case(torch, kf, TINY4, 29, [(0, 2), (2, 3), (3, 4)], (70, 5, 130), [[0], [1, 2]], 8, paged=True)
 
 
 def test_qwen3_tiny_ring(torch, kf):
