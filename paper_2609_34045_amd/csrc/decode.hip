@@ -17,6 +17,8 @@
 // Attention is split-KV over an fp16 cache, [user][kv_head][pos][hd]; each
 // workgroup serves all query heads of one KV head, and a second small kernel
 // merges the splits of each (row, KV head) (online-softmax rescaling).
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace kf {
@@ -442,7 +444,7 @@ void gemv_kernel(const GemvParams p) {
 #define KF_ATTN_J 4
 #endif
 
-template <int HD, int G>
+template <int HD, int G, int DEPTH>
 __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   constexpr int LPK = HD / 8;      // lanes per key (one 16-byte slice each)
   constexpr int KPW = 64 / LPK;    // key groups per wave
@@ -486,23 +488,30 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     for (int i = 0; i < 8; ++i) acc[h][i] = 0.f;
   }
 
-  // The first chunk's K and V are requested before the query, which the
-  // previous kernel has just written.
+  // The first chunks' K and V are requested before the query, which the
+  // previous kernel has just written.  DEPTH chunks per wave are in flight:
+  // slot s holds the chunk processed at steps s, s + DEPTH, ... and is reloaded
+  // with the chunk DEPTH steps ahead once its values are in registers.
+  static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
   int c0 = wave * CH;
-  v4u kw[J], vw[J];
-  bool ok[J];
-  auto load_chunk = [&](int c) {  // keys past nk re-read the chunk's first key (c < nk)
+  v4u kw[DEPTH][J], vw[DEPTH][J];
+  bool ok[DEPTH][J];
+  auto load_chunk = [&](int c, auto slot) {  // keys past nk re-read the chunk's first key (c < nk)
+    constexpr int sl = decltype(slot)::value;
     const int64_t base = chunk_base(c);
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int r = j * KPW + kgrp;
-      ok[j] = c + r < nk;
-      const int64_t at = base + (int64_t)(ok[j] ? r : 0) * HD;
-      kw[j] = *reinterpret_cast<const v4u*>(p.kc + at);
-      vw[j] = *reinterpret_cast<const v4u*>(p.vc + at);
+      ok[sl][j] = c + r < nk;
+      const int64_t at = base + (int64_t)(ok[sl][j] ? r : 0) * HD;
+      kw[sl][j] = *reinterpret_cast<const v4u*>(p.kc + at);
+      vw[sl][j] = *reinterpret_cast<const v4u*>(p.vc + at);
     }
   };
-  if (c0 < nk) load_chunk(c0);
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, DEPTH - 1>;
+  if (c0 < nk) load_chunk(c0, S0{});
+  if (DEPTH > 1 && c0 + 4 * CH < nk) load_chunk(c0 + 4 * CH, S1{});
 
   // The scaled query as fp16 pairs: a score is then 4 packed fp16 dot products
   // (fp32 accumulation) against the key's fp16 values as stored in the cache.
@@ -517,13 +526,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     qh[h][3] = __builtin_convertvector(f2{hi.z, hi.w}, h2);
   }
 
-  for (; c0 < nk; c0 += 4 * CH) {
+  // One step: the chunk at c0, held in slot `slot`.
+  auto step = [&](auto slot) {
+    constexpr int sl = decltype(slot)::value;
     float sc[J][G];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       // Pairs are taken from the whole 8-half vector by shuffles (a bit cast of a
       // single dword element of the loaded vector is lowered to element 0).
-      const h8 k8 = __builtin_bit_cast(h8, kw[j]);
+      const h8 k8 = __builtin_bit_cast(h8, kw[sl][j]);
       const h2 k0 = __builtin_shufflevector(k8, k8, 0, 1), k1 = __builtin_shufflevector(k8, k8, 2, 3),
                k2 = __builtin_shufflevector(k8, k8, 4, 5), k3 = __builtin_shufflevector(k8, k8, 6, 7);
 #pragma unroll
@@ -541,7 +552,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     h2 vp[J / 2][8];
 #pragma unroll
     for (int m = 0; m < J / 2; ++m) {
-      const h8 a = __builtin_bit_cast(h8, vw[2 * m]), c = __builtin_bit_cast(h8, vw[2 * m + 1]);
+      const h8 a = __builtin_bit_cast(h8, vw[sl][2 * m]), c = __builtin_bit_cast(h8, vw[sl][2 * m + 1]);
       vp[m][0] = __builtin_shufflevector(a, c, 0, 8);
       vp[m][1] = __builtin_shufflevector(a, c, 1, 9);
       vp[m][2] = __builtin_shufflevector(a, c, 2, 10);
@@ -553,8 +564,9 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     }
     bool okc[J];
 #pragma unroll
-    for (int j = 0; j < J; ++j) okc[j] = ok[j];
-    if (c0 + 4 * CH < nk) load_chunk(c0 + 4 * CH);  // next chunk in flight during this one's math
+    for (int j = 0; j < J; ++j) okc[j] = ok[sl][j];
+    // the chunk DEPTH steps ahead is in flight during this one's math
+    if (c0 + DEPTH * 4 * CH < nk) load_chunk(c0 + DEPTH * 4 * CH, slot);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       float mc = -INFINITY;
@@ -582,6 +594,14 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc[h][i] = __builtin_amdgcn_fdot2(vp[m][i], pp, acc[h][i], false);
       }
+    }
+  };
+  while (c0 < nk) {
+    step(S0{});
+    c0 += 4 * CH;
+    if (DEPTH > 1 && c0 < nk) {
+      step(S1{});
+      c0 += 4 * CH;
     }
   }
 
@@ -981,7 +1001,12 @@ hipError_t launch_qk_norm_rope(const QkNormParams& p, int batch, hipStream_t s) 
 
 template <int HD, int G>
 static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
-  hipLaunchKernelGGL((attn_decode_kernel<HD, G>), dim3(p.n_split, p.nkv, batch), dim3(256), 0, s, p);
+  const dim3 grid(p.n_split, p.nkv, batch);
+  // Two chunks in flight per wave pay off only where few workgroups stream long
+  // splits (batch 1, 512 keys or more: 8B-shaped 32K context 33.9 -> 29.8 us);
+  // elsewhere the 36 extra VGPRs cost more in occupancy than they gain.
+  if (batch == 1 && p.split >= 512) hipLaunchKernelGGL((attn_decode_kernel<HD, G, 2>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((attn_decode_kernel<HD, G, 1>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
