@@ -63,7 +63,8 @@ kf_status kf_ring_destroy(kf_ring* ring);
  *   len .. len + n_tokens - 1, where len is the user's length (equal in every
  *   member, else KF_EINVAL; len + n_tokens <= max_ctx, else KF_ERANGE).
  *   next_token_dev int32 [1]: the greedy token after the chunk.
- * The user's length advances by n_tokens in every member.
+ * The user's length advances by n_tokens in every member.  A member with a paged
+ * cache must have free pages for the chunk (KF_ENOMEM otherwise, nothing enqueued).
  */
 kf_status kf_ring_prefill(kf_ring* ring, int32_t user, int32_t n_tokens, const int32_t* tokens_dev,
                           int32_t* next_token_dev);
@@ -79,7 +80,9 @@ kf_status kf_ring_prefill(kf_ring* ring, int32_t user, int32_t n_tokens, const i
  *     ready when the call is made.
  *   tokens_out_dev int32 [steps, U]: row t receives the tokens sampled at step t, which
  *     are the inputs of step t + 1.
- * Every user's length advances by `steps` in every member.  Work is enqueued in the
+ * Every user's length advances by `steps` in every member.  A member with a paged
+ * cache must have free pages for every user's `steps` more positions, counted from
+ * the user's length (KF_ENOMEM otherwise, nothing enqueued).  Work is enqueued in the
  * order in which each member meets the groups: step by step, group after group, so
  * member i takes group g's token while member i - 1 takes group g + 1's.  Everything
  * the call enqueues is ordered before the last work it puts on stages[0]'s stream.

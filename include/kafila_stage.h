@@ -176,7 +176,8 @@ kf_status kf_kv_create(kf_stage* stage, int32_t max_users, int32_t max_ctx, kf_k
 kf_status kf_kv_create_paged(kf_stage* stage, int32_t max_users, int32_t max_ctx, int32_t n_pages, kf_kv** out);
 kf_status kf_kv_destroy(kf_kv* kv);
 
-/* Pages of the cache and, for a paged cache, how many are free (0 for a reserved cache).  Host-only. */
+/* Pages of the cache and, for a paged cache, how many are free (-1 for a reserved cache, whose users
+ * hold all their pages from the start).  Host-only. */
 kf_status kf_kv_pages(const kf_kv* kv, int32_t* total, int32_t* free_pages);
 
 /* The stage a cache was created on, and its capacity.  Any output pointer may be NULL.  Host-only. */

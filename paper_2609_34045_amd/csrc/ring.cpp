@@ -59,6 +59,23 @@ struct kf_ring {
     buf = nullptr;
   }
 
+  // Every paged member must have free pages for `grow` more positions of each user
+  // (counted from the user's length), so that no member runs short mid-call.
+  kf_status pool_check(int n, const std::vector<int>& len, int grow) const {
+    for (int i = 0; i < m; ++i) {
+      int32_t total = 0, free_pages = 0;
+      KF_RING_TRY(kf_kv_pages(kv[i], &total, &free_pages));
+      if (free_pages < 0) continue;  // a reserved cache
+      int64_t need = 0;
+      for (int j = 0; j < n; ++j)
+        need += ((int64_t)len[j] + grow + KF_KV_PAGE - 1) / KF_KV_PAGE - ((int64_t)len[j] + KF_KV_PAGE - 1) / KF_KV_PAGE;
+      if (need > free_pages)
+        return fail(KF_ENOMEM, "member %d's KV pool has %d free pages, the call may need %lld", i, (int)free_pages,
+                    (long long)need);
+    }
+    return KF_OK;
+  }
+
   // Every user of the list must hold the same length in every member; returns it per user.
   kf_status lengths(const int32_t* users, int n, std::vector<int>& len) const {
     len.assign(n, 0);
@@ -197,6 +214,7 @@ kf_status kf_ring_prefill(kf_ring* r, int32_t user, int32_t n_tokens, const int3
   KF_RING_TRY(r->lengths(&user, 1, len));
   if ((int64_t)len[0] + n_tokens > r->max_ctx)
     return fail(KF_ERANGE, "user %d: %d + %d positions exceed max_ctx %d", user, len[0], n_tokens, r->max_ctx);
+  KF_RING_TRY(r->pool_check(1, len, n_tokens));
 
   for (int i = 0; i < r->m; ++i) {
     if (i > 0) KF_RING_HIP(hipStreamWaitEvent(r->stream[i], r->ev_pf[i - 1], 0), "hand-off wait");
@@ -229,6 +247,7 @@ kf_status kf_ring_generate(kf_ring* r, int32_t n_groups, const int32_t* group_si
   for (int j = 0; j < U; ++j)
     if ((int64_t)len[j] + steps > r->max_ctx)
       return fail(KF_ERANGE, "user %d: %d + %d positions exceed max_ctx %d", users[j], len[j], steps, r->max_ctx);
+  KF_RING_TRY(r->pool_check(U, len, steps));
 
   const int m = r->m;
   int32_t pos[KF_MAX_BATCH];

@@ -116,16 +116,14 @@ struct kf_kv {
 
 static int pages_for(int64_t len) { return (int)((len + kKvPage - 1) / kKvPage); }
 
-// Lend each user of `users` the pages it needs to hold `upto[i]` positions, or
-// change nothing and fail when the pool is short.  New table entries are written
-// on the stage's stream before any later work there reads them.
+// Lend each of the (distinct) `users` the pages it needs to hold `upto[i]`
+// positions, or change nothing and fail when the pool is short.  New table
+// entries are written on the stage's stream before any later work there reads them.
 static kf_status kv_grant(kf_kv* kv, int n, const int* users, const int64_t* upto) {
   if (!kv->table) return KF_OK;  // reserved cache: every page is held from the start
   int64_t want = 0;
   for (int i = 0; i < n; ++i) {
-    int need = pages_for(upto[i]) - kv->held[users[i]];
-    for (int j = 0; j < i; ++j)
-      if (users[j] == users[i]) need = 0;  // counted once (the larger request comes first)
+    const int need = pages_for(upto[i]) - kv->held[users[i]];
     if (need > 0) want += need;
   }
   if (want > (int64_t)kv->free_pages.size())
@@ -570,7 +568,7 @@ kf_status kf_kv_create_paged(kf_stage* s, int32_t max_users, int32_t max_ctx, in
 kf_status kf_kv_pages(const kf_kv* kv, int32_t* total, int32_t* free_pages) {
   if (!kv) return fail(KF_EINVAL, "kv is NULL");
   if (total) *total = kv->n_pages;
-  if (free_pages) *free_pages = kv->table ? (int32_t)kv->free_pages.size() : 0;
+  if (free_pages) *free_pages = kv->table ? (int32_t)kv->free_pages.size() : -1;
   return KF_OK;
 }
 
@@ -713,15 +711,15 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   const int H = c.hidden, hd = c.head_dim;
   hipStream_t st = s->stream;
 
-  int64_t upto[kMaxBatch];
-  for (int b = 0; b < batch; ++b) upto[b] = (int64_t)positions[b] + 1;
-  kf_status gst = kv_grant(kv, batch, users, upto);
-  if (gst != KF_OK) return gst;
-
-  const Tracer tr = s->tracer();
   int split, n_split;
   attn_split(c.n_kv_heads, batch, total_len, max_len, kv->max_split, &split, &n_split);
   if (split % kKvPage) return fail(KF_EINVAL, "split of %d keys is not a whole number of pages", split);
+  int64_t upto[kMaxBatch];
+  for (int b = 0; b < batch; ++b) upto[b] = (int64_t)positions[b] + 1;
+  const kf_status gst = kv_grant(kv, batch, users, upto);
+  if (gst != KF_OK) return gst;
+
+  const Tracer tr = s->tracer();
 
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];

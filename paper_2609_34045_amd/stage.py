@@ -345,7 +345,7 @@ class KV:
         _check(self._lib.kf_kv_set_len(self.handle, user, n), "kf_kv_set_len")
 
     def pages(self):
-        """(pages in the cache, free pages); a reserved cache reports no free pages."""
+        """(pages in the cache, free pages); a reserved cache reports -1 free pages."""
         t, f = ctypes.c_int32(), ctypes.c_int32()
         _check(self._lib.kf_kv_pages(self.handle, ctypes.byref(t), ctypes.byref(f)), "kf_kv_pages")
         return t.value, f.value

@@ -172,3 +172,31 @@ def test_ring_checks_run_before_anything_is_enqueued(torch, kf):
     with pytest.raises(st.KFError):
         rg.Ring(stages, kvs[::-1])  # a cache of another stage
     close(ring, stages, kvs)
+
+
+def test_ring_refuses_work_a_member_pool_cannot_hold(torch, kf):
+    """A paged member whose pool is short refuses the whole call before any member enqueues."""
+    st, rg = kf
+    model = SeededModel(TINY4, 30)
+    s0 = st.Stage(TINY4, 0, 2, model.layer, model.head(), stream=torch.cuda.Stream())
+    s1 = st.Stage(TINY4, 2, 4, model.layer, None, stream=torch.cuda.Stream())
+    k0, k1 = s0.kv(2, 256), s1.kv(2, 256, pages=2)  # member 1: room for one page per user
+    ring = rg.Ring([s0, s1], [k0, k1], max_groups=2, max_prefill=64)
+    toks = [torch.from_numpy(synth.tokens(30, u, 70, TINY4.vocab).astype(np.int32)).cuda() for u in range(2)]
+    torch.cuda.synchronize()
+    first = [ring.prefill(u, toks[u][:60]) for u in range(2)]
+    ring.sync()
+    assert k1.pages() == (2, 0) and k0.pages()[1] == -1
+    tin = torch.cat(first)
+    torch.cuda.synchronize()
+    with pytest.raises(st.KFError) as e:  # positions 60..64: each user needs a second page in member 1
+        ring.generate([[0], [1]], tin, 5)
+    assert e.value.status == st.KF_ENOMEM and "member 1" in e.value.message
+    with pytest.raises(st.KFError) as e:
+        ring.prefill(0, toks[0][60:70])
+    assert e.value.status == st.KF_ENOMEM
+    assert [k.len(u) for k in (k0, k1) for u in range(2)] == [60, 60, 60, 60]
+    out = ring.generate([[0], [1]], tin, 4)  # positions 60..63 stay on the pages held
+    ring.sync()
+    assert out.shape == (4, 2) and [k.len(u) for k in (k0, k1) for u in range(2)] == [64] * 4
+    close(ring, [s0, s1], [k0, k1])
