@@ -275,7 +275,8 @@ typedef enum {
   KF_K_PF_GATEUP = 13, /* prefill: gate/up GEMM + SwiGLU */
   KF_K_PF_DOWN = 14,   /* prefill: down GEMM + residual */
   KF_K_PF_STORE = 15,  /* prefill: hidden output store */
-  KF_K_QKNORM = 16,    /* decode: per-head q/k RMSNorm + RoPE + K append (qk_norm blocks) */
+  KF_K_QKNORM = 16,    /* kept for numbering: the decode per-head q/k RMSNorm + RoPE of qk_norm blocks
+                          now runs inside the attention launch (KF_K_ATTN); nothing records here */
   KF_K_COUNT = 17
 } kf_kernel_class;
 #define KF_K_ALL 0x1ffff

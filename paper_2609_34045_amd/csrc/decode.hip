@@ -66,6 +66,9 @@ __device__ __forceinline__ void f16x8(const v4u w, float (&f)[8]) {
 
 // fp32 to fp16 bits, round to nearest even.
 __device__ __forceinline__ uint16_t f32_to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+__device__ __forceinline__ uint32_t f16_pair(float lo, float hi) {
+  return (uint32_t)f32_to_f16(lo) | ((uint32_t)f32_to_f16(hi) << 16);
+}
 
 // Round to nearest even; NaN stays NaN.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
@@ -116,6 +119,7 @@ __device__ __forceinline__ float dpp(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
 }
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+constexpr int kDppRor8 = 0x128;  // row_ror:8, i.e. lane xor 8 within each row of 16
 
 template <int N>
 __device__ __forceinline__ float group_sum(float v) {
@@ -513,22 +517,95 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   if (c0 < nk) load_chunk(c0, S0{});
   if (DEPTH > 1 && c0 + 4 * CH < nk) load_chunk(c0 + 4 * CH, S1{});
 
+  // Blocks with q/k norms: the workgroup whose split holds row b's new key
+  // requests that key's raw projection now, so that its latency overlaps the
+  // query's rather than following it.
+  const bool qkn = p.kraw != nullptr;
+  const int npos = len - 1;  // row b's new position
+  const bool own_new = qkn && nk > 0 && npos >= s0 && npos < s0 + nk;
+  v4f kr_lo = {0.f, 0.f, 0.f, 0.f}, kr_hi = kr_lo;
+  v4u kgain = {0u, 0u, 0u, 0u};
+  if (own_new && wave == 0) {
+    const v4f* src = reinterpret_cast<const v4f*>(p.kraw + ((int64_t)b * p.nkv + g) * HD + d0);
+    kr_lo = src[0];
+    kr_hi = src[1];
+    kgain = *reinterpret_cast<const v4u*>(p.gk + d0);
+  }
+
+  // Per-head norm + RoPE (blocks with q/k norms) of a head vector held as 8
+  // values per lane by the LPK lanes of a key group: the squares are summed over
+  // the group, and the rotation partner of dim d (d +- HD/2) sits LPK/2 lanes away.
+  // This lane's rotation factors (dims d0..d0+7 at the new position, sign folded
+  // into the sine) and the query gains: the same for every head of the group.
+  float rc[8], rsn[8], gqf[8];
+  if (qkn) {
+    const int i0 = d0 % (HD / 2);
+    const float sgn = d0 < HD / 2 ? -1.f : 1.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      rc[i] = p.rope_cos[(int64_t)npos * (HD / 2) + i0 + i];
+      rsn[i] = sgn * p.rope_sin[(int64_t)npos * (HD / 2) + i0 + i];
+    }
+    bf16x8(*reinterpret_cast<const v4u*>(p.gq + d0), gqf);
+  }
+  auto norm_rope = [&](float (&x)[8], const float (&gf)[8]) {
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
+    const float rs = 1.0f / sqrtf(group_sum<LPK>(ss) / (float)HD + p.eps);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] *= rs * gf[i];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {  // the partner dim (d +- HD/2) is LPK/2 lanes away
+      const float y = LPK == 16 ? dpp<kDppRor8>(x[i]) : __shfl_xor(x[i], LPK / 2);
+      x[i] = x[i] * rc[i] + y * rsn[i];
+    }
+  };
+
   // The scaled query as fp16 pairs: a score is then 4 packed fp16 dot products
   // (fp32 accumulation) against the key's fp16 values as stored in the cache.
   h2 qh[G][4];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const v4f* src = reinterpret_cast<const v4f*>(p.q + (int64_t)b * p.nq * HD + (hq0 + h) * HD + d0);
-    const v4f lo = src[0] * p.scale_log2, hi = src[1] * p.scale_log2;
-    qh[h][0] = __builtin_convertvector(f2{lo.x, lo.y}, h2);
-    qh[h][1] = __builtin_convertvector(f2{lo.z, lo.w}, h2);
-    qh[h][2] = __builtin_convertvector(f2{hi.x, hi.y}, h2);
-    qh[h][3] = __builtin_convertvector(f2{hi.z, hi.w}, h2);
+    const v4f lo0 = src[0], hi0 = src[1];
+    float x[8] = {lo0.x, lo0.y, lo0.z, lo0.w, hi0.x, hi0.y, hi0.z, hi0.w};
+    if (qkn) norm_rope(x, gqf);
+    const float sc = p.scale_log2;
+    qh[h][0] = __builtin_convertvector(f2{x[0] * sc, x[1] * sc}, h2);
+    qh[h][1] = __builtin_convertvector(f2{x[2] * sc, x[3] * sc}, h2);
+    qh[h][2] = __builtin_convertvector(f2{x[4] * sc, x[5] * sc}, h2);
+    qh[h][3] = __builtin_convertvector(f2{x[6] * sc, x[7] * sc}, h2);
+  }
+
+  // The new key (blocks with q/k norms): the workgroup whose split holds it
+  // normalises and rotates it once (wave 0), stores it to the cache for later
+  // steps and to LDS, and the lanes that loaded that slot from the cache take
+  // it from LDS instead.
+  __shared__ __attribute__((aligned(16))) uint16_t knew[HD];
+  if (own_new) {
+    if (wave == 0) {
+      float x[8] = {kr_lo.x, kr_lo.y, kr_lo.z, kr_lo.w, kr_hi.x, kr_hi.y, kr_hi.z, kr_hi.w};
+      float gkf[8];
+      bf16x8(kgain, gkf);
+      norm_rope(x, gkf);
+      if (kgrp == 0) {
+        const v4u kv16 = v4u{f16_pair(x[0], x[1]), f16_pair(x[2], x[3]), f16_pair(x[4], x[5]), f16_pair(x[6], x[7])};
+        *reinterpret_cast<v4u*>(p.kc + kv_offset(p.kv, u, g, npos, HD) + d0) = kv16;
+        *reinterpret_cast<v4u*>(&knew[d0]) = kv16;
+      }
+    }
+    __syncthreads();
   }
 
   // One step: the chunk at c0, held in slot `slot`.
   auto step = [&](auto slot) {
     constexpr int sl = decltype(slot)::value;
+    if (own_new) {
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        if (s0 + c0 + j * KPW + kgrp == npos) kw[sl][j] = *reinterpret_cast<const v4u*>(&knew[d0]);
+    }
     float sc[J][G];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
@@ -904,35 +981,6 @@ __global__ void kv_table_update_kernel(int* table, const KvTableUpdate u) {
   if (i < u.n) table[u.idx[i]] = u.val[i];
 }
 
-// ------------------------------------------------------------------ q / k head norms
-// One wave per (head, batch row): lane l holds elements l and l + HD/2 of the
-// head vector, which are also the pair RoPE rotates together.
-template <int HD>
-__global__ __launch_bounds__(64) void qk_norm_rope_kernel(const QkNormParams p) {
-  constexpr int HALF = HD / 2;
-  const int h = blockIdx.x, b = blockIdx.y, l = threadIdx.x;
-  const bool isq = h < p.nq;
-  const float* src = isq ? p.q + ((int64_t)b * p.nq + h) * HD : p.kraw + ((int64_t)b * p.nkv + h - p.nq) * HD;
-  const bool act = l < HALF;
-  const float a = act ? src[l] : 0.f, c = act ? src[l + HALF] : 0.f;
-  const float rs = 1.0f / sqrtf(wave_sum(a * a + c * c) / (float)HD + p.eps);
-  if (!act) return;
-  const uint16_t* g = isq ? p.gq : p.gk;
-  const float x1 = a * rs * bf16_to_f32(g[l]), x2 = c * rs * bf16_to_f32(g[l + HALF]);
-  const int pos = p.pos[b];
-  const float cs = p.rope_cos[(int64_t)pos * HALF + l], sn = p.rope_sin[(int64_t)pos * HALF + l];
-  const float z1 = x1 * cs - x2 * sn, z2 = x2 * cs + x1 * sn;
-  if (isq) {
-    float* dst = p.q + ((int64_t)b * p.nq + h) * HD;
-    dst[l] = z1;
-    dst[l + HALF] = z2;
-  } else {
-    uint16_t* k = p.kc + kv_offset(p.kv, p.users[b], h - p.nq, pos, HD);
-    k[l] = f32_to_f16(z1);
-    k[l + HALF] = f32_to_f16(z2);
-  }
-}
-
 // ------------------------------------------------------------------ launchers
 template <int B, int R, int U>
 static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
@@ -988,15 +1036,6 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   const int grid = gemv_grid(epi, R, p);
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
   return hipErrorInvalidValue;
-}
-
-hipError_t launch_qk_norm_rope(const QkNormParams& p, int batch, hipStream_t s) {
-  if (batch < 1 || batch > kMaxBatch) return hipErrorInvalidValue;
-  const dim3 grid(p.nq + p.nkv, batch);
-  if (p.hd == 128) hipLaunchKernelGGL(qk_norm_rope_kernel<128>, grid, dim3(64), 0, s, p);
-  else if (p.hd == 64) hipLaunchKernelGGL(qk_norm_rope_kernel<64>, grid, dim3(64), 0, s, p);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
 }
 
 template <int HD, int G>

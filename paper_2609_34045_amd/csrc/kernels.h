@@ -79,7 +79,7 @@ struct GemvParams {
   int pos[kMaxBatch];
   // Blocks with per-head q/k norms: when set, q goes to `q` and k to kraw
   // ([B][nkv][hd] fp32) as projected (after the attention RMSNorm), without
-  // RoPE; launch_qk_norm_rope finishes both.  v goes to the cache as usual.
+  // RoPE; the decode attention finishes both.  v goes to the cache as usual.
   float* kraw;
 
   // kEpiSwiGLU
@@ -104,7 +104,7 @@ struct GemvParams {
 
 struct AttnParams {
   const float* q;      // [B][nq*hd] rotated queries
-  const uint16_t* kc;  // layer base (fp16 bits), pages as in KvPages
+  uint16_t* kc;        // layer base (fp16 bits), pages as in KvPages (written only for the new key of qk-norm blocks)
   const uint16_t* vc;
   float* part_acc;     // [B][nq][max_split][hd]
   float* part_ml;      // [B][nq][max_split][2]
@@ -116,23 +116,18 @@ struct AttnParams {
   float scale_log2;    // log2(e) / sqrt(hd)
   int users[kMaxBatch];
   int len[kMaxBatch];  // keys visible to row b: position + 1
-};
-
-// Per-head RMSNorm + RoPE of the raw q and k rows (Qwen3-style blocks); k is
-// appended to the cache at each row's position, q is rotated in place.
-struct QkNormParams {
-  float* q;             // [B][nq][hd]
-  const float* kraw;    // [B][nkv][hd]
-  uint16_t* kc;         // layer base of the K cache (fp16 bits), pages as in KvPages
-  const uint16_t* gq;   // [hd] bf16 gains
+  // Blocks with per-head q/k norms: q holds the projections as they come from
+  // the QKV GEMV (no RoPE).  Every workgroup RMS-normalises (gains gq, eps) and
+  // rotates the query heads it scores; the workgroup whose split holds row b's
+  // new position does the same for the new key (kraw, gains gk), stores it to the
+  // cache and scores it from registers.  kraw NULL: q is already rotated and the
+  // new key is in the cache.
+  const float* kraw;      // [B][nkv][hd]
+  const uint16_t* gq;     // [hd] bf16
   const uint16_t* gk;
-  const float* rope_cos;
+  const float* rope_cos;  // [max_ctx][hd/2]
   const float* rope_sin;
-  KvPages kv;
-  int nq, nkv, hd;
   float eps;
-  int users[kMaxBatch];
-  int pos[kMaxBatch];
 };
 
 // Launchers (return hipGetLastError() of the launch).
@@ -142,7 +137,6 @@ hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
-hipError_t launch_qk_norm_rope(const QkNormParams& p, int batch, hipStream_t s);
 // x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] bf16).
 hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,

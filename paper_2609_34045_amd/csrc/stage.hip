@@ -764,29 +764,6 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
     tr.end(KF_K_QKV);
     KF_HIP(le, "qkv launch");
-    if (c.qk_norm) {
-      QkNormParams qn{};
-      qn.q = s->q;
-      qn.kraw = s->kraw;
-      qn.kc = kv->k + loff;
-      qn.gq = L.g_qn;
-      qn.gk = L.g_kn;
-      qn.rope_cos = kv->rcos;
-      qn.rope_sin = kv->rsin;
-      qn.kv = kv->pages();
-      qn.nq = c.n_q_heads;
-      qn.nkv = c.n_kv_heads;
-      qn.hd = hd;
-      qn.eps = c.rms_eps;
-      for (int b = 0; b < kMaxBatch; ++b) {
-        qn.users[b] = g.users[b];
-        qn.pos[b] = g.pos[b];
-      }
-      tr.begin(KF_K_QKNORM);
-      const hipError_t qe = launch_qk_norm_rope(qn, batch, st);
-      tr.end(KF_K_QKNORM);
-      KF_HIP(qe, "q/k norm launch");
-    }
 
     AttnParams a{};
     a.q = s->q;
@@ -795,6 +772,14 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     a.part_acc = kv->part_acc;
     a.part_ml = kv->part_ml;
     a.kv = kv->pages();
+    if (c.qk_norm) {  // q / k left raw by the QKV launch: the attention normalises and rotates them
+      a.kraw = s->kraw;
+      a.gq = L.g_qn;
+      a.gk = L.g_kn;
+      a.rope_cos = kv->rcos;
+      a.rope_sin = kv->rsin;
+      a.eps = c.rms_eps;
+    }
     a.nq = c.n_q_heads;
     a.nkv = c.n_kv_heads;
     a.hd = hd;
