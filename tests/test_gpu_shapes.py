@@ -1,0 +1,75 @@
+"""Every query-group size the decode attention is built for, against the float64 oracle.
+
+The decode attention is instantiated per G = n_q_heads / n_kv_heads (1 to 8) and
+head_dim (64, 128); the workload shapes reach G = 4, 5 and 8.  Small two-layer
+stages with the head cover the rest, G = 1 (multi-head attention, the degenerate
+case) included, and one Qwen3-style variant: chunked prefill from tokens,
+ragged batched decode, and the head's greedy token.  Every call goes through the
+C ABI.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleStage
+from tests.helpers import SeededModel, argmax_agrees, assert_hidden_close
+
+pytestmark = pytest.mark.gpu
+
+CASES = [  # (n_q_heads, n_kv_heads, head_dim, qk_norm)
+    (4, 4, 64, False),    # G = 1
+    (4, 2, 128, False),   # G = 2
+    (6, 2, 64, False),    # G = 3
+    (12, 2, 128, False),  # G = 6
+    (14, 2, 64, False),   # G = 7
+    (6, 3, 128, True),    # G = 2, per-head q/k norms, query width 768 against hidden 256
+]
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+@pytest.fixture(scope="module")
+def st():
+    from paper_2609_34045_amd import stage
+    return stage
+
+
+def host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("nq,nkv,hd,qkn", CASES, ids=[f"g{c[0] // c[1]}_hd{c[2]}{'_qknorm' if c[3] else ''}" for c in CASES])
+def test_group_size(torch, st, nq, nkv, hd, qkn):
+    shape = synth.ModelShape(2, 256, nq, nkv, hd, 512, 300, 1e-5, 1e4, qk_norm=qkn)
+    cfg = 50 + nq + nkv + hd // 64
+    model = SeededModel(shape, cfg)
+    g = st.Stage(shape, 0, 2, model.layer, model.head())
+    kv = g.kv(3, 200)
+    o = OracleStage(shape, 0, 2, model.layer, model.head(), max_users=3, max_ctx=200)
+    worst = 0.0
+    for u, n in ((0, 70), (1, 5), (2, 130)):  # prompts: several splits, one tiny, several key blocks
+        toks = synth.tokens(cfg, u, n, shape.vocab)
+        for c0 in range(0, n, 48):
+            part = toks[c0:c0 + 48]
+            y = g.prefill(kv, u, c0, tokens=torch.from_numpy(part).cuda())
+            worst = max(worst, assert_hidden_close(host(y), o.prefill(u, c0, tokens=part), what=f"prefill {u}@{c0}"))
+    for step, users in enumerate(([0, 1, 2], [2, 0], [1], [0, 1, 2])):
+        pos = [kv.len(u) for u in users]
+        x = synth.hidden_states(cfg, synth.STREAM_DECODE_HIDDEN, step, len(users), shape.hidden)
+        y = g.decode(kv, users, pos, hidden=torch.from_numpy(x).cuda())
+        ref = o.decode(users, pos, hidden=x)
+        worst = max(worst, assert_hidden_close(host(y), ref, what=f"decode {step}"))
+        lg = host(g.head_logits(y))
+        lr = o.logits(ref)
+        tg = host(g.head_argmax(y)).astype(np.int64)
+        for b in range(len(users)):
+            assert argmax_agrees(int(tg[b]), int(np.argmax(lr[b])), lr[b], lg[b])
+    print(f"G={nq // nkv} hd={hd} qk_norm={qkn} max row rel err", worst)
+    kv.close()
+    g.close()
