@@ -441,9 +441,11 @@ void gemv_kernel(const GemvParams p) {
 // A key's hd elements are read by hd/8 lanes, 16 bytes each; all G query heads of
 // the group are scored against it, so each K/V byte is read once per KV head.
 // Each wave runs its own online softmax over chunks of 4 keys per lane group (K
-// and V of a chunk are loaded together, so one memory latency covers both); the
-// four waves' (max, sum, acc) states are merged through LDS and written as the
-// split's partial.
+// and V of a chunk are loaded together, so one memory latency covers both, and
+// DEPTH chunks are in flight); the four waves' (max, sum, acc) states are merged
+// through LDS and written as the split's partial.  For blocks with per-head q/k
+// norms the kernel also normalises and rotates the queries, and the new key in
+// the workgroup that holds it.
 #ifndef KF_ATTN_J
 #define KF_ATTN_J 4
 #endif
