@@ -258,7 +258,10 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       const int r = tid / B, b = tid % B;
       const float gt = fin[r * B + b] * rs[b];
       const float up = fin[(r + R / 2) * B + b] * rs[b];
-      p.act[(int64_t)b * p.N + wg * (R / 2) + r] = gt / (1.0f + expf(-gt)) * up;
+      const float a = gt / (1.0f + expf(-gt)) * up;
+      const int64_t at = (int64_t)b * p.N + wg * (R / 2) + r;
+      if (p.act16) reinterpret_cast<uint16_t*>(p.act)[at] = f32_to_f16(a);
+      else p.act[at] = a;
     }
   } else {  // kEpiLMHead
     if (p.logits) {
@@ -321,7 +324,7 @@ __device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, in
 // input rows and partial sums put the kernel just past 128 VGPRs (3 waves per
 // SIMD), so the register budget is held to 4 waves there.  Smaller batches are
 // left to the compiler (a cap costs the batch-1 gate/up kernel a wave).
-template <int B, int R, int U, int EPI, bool NORM, bool SRC = false>
+template <int B, int R, int U, int EPI, bool NORM, bool SRC = false, bool IN16 = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(B >= 3 ? KF_GEMV_MIN_WAVES : 1)))
 void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
@@ -362,6 +365,11 @@ void gemv_kernel(const GemvParams p) {
         for (int b = 0; b < B; ++b) {
           if (SRC) {
             stage_input_chunk(p, b, c, xl[u][b], xh[u][b]);
+          } else if (IN16) {  // 8 fp16 inputs (16 bytes), converted exactly
+            float f[8];
+            f16x8(*reinterpret_cast<const v4u*>(reinterpret_cast<const uint16_t*>(p.in) + (int64_t)b * K + c * 8), f);
+            xl[u][b] = v4f{f[0], f[1], f[2], f[3]};
+            xh[u][b] = v4f{f[4], f[5], f[6], f[7]};
           } else {
             const v4f* src = reinterpret_cast<const v4f*>(p.in + (int64_t)b * K + c * 8);
             xl[u][b] = src[0];
@@ -988,7 +996,9 @@ template <int B, int R, int U>
 static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
   if (epi == kEpiQKV && norm)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
-  else if (epi == kEpiResid && !norm)
+  else if (epi == kEpiResid && !norm && B > 1 && p.in16)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiResid && !norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiSwiGLU && norm)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);

@@ -83,7 +83,10 @@ struct GemvParams {
   float* kraw;
 
   // kEpiSwiGLU
-  float* act;          // [B][N] with N = F
+  float* act;          // [B][N] with N = F: fp32, or fp16 when act16 is set
+  int act16;
+  // Input rows `in` stored as fp16 (the down projection's input at batch > 1), else fp32.
+  int in16;
 
   // Launches with the stage input as their input rows (instead of `in`): the
   // first layer's QKV and the LM head.  Exactly one of src / tokens is set.

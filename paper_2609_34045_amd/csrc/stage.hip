@@ -815,6 +815,10 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.K = H;
     gu.N = c.ffn;
     gu.act = s->act;
+    // From batch 2 the SwiGLU output goes to the down projection as fp16 (the
+    // prefill's down GEMM takes the same operand in fp16): the input rows of
+    // batch 2-4 then fit the vector cache beside the weights stream.
+    gu.act16 = batch > 1;
     {
       tr.begin(KF_K_GATEUP);
       const hipError_t le = launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
@@ -826,6 +830,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     d.batch = batch;
     d.w0 = L.wd;
     d.in = s->act;
+    d.in16 = batch > 1;
     d.K = c.ffn;
     d.N = H;
     d.x = s->x;
