@@ -247,6 +247,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
         const int64_t at = (int64_t)b * p.N + row;
         const float v = pre.a + fin[t];
         p.x[at] = v;
+        if (p.x16) p.x16[at] = f32_to_f16(v);
         if (p.out2) {
           if (p.out2_bf16) reinterpret_cast<uint16_t*>(p.out2)[at] = f32_to_bf16(v);
           else reinterpret_cast<float*>(p.out2)[at] = v;
@@ -735,6 +736,65 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   }
 }
 
+// Merge of the split-KV partials of one (head h, row b): weights 2^(m_s - M)
+// over the splits that saw keys (M their largest max), the weighted partial
+// vectors summed and divided by the weighted partial sums.  The split weights are
+// computed by all threads at once and kept in LDS; then each wave sums every
+// fourth split's vector (independent loads) and the four sums are combined.  The
+// result goes out in fp16 for the output projection's GEMV (batch > 1).
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams a, uint16_t* __restrict__ o16) {
+  constexpr int DPL = HD / 64;
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ns = a.n_split;
+  const int64_t r0 = ((int64_t)b * a.nq + h) * a.max_split;
+  const float* ml = a.part_ml + r0 * 2;
+  const float* acc = a.part_acc + r0 * HD + lane * DPL;
+  __shared__ float wsm[kAttnMaxSplitCount];
+  __shared__ float red[4][HD];
+  __shared__ float sM[4], sL[4];
+
+  float M = -INFINITY;
+  for (int s = tid; s < ns; s += 256)
+    if (ml[2 * s + 1] > 0.f) M = fmaxf(M, ml[2 * s]);
+  M = wave_max(M);
+  if (lane == 0) sM[wave] = M;
+  __syncthreads();
+  M = fmaxf(fmaxf(sM[0], sM[1]), fmaxf(sM[2], sM[3]));
+  float L = 0.f;
+  for (int s = tid; s < ns; s += 256) {
+    const float l = ml[2 * s + 1];
+    const float w = l > 0.f ? __builtin_amdgcn_exp2f(ml[2 * s] - M) : 0.f;  // no keys: weight 0
+    wsm[s] = w;
+    L += w * l;
+  }
+  L = wave_sum(L);
+  if (lane == 0) sL[wave] = L;
+  __syncthreads();
+
+  float o[DPL];
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) o[i] = 0.f;
+#pragma unroll 8
+  for (int s = wave; s < ns; s += 4) {
+    const float w = wsm[s];
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) o[i] += w * acc[(int64_t)s * HD + i];
+  }
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) red[wave][lane * DPL + i] = o[i];
+  __syncthreads();
+  if (wave == 0) {
+    const float inv = 1.0f / ((sL[0] + sL[1]) + (sL[2] + sL[3]));  // every row has at least one key
+    uint16_t* dst = o16 + ((int64_t)b * a.nq + h) * HD + lane * DPL;
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) {
+      const int d = lane * DPL + i;
+      dst[i] = f32_to_f16(((red[0][d] + red[1][d]) + (red[2][d] + red[3][d])) * inv);
+    }
+  }
+}
+
 // Output projection fused with the merge of the split-KV partials.  Workgroup
 // (row block rb, query head h) merges head h's partials of every batch row
 // into o_h in LDS (wave b takes row b: weights 2^(m_s - M) per split, sum of
@@ -1000,7 +1060,9 @@ static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiResid && !norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
-  else if (epi == kEpiSwiGLU && norm)
+  else if (epi == kEpiSwiGLU && norm && B > 1 && p.in16)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiSwiGLU && norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiLMHead && norm)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true>), dim3(grid), dim3(256), 0, s, p);
@@ -1092,6 +1154,15 @@ static hipError_t oproj_dispatch(const AttnParams& a, const uint16_t* w, float* 
     case 4: hipLaunchKernelGGL((oproj_heads_kernel<4, HD>), grid, dim3(256), 0, s, a, w, x, N); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_merge(const AttnParams& a, uint16_t* o16, int batch, hipStream_t s) {
+  if (batch < 1 || batch > kMaxBatch) return hipErrorInvalidValue;
+  const dim3 grid(a.nq, batch);
+  if (a.hd == 128) hipLaunchKernelGGL(attn_merge_kernel<128>, grid, dim3(256), 0, s, a, o16);
+  else if (a.hd == 64) hipLaunchKernelGGL(attn_merge_kernel<64>, grid, dim3(256), 0, s, a, o16);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

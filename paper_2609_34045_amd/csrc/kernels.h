@@ -66,6 +66,7 @@ struct GemvParams {
   float* x;            // [B][N] residual stream, updated in place
   void* out2;          // optional [B][N] copy of the updated rows (hidden output), dtype out2_bf16
   int out2_bf16;
+  uint16_t* x16;       // optional [B][N] fp16 copy of the updated rows (the next GEMV's input)
 
   // kEpiQKV
   float* q;            // [B][nq*hd]
@@ -140,6 +141,8 @@ hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
+// o16[b][h*hd:(h+1)*hd] (fp16) = head h of row b merged from the attention partials in p.
+hipError_t launch_attn_merge(const AttnParams& p, uint16_t* o16, int batch, hipStream_t s);
 // x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] bf16).
 hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,

@@ -52,6 +52,8 @@ struct kf_stage {
   // decode workspace
   char* ws = nullptr;
   float *x = nullptr, *q = nullptr, *act = nullptr;
+  // batch > 1: merged attention output and the residual after the output projection, in fp16
+  uint16_t *o16 = nullptr, *x16 = nullptr;
   float* kraw = nullptr;  // [B][nkv][hd] new keys before their norm and RoPE (qk_norm blocks)
   float* part_val = nullptr;
   int* part_idx = nullptr;
@@ -227,6 +229,8 @@ static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
   n += align256(B * H * 4);                           // x
   n += align256(B * c.n_q_heads * c.head_dim * 4);    // q
   n += align256(B * (int64_t)c.ffn * 4);              // act
+  n += align256(B * c.n_q_heads * c.head_dim * 2);    // o16
+  n += align256(B * H * 2);                           // x16
   if (c.qk_norm) n += align256(B * (int64_t)c.n_kv_heads * c.head_dim * 4);  // kraw
   if (has_head) {
     const int64_t wgs = (c.vocab + 3) / 4;  // enough for any rows-per-workgroup choice
@@ -416,6 +420,8 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->x = (float*)take(B * H * 4);
   s->q = (float*)take(B * c.n_q_heads * hd * 4);
   s->act = (float*)take(B * F * 4);
+  s->o16 = (uint16_t*)take(B * c.n_q_heads * hd * 2);
+  s->x16 = (uint16_t*)take(B * H * 2);
   if (c.qk_norm) s->kraw = (float*)take(B * c.n_kv_heads * hd * 4);
   if (has_head) {
     s->lm_wg = (int)((V + kGemvRows - 1) / kGemvRows);
@@ -798,9 +804,29 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       KF_HIP(le, "attention launch");
     }
 
-    {
+    if (batch == 1) {  // the merge fused into a head-split output projection (one launch)
       tr.begin(KF_K_OPROJ);
       const hipError_t le = launch_oproj_heads(a, L.wo, s->x, H, batch, st);
+      tr.end(KF_K_OPROJ);
+      KF_HIP(le, "o-proj launch");
+    } else {
+      // The merge on its own, then a row-owning GEMV that also leaves the updated
+      // residual in fp16 for the gate/up launch: at batch 2-4 the input rows in
+      // fp32 would crowd the vector cache the weights stream through.
+      tr.begin(KF_K_OPROJ);
+      hipError_t le = launch_attn_merge(a, s->o16, batch, st);
+      if (le == hipSuccess) {
+        GemvParams op{};
+        op.batch = batch;
+        op.w0 = L.wo;
+        op.in = reinterpret_cast<const float*>(s->o16);
+        op.in16 = 1;
+        op.K = c.n_q_heads * hd;
+        op.N = H;
+        op.x = s->x;
+        op.x16 = s->x16;
+        le = launch_gemv(kEpiResid, kGemvRows, kGemvChunks, false, op, st);
+      }
       tr.end(KF_K_OPROJ);
       KF_HIP(le, "o-proj launch");
     }
@@ -811,7 +837,8 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.w0 = L.wg;
     gu.w1 = L.wu;
     gu.gain = L.g_mlp;
-    gu.in = s->x;
+    gu.in = batch > 1 ? reinterpret_cast<const float*>(s->x16) : s->x;
+    gu.in16 = batch > 1;
     gu.K = H;
     gu.N = c.ffn;
     gu.act = s->act;
