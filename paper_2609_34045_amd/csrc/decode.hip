@@ -247,10 +247,9 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
         const int64_t at = (int64_t)b * p.N + row;
         const float v = pre.a + fin[t];
         p.x[at] = v;
-        if (p.x16) p.x16[at] = f32_to_f16(v);
         if (p.out2) {
-          if (p.out2_bf16) reinterpret_cast<uint16_t*>(p.out2)[at] = f32_to_bf16(v);
-          else reinterpret_cast<float*>(p.out2)[at] = v;
+          if (p.out2_type == kOut2F32) reinterpret_cast<float*>(p.out2)[at] = v;
+          else reinterpret_cast<uint16_t*>(p.out2)[at] = p.out2_type == kOut2BF16 ? f32_to_bf16(v) : f32_to_f16(v);
         }
       }
     }
@@ -1054,7 +1053,9 @@ __global__ void kv_table_update_kernel(int* table, const KvTableUpdate u) {
 // ------------------------------------------------------------------ launchers
 template <int B, int R, int U>
 static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
-  if (epi == kEpiQKV && norm)
+  if (epi == kEpiQKV && norm && B > 1 && p.in16)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiQKV && norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiResid && !norm && B > 1 && p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);

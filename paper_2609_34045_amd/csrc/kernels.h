@@ -51,6 +51,9 @@ enum GemvEpi : int {
   kEpiLMHead = 3,  // optional fp32 logits, per-workgroup (max, lowest index) partials
 };
 
+// Element type of a residual GEMV's optional copy output.
+enum { kOut2F32 = 0, kOut2BF16 = 1, kOut2F16 = 2 };
+
 // One decode GEMV launch: y[b][n] = sum_k W[n][k] * in[b][k] (* gain[k] * rsqrt(mean(in^2)+eps) if norm).
 struct GemvParams {
   const uint16_t* w0;  // matrix rows (QKV: [q;k;v] rows; SwiGLU: gate; others: the matrix)
@@ -64,9 +67,8 @@ struct GemvParams {
 
   // kEpiResid
   float* x;            // [B][N] residual stream, updated in place
-  void* out2;          // optional [B][N] copy of the updated rows (hidden output), dtype out2_bf16
-  int out2_bf16;
-  uint16_t* x16;       // optional [B][N] fp16 copy of the updated rows (the next GEMV's input)
+  void* out2;          // optional [B][N] copy of the updated rows, element type out2_type
+  int out2_type;       // kOut2F32, kOut2BF16 (a bf16 hidden output) or kOut2F16 (the next GEMV's input)
 
   // kEpiQKV
   float* q;            // [B][nq*hd]

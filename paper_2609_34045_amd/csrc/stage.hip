@@ -737,7 +737,9 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     // attention RMSNorm + QKV + RoPE + KV append
     g.w0 = L.wqkv;
     g.gain = L.g_attn;
-    g.in = s->x;
+    // from batch 2 the previous layer's down projection left the residual in fp16 too
+    g.in = batch > 1 ? reinterpret_cast<const float*>(s->x16) : s->x;
+    g.in16 = batch > 1;
     g.K = H;
     g.N = (c.n_q_heads + 2 * c.n_kv_heads) * hd;
     g.q = s->q;
@@ -764,6 +766,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.vocab = c.vocab;
       g.x_init = s->x;
       g.err_flag = s->err_flag;
+      g.in16 = 0;  // the input rows come from src / tokens
       le = launch_gemv_src(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
     } else {
       le = launch_gemv(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
@@ -824,7 +827,8 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
         op.K = c.n_q_heads * hd;
         op.N = H;
         op.x = s->x;
-        op.x16 = s->x16;
+        op.out2 = s->x16;
+        op.out2_type = kOut2F16;
         le = launch_gemv(kEpiResid, kGemvRows, kGemvChunks, false, op, st);
       }
       tr.end(KF_K_OPROJ);
@@ -863,7 +867,10 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     d.x = s->x;
     if (l == s->hi - 1) {
       d.out2 = hidden_out_dev;
-      d.out2_bf16 = io == KF_BF16;
+      d.out2_type = io == KF_BF16 ? kOut2BF16 : kOut2F32;
+    } else if (batch > 1) {
+      d.out2 = s->x16;  // the next layer's QKV input
+      d.out2_type = kOut2F16;
     }
     {
       tr.begin(KF_K_DOWN);
