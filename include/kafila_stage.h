@@ -129,7 +129,11 @@ kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t layer_lo, int32_t l
  * device) before the call returns, so the caller may free them afterwards.  Every
  * layer tensor of every held layer must be present exactly once (kinds 0..8, plus
  * KF_W_Q_NORM and KF_W_K_NORM when qk_norm), plus the three head tensors when
- * has_head; anything else is KF_EINVAL.  hip_stream (a
+ * has_head; anything else is KF_EINVAL.  The weight matrices (kinds Q, K, V, O, GATE,
+ * UP, DOWN, LM_HEAD) are stored in fp16, rounded to nearest even from the bf16
+ * given: exact for 2^-17 <= |w| < 65504 and for 0, within 2^-25 below that.  A finite
+ * weight that fp16 cannot hold (|w| >= 65520) is KF_EINVAL.  Gains and the
+ * embedding table stay bf16.  hip_stream (a
  * hipStream_t, NULL for the default stream) is where all later work is enqueued.
  */
 kf_status kf_stage_init(const kf_model_config* cfg, int32_t layer_lo, int32_t layer_hi, int32_t has_head,
@@ -230,8 +234,8 @@ kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32
  * pos0 must equal the user's length and pos0 + n_tokens <= max_ctx.  Token i attends
  * slots 0..pos0+i.  tokens_dev int32 [n] or hidden_in_dev [n, H]; hidden_out_dev [n, H].
  * A paged cache lends the pages up to pos0 + n (KF_ENOMEM if it cannot).
- * Dense products run on the matrix cores with fp16 operands (bf16 weights converted
- * exactly while staged) and fp32 accumulation.
+ * Dense products run on the matrix cores with fp16 operands (the stage's fp16 weights)
+ * and fp32 accumulation.
  * On success the user's length advances by n_tokens.
  */
 kf_status kf_stage_prefill(kf_stage* stage, kf_kv* kv, int32_t user, int32_t pos0, int32_t n_tokens,

@@ -3,7 +3,8 @@
 // At this batch size a stage reads each weight once per step and does a
 // handful of FLOPs per weight byte, so every matrix product here is an
 // HBM-bound GEMV (Section V-A of the paper prices a stage by exactly these
-// bytes).  The kernels therefore stream bf16 weights with 16-byte non-temporal
+// bytes).  The kernels therefore stream the weights (fp16, converted from the model's
+// bf16 when the stage is created) with 16-byte non-temporal
 // loads, keep the (tiny) activations in L1/L2, and fuse everything elementwise
 // into the GEMV that produces or consumes it:
 //   * RMSNorm is folded into the consuming GEMV: the same loop that multiplies
@@ -62,6 +63,19 @@ __device__ __forceinline__ void f16x8(const v4u w, float (&f)[8]) {
   const f8 v = __builtin_convertvector(__builtin_bit_cast(h8, w), f8);
 #pragma unroll
   for (int i = 0; i < 8; ++i) f[i] = v[i];
+}
+
+#ifndef KF_GEMV_DOT
+#define KF_GEMV_DOT 0xF  // GEMV epilogues (bit per GemvEpi) whose fp16-input launches use packed dot products
+#endif
+
+// As f16x8, for products against fp32 inputs at batch > 1: the empty asm keeps
+// the conversions separate instructions, since folding each into every row's
+// FMA (a mixed-precision FMA per product) is several times slower.
+__device__ __forceinline__ void f16x8_apart(const v4u w, float (&f)[8]) {
+  f16x8(w, f);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) asm("" : "+v"(f[i]));
 }
 
 // fp32 to fp16 bits, round to nearest even.
@@ -353,8 +367,12 @@ void gemv_kernel(const GemvParams p) {
   // weight rows arrive; measured faster at batch > 1 and for QKV, while the
   // batch-1 gate/up and down launches are faster with the weights first.
   constexpr bool kInputFirst = B > 1 || EPI == kEpiQKV;
+  // fp16 inputs (batch 2-4) meet the fp16 weights in packed dot products: two
+  // products per instruction, summed in fp32.
+  constexpr bool kDot = IN16 && !SRC && ((KF_GEMV_DOT >> EPI) & 1);
   for (int c0 = tid; c0 < nch; c0 += T * U) {
     v4f xl[U][B], xh[U][B];
+    v4u xr[U][B];
     v4u gv[U];
     v4u wv[U][R];
     auto load_input = [&]() {
@@ -365,6 +383,8 @@ void gemv_kernel(const GemvParams p) {
         for (int b = 0; b < B; ++b) {
           if (SRC) {
             stage_input_chunk(p, b, c, xl[u][b], xh[u][b]);
+          } else if (kDot) {
+            xr[u][b] = *reinterpret_cast<const v4u*>(reinterpret_cast<const uint16_t*>(p.in) + (int64_t)b * K + c * 8);
           } else if (IN16) {  // 8 fp16 inputs (16 bytes), converted exactly
             float f[8];
             f16x8(*reinterpret_cast<const v4u*>(reinterpret_cast<const uint16_t*>(p.in) + (int64_t)b * K + c * 8), f);
@@ -390,6 +410,10 @@ void gemv_kernel(const GemvParams p) {
       }
     }
     if (!kInputFirst) load_input();
+    // every load of the chunk is issued before any arithmetic on it (left to
+    // itself the scheduler may sink each weight load to its first use, which
+    // leaves one 16-byte load per thread in flight)
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int c = c0 + u * T;
@@ -400,6 +424,44 @@ void gemv_kernel(const GemvParams p) {
             reinterpret_cast<v4f*>(p.x_init + (int64_t)b * K + c * 8)[0] = xl[u][b];
             reinterpret_cast<v4f*>(p.x_init + (int64_t)b * K + c * 8)[1] = xh[u][b];
           }
+        }
+        if constexpr (kDot) {
+          // input pairs in fp16; with the norm, x * gain rounded to fp16 (sum(x^2) in fp32)
+          h2 xp[B][4];
+          float gf[8];
+          if (NORM) bf16x8(gv[u], gf);
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+            if (NORM) {
+              float f[8];
+              f16x8_apart(xr[u][b], f);
+#pragma unroll
+              for (int i = 0; i < 8; ++i) acc[R * B + b] += f[i] * f[i];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) xp[b][j] = __builtin_convertvector(f2{f[2 * j] * gf[2 * j], f[2 * j + 1] * gf[2 * j + 1]}, h2);
+            } else {
+              const h8 x8 = __builtin_bit_cast(h8, xr[u][b]);
+              xp[b][0] = __builtin_shufflevector(x8, x8, 0, 1);
+              xp[b][1] = __builtin_shufflevector(x8, x8, 2, 3);
+              xp[b][2] = __builtin_shufflevector(x8, x8, 4, 5);
+              xp[b][3] = __builtin_shufflevector(x8, x8, 6, 7);
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < R; ++r) {
+            const h8 w8 = __builtin_bit_cast(h8, wv[u][r]);
+            const h2 w0 = __builtin_shufflevector(w8, w8, 0, 1), w1 = __builtin_shufflevector(w8, w8, 2, 3),
+                     w2 = __builtin_shufflevector(w8, w8, 4, 5), w3 = __builtin_shufflevector(w8, w8, 6, 7);
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+              float a = acc[r * B + b];
+              a = __builtin_amdgcn_fdot2(w0, xp[b][0], a, false);
+              a = __builtin_amdgcn_fdot2(w1, xp[b][1], a, false);
+              a = __builtin_amdgcn_fdot2(w2, xp[b][2], a, false);
+              acc[r * B + b] = __builtin_amdgcn_fdot2(w3, xp[b][3], a, false);
+            }
+          }
+          continue;
         }
         float xf[B][8];
 #pragma unroll
@@ -423,7 +485,8 @@ void gemv_kernel(const GemvParams p) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
           float wf[8];
-          bf16x8(wv[u][r], wf);
+          if (B > 1) f16x8_apart(wv[u][r], wf);
+          else f16x8(wv[u][r], wf);
 #pragma unroll
           for (int b = 0; b < B; ++b) {
 #pragma unroll
@@ -903,7 +966,7 @@ __global__ __launch_bounds__(256) void oproj_heads_kernel(const AttnParams a, co
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
     float wf[8];
-    bf16x8(wv[i], wf);
+    f16x8(wv[i], wf);
 #pragma unroll
     for (int bb = 0; bb < B; ++bb) {
       float t = 0.f;
@@ -1001,6 +1064,19 @@ __global__ __launch_bounds__(1024) void argmax_final_kernel(const float* part_va
       if (max_logit) max_logit[b] = best;
     }
   }
+}
+
+// In place: bf16 bits -> fp16 bits, round to nearest even.  Raises *bad when a
+// finite value lies beyond the fp16 range (it would become infinite).
+__global__ void weights_to_f16_kernel(uint16_t* w, int64_t n, int* bad) {
+  int flag = 0;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const float v = bf16_to_f32(w[i]);
+    const _Float16 h = (_Float16)v;
+    flag |= __builtin_isinf((float)h) && !__builtin_isinf(v);
+    w[i] = __builtin_bit_cast(uint16_t, h);
+  }
+  if (flag) atomicOr(bad, 1);
 }
 
 __global__ void store_hidden_kernel(const float* x, void* out, int out_bf16, int64_t n) {
@@ -1184,6 +1260,13 @@ hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
                                float* max_logit, hipStream_t s) {
   hipLaunchKernelGGL(argmax_final_kernel, dim3(rows), dim3(1024), 0, s, part_val, part_idx, n_wg, token, max_logit);
+  return hipGetLastError();
+}
+
+hipError_t launch_weights_to_f16(uint16_t* w, int64_t n, int* bad, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(weights_to_f16_kernel, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0, s, w, n, bad);
   return hipGetLastError();
 }
 

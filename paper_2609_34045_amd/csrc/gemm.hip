@@ -1,7 +1,7 @@
 // Prefill projections on the matrix cores: C[M][N] (+)= A[M][K] x W[N][K]^T.
 //
-// A is fp16 activations, W is bf16 weights (converted to fp16 exactly while
-// staged), both K-contiguous; the product runs on v_mfma_f32_32x32x16_f16 with
+// A is fp16 activations, W is fp16 weights (converted from the model's bf16
+// once, when the stage is created), both K-contiguous; the product runs on v_mfma_f32_32x32x16_f16 with
 // fp32 accumulation.  At a 512-token chunk the projections are large enough
 // to be bound by the matrix cores, which sets the tile shape:
 //   * 256 x 256 x 32 workgroup tiles, eight waves (two per SIMD) of 128 x 64,
@@ -15,8 +15,6 @@
 //     within a row so that fragment reads are free of bank conflicts;
 //   * each wave reads the fragments of the next 16-wide K slice while the
 //     MFMAs of the current one run;
-//   * weights stay bf16 in LDS and are converted to fp16 after the fragment
-//     read (exact; 12 ALU operations per 8 values, alongside the MFMAs);
 //   * narrow projections (few 256-wide column tiles) are split along K over
 //     several workgroups so that the grid covers the 256 CUs; the slices are
 //     either stored whole for the consuming kernel to add in order
@@ -34,8 +32,6 @@ namespace {
 
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -49,9 +45,6 @@ constexpr int kGemmWN = KF_GEMM_WN;
 constexpr int kGemmThreads = 128 * kGemmWN;
 #ifndef KF_GEMM_READS_PER_SLOT
 #define KF_GEMM_READS_PER_SLOT 1  // fragment reads issued per MFMA slot
-#endif
-#ifndef KF_GEMM_CVT_SLOT
-#define KF_GEMM_CVT_SLOT 8  // first MFMA slot of a half step that converts weights
 #endif
 #ifndef KF_GEMM_STAGGER
 #define KF_GEMM_STAGGER 1  // rotate the split-K atomic epilogue per K slice
@@ -67,15 +60,6 @@ static_assert(STAGES >= 3 && STAGES <= 5, "ring depth");
 constexpr int TILE_BYTES = BM * BK * 2;     // one operand's tile per stage (16 KB)
 constexpr int ROW_BYTES = BK * 2;           // 64 B: four 16-byte chunks per tile row
 
-__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, h2));
-}
-__device__ __forceinline__ v4u bf16x8_to_f16x8(v4u w) {
-  return v4u{pack_f16(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u)),
-             pack_f16(__uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)),
-             pack_f16(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xffff0000u)),
-             pack_f16(__uint_as_float(w.w << 16), __uint_as_float(w.w & 0xffff0000u))};
-}
 __device__ __forceinline__ uint16_t to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
 __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b), c, 0, 0, 0);
@@ -93,6 +77,9 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
+
+// Wait until this wave's LDS reads have returned (global loads may stay in flight).
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14)); }
 
 // Workgroup barrier that orders LDS accesses without waiting on outstanding
 // global loads (the compiler may not move memory operations across it).
@@ -120,7 +107,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
   constexpr int LOADS = TILE_BYTES / 1024 / NW;  // 1 KB direct loads per wave per operand per stage
   constexpr int SLOTS = 4 * JW;              // MFMAs per wave per 16-wide K slice
   static_assert(WN == 2 || WN == 4, "four or eight waves");
-  // STAGES x (A tile, W tile), each [256 rows][4 swizzled 16-byte chunks]; W stays bf16 here.
+  // STAGES x (A tile, W tile), each [256 rows][4 swizzled 16-byte chunks]; both fp16.
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * 2 * TILE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -183,14 +170,12 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // The K loop is scheduled by hand: each half step is 16 MFMA slots; the
+  // The K loop is scheduled by hand: each half step is SLOTS MFMA slots; the
   // first slots also issue the fragment reads for the next half (and, after
-  // the barrier, one global->LDS load each), the last slots convert the weight
-  // fragments read (whose reads have returned by then).
+  // the barrier, one global->LDS load each).
   const int rl = lane & 31, kh = lane >> 5;
   // fragment read q (0..JW+3) of sub-step s (16 values of K) of a stage: weight
-  // block q (still bf16) for q < JW, then A block q-JW, so that the conversions
-  // wait only on the first JW reads
+  // block q for q < JW, then A block q-JW
   auto read_frag = [&](int stage, int s, int q, v4u (&fa)[4], v4u (&fw)[JW]) {
     const bool w = q < JW;
     const uint8_t* buf = smem + stage * 2 * TILE_BYTES + (w ? TILE_BYTES : 0);
@@ -199,11 +184,6 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
     if (w) fw[q] = v;
     else fa[q - JW] = v;
   };
-  // conversion of dword d (0..4 JW - 1) of the weight fragments (fragment d/4)
-  auto convert_dword = [&](v4u (&fw)[JW], int d) {
-    const uint32_t w = fw[d >> 2][d & 3];
-    fw[d >> 2][d & 3] = pack_f16(__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u));
-  };
   // global->LDS load q (0..2 LOADS - 1) of step kt into a stage: A for even q, W for odd q
   auto load_part = [&](int kt, int stage, int q) {
     uint8_t* buf = smem + stage * 2 * TILE_BYTES + (q & 1) * TILE_BYTES + 1024 * (NW * (q >> 1) + wave);
@@ -211,12 +191,10 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
     __builtin_amdgcn_global_load_lds(src, (lds_ptr)buf, 16, 0, 0);
   };
   // One half step: the SLOTS MFMAs on (fa, fw), the reads of the next fragments
-  // into (na, nw) and their conversion, and optionally the loads of step kt.
-  // Reads go out RPS per slot from slot 0; the 4 JW dword conversions are
-  // spread over slots C0..SLOTS-1.
+  // into (na, nw), RPS per slot from slot 0, and optionally the loads of step kt.
   auto half = [&](const v4u (&fa)[4], const v4u (&fw)[JW], int rstage, int rs, v4u (&na)[4], v4u (&nw)[JW],
                   bool load, int kt, int lstage) {
-    constexpr int RPS = KF_GEMM_READS_PER_SLOT, C0 = KF_GEMM_CVT_SLOT * SLOTS / 16, ND = 4 * JW;
+    constexpr int RPS = KF_GEMM_READS_PER_SLOT;
 #pragma unroll
     for (int q = 0; q < SLOTS; ++q) {
       acc[q / JW][q % JW] = mfma32(fa[q / JW], fw[q % JW], acc[q / JW][q % JW]);
@@ -224,10 +202,6 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
       for (int r = 0; r < RPS; ++r)
         if (q * RPS + r < JW + 4) read_frag(rstage, rs, q * RPS + r, na, nw);
       if (load && q < 2 * LOADS) load_part(kt, lstage, q);
-      if (q >= C0) {
-#pragma unroll
-        for (int d = (q - C0) * ND / (SLOTS - C0); d < (q - C0 + 1) * ND / (SLOTS - C0); ++d) convert_dword(nw, d);
-      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -245,16 +219,15 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
   v4u fa0[4], fw0[JW], fa1[4], fw1[JW];
 #pragma unroll
   for (int q = 0; q < JW + 4; ++q) read_frag(0, 0, q, fa0, fw0);
-#pragma unroll
-  for (int d = 0; d < 4 * JW; ++d) convert_dword(fw0, d);
   for (int k = 0; k + 1 < nk; ++k) {
     __builtin_amdgcn_sched_barrier(0);
     half(fa0, fw0, k % STAGES, 1, fa1, fw1, false, 0, 0);
     // this wave's loads for step k+1 are complete once only the next STAGES-2 steps' remain
     wait_vm<(STAGES - 2) * 2 * LOADS>();
+    wait_lds();  // this wave's reads of stage k % STAGES have returned (issued a half step ago)
     // Every wave's loads for step k+1 have landed and every wave's reads of
-    // stage k % STAGES have returned (they fed the conversions above).  A bare
-    // barrier: a fence here would also drain the loads in flight.
+    // stage k % STAGES have returned.  A bare barrier: a fence here would also
+    // drain the loads in flight.
     block_barrier();
     half(fa1, fw1, (k + 1) % STAGES, 0, fa0, fw0, true, k + STAGES < nk ? k + STAGES : nk - 1, k % STAGES);
   }

@@ -45,7 +45,7 @@ struct Tracer {
 };
 
 enum GemvEpi : int {
-  kEpiQKV = 0,     // RoPE on q and k, q -> fp32 workspace, k and v -> bf16 cache at the row's position
+  kEpiQKV = 0,     // RoPE on q and k, q -> fp32 workspace, k and v -> fp16 cache at the row's position
   kEpiResid = 1,   // x[b][row] += y (fp32 residual stream), optional copy to the hidden output
   kEpiSwiGLU = 2,  // a[b][j] = silu(gate_j) * up_j
   kEpiLMHead = 3,  // optional fp32 logits, per-workgroup (max, lowest index) partials
@@ -56,7 +56,7 @@ enum { kOut2F32 = 0, kOut2BF16 = 1, kOut2F16 = 2 };
 
 // One decode GEMV launch: y[b][n] = sum_k W[n][k] * in[b][k] (* gain[k] * rsqrt(mean(in^2)+eps) if norm).
 struct GemvParams {
-  const uint16_t* w0;  // matrix rows (QKV: [q;k;v] rows; SwiGLU: gate; others: the matrix)
+  const uint16_t* w0;  // fp16 matrix rows (QKV: [q;k;v] rows; SwiGLU: gate; others: the matrix)
   const uint16_t* w1;  // SwiGLU: up rows; unused otherwise
   const uint16_t* gain;  // RMSNorm gain [K] when the launch normalises its input
   const float* in;     // [B][K] fp32
@@ -145,12 +145,15 @@ hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool 
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
 // o16[b][h*hd:(h+1)*hd] (fp16) = head h of row b merged from the attention partials in p.
 hipError_t launch_attn_merge(const AttnParams& p, uint16_t* o16, int batch, hipStream_t s);
-// x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] bf16).
+// x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] fp16).
 hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,
                               float* x, int rows, int H, int* err_flag, hipStream_t s);
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n_wg, int rows, int32_t* token,
                                float* max_logit, hipStream_t s);
+// In place over n elements: bf16 weights to fp16 (round to nearest even); *bad |= 1
+// if a finite weight is beyond the fp16 range.
+hipError_t launch_weights_to_f16(uint16_t* w, int64_t n, int* bad, hipStream_t s);
 hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t n, hipStream_t s);
 // Positions [pos0, pos0 + n) of one user in one layer (k, v: the layer's base)
 // from / to [n][nkv][hd] rows.  src_type: 0 fp32, 1 bf16, 2 fp16 (the kf_dtype values).

@@ -429,6 +429,25 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
     s->part_idx = (int*)take(B * s->lm_wg * 4);
   }
   s->err_flag = (int*)take(4);
+
+  // The matrices are kept in fp16, the type every product here takes (the
+  // matrix cores and the decode GEMVs): converted once, in place.  Gains and the
+  // embedding table stay bf16.
+  {
+    hipError_t e = hipDeviceSynchronize();  // the uploads and the workspace clear ran on the null stream
+    const int64_t mats[5] = {nqkv * H, H * (int64_t)c.n_q_heads * hd, F * H, F * H, H * F};
+    for (int l = 0; l < nl && e == hipSuccess; ++l) {
+      LayerW& L = s->layers[l];
+      uint16_t* ptrs[5] = {L.wqkv, L.wo, L.wg, L.wu, L.wd};
+      for (int m = 0; m < 5 && e == hipSuccess; ++m) e = launch_weights_to_f16(ptrs[m], mats[m], s->err_flag, s->stream);
+    }
+    if (e == hipSuccess && has_head) e = launch_weights_to_f16(s->lm_head, V * H, s->err_flag, s->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    int bad = 0;
+    if (e == hipSuccess) e = hipMemcpy(&bad, s->err_flag, 4, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return cleanup(fail(KF_EDEVICE, "weight conversion: %s", hipGetErrorString(e)));
+    if (bad) return cleanup(fail(KF_EINVAL, "a weight matrix holds a value beyond the fp16 range (|w| >= 65520)"));
+  }
   *out = s;
   clear_error();
   return KF_OK;

@@ -94,3 +94,34 @@ def test_decode_at_the_last_slot_of_the_largest_cache(torch, st, paged):
         g.kv(1, MAX_CTX + 1)
     assert e.value.status == st.KF_ERANGE
     g.close()
+
+
+def test_weight_matrices_beyond_the_fp16_range_are_refused(torch, st):
+    """The stage keeps its matrices in fp16: a finite bf16 weight fp16 cannot hold fails init.
+
+    65280 is the largest bf16 value below the fp16 maximum (65504) and is kept;
+    65536 would become infinite.  Gains stay bf16 and take any finite value.
+    """
+    model = SeededModel(TINY, 41)
+    base = {l: model.layer(l) for l in range(2)}
+
+    def with_value(kind, value, layer=1, at=5):
+        w = base[layer][kind].copy()
+        w.flat[at] = to_bf16(np.array([value]))[0]
+        return {l: ({**base[l], kind: w} if l == layer else base[l]) for l in range(2)}
+
+    for kind in ("wq", "wd"):
+        for v in (65536.0, -1.0e6):
+            with pytest.raises(st.KFError) as e:
+                st.Stage(TINY, 0, 2, with_value(kind, v), None)
+            assert e.value.status == st.KF_EINVAL and "fp16" in e.value.message, (kind, v)
+    head = dict(model.head())
+    lm = head["lm_head"].copy()
+    lm.flat[7] = to_bf16(np.array([1.0e5]))[0]
+    with pytest.raises(st.KFError) as e:
+        st.Stage(TINY, 0, 2, base, {**head, "lm_head": lm})
+    assert e.value.status == st.KF_EINVAL
+    g = st.Stage(TINY, 0, 2, with_value("wu", -65280.0), None)
+    g.close()
+    g = st.Stage(TINY, 0, 2, with_value("mlp_norm", 1.0e6), None)  # a gain: stays bf16
+    g.close()
