@@ -1186,6 +1186,12 @@ hipError_t launch_gemv_src(int epi, int R, int U, bool norm, const GemvParams& p
 hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
   const int grid = gemv_grid(epi, R, p);
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
+  // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
+  // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.
+  if (R == 4 && U == 1 && epi == kEpiQKV && p.batch == 1 && norm && !p.in16) {
+    hipLaunchKernelGGL((gemv_kernel<1, 4, 1, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
+    return hipGetLastError();
+  }
   return hipErrorInvalidValue;
 }
 

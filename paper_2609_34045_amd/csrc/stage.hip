@@ -21,6 +21,7 @@ using namespace kf;
 // Decode GEMVs take 8 output rows per workgroup and one 16-byte chunk per row in
 // flight per thread (other shapes were measured slower at every batch).
 constexpr int kGemvRows = 8, kGemvChunks = 1;
+constexpr int kQkvRowsBatch1 = 4;  // the batch-1 QKV launch (after the first layer) takes 4-row workgroups
 #ifndef KF_ATTN_TARGET_WGS
 #define KF_ATTN_TARGET_WGS 256
 #endif
@@ -788,7 +789,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.in16 = 0;  // the input rows come from src / tokens
       le = launch_gemv_src(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
     } else {
-      le = launch_gemv(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
+      le = launch_gemv(kEpiQKV, batch == 1 ? kQkvRowsBatch1 : kGemvRows, kGemvChunks, true, g, st);
     }
     tr.end(KF_K_QKV);
     KF_HIP(le, "qkv launch");
