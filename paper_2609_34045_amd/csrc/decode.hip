@@ -1183,9 +1183,28 @@ hipError_t launch_gemv_src(int epi, int R, int U, bool norm, const GemvParams& p
   return hipErrorInvalidValue;
 }
 
+// Residual GEMV in workgroups of 4 rows (fp16 inputs from batch 2, as at 8 rows).
+template <int B>
+static hipError_t resid4_launch(const GemvParams& p, int grid, hipStream_t s) {
+  if (B > 1 && p.in16)
+    hipLaunchKernelGGL((gemv_kernel<B, 4, 1, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((gemv_kernel<B, 4, 1, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
   const int grid = gemv_grid(epi, R, p);
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
+  if (R == 4 && U == 1 && epi == kEpiResid && !norm) {
+    switch (p.batch) {
+      case 1: return resid4_launch<1>(p, grid, s);
+      case 2: return resid4_launch<2>(p, grid, s);
+      case 3: return resid4_launch<3>(p, grid, s);
+      case 4: return resid4_launch<4>(p, grid, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
   // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.
   if (R == 4 && U == 1 && epi == kEpiQKV && p.batch == 1 && norm && !p.in16) {
