@@ -113,7 +113,8 @@ const char* kf_last_error(void);
 /*
  * Byte sizes behind the stage-cost model (Section V-A, eq. (2)) and the block
  * limit at a declared context and concurrency (Section V-C).
- *   beta_block : bytes of one decoder layer's weights (bf16, including both gains)
+ *   beta_block : bytes of one decoder layer's weights (2 bytes per element as given in bf16 and as
+ *                held: fp16 matrices, bf16 gains; both gains included)
  *   beta_head  : bytes of the head's weights (embedding + final gain + LM head), 0 without the head
  *   resident   : device bytes kf_stage_init + kf_kv_create(max_users, max_ctx) would hold for
  *                layers [lo, hi): weights, KV cache, RoPE table and decode workspaces
