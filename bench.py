@@ -510,7 +510,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "f16",  # fp16 weight matrices and KV cache, fp32 sums
         "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}) of a {s.n_layers}-layer model, H{s.hidden}, "
