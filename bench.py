@@ -59,6 +59,8 @@ def parse():
     ap.add_argument("--paged", action="store_true",
                     help="decode over a paged KV cache (a pool of 64-position pages shared by the users, the "
                          "contexts injected page by page in turn so that every user's pages are scattered)")
+    ap.add_argument("--ordered", action="store_true",
+                    help="batch-1 decode with the ordered (run-to-run bit-identical) output projection")
     ap.add_argument("--ring", action="store_true",
                     help="the whole 8B-shaped model as a ring of stages on this GPU: four concurrent users "
                          "against one user, in turn, batched, and over 2 and 4 members on their own streams")
@@ -71,7 +73,7 @@ def step_bytes(wl, positions) -> int:
     and with the head the LM head plus the gathered embedding rows."""
     s = wl.shape
     L = wl.layer_hi - wl.layer_lo
-    kv_per_key = 4 * s.n_kv_heads * s.head_dim  # K and V, bf16
+    kv_per_key = 4 * s.n_kv_heads * s.head_dim  # K and V, 2 bytes each (the fp16 cache)
     b = L * s.block_bytes()
     b += sum(L * kv_per_key * (p + 1) for p in positions)  # reads (the new key included)
     b += len(positions) * L * kv_per_key  # appends
@@ -401,6 +403,8 @@ def main():
     log(f"[bench] generated {wl.name} weights in {time.perf_counter() - t0:.1f} s")
     t0 = time.perf_counter()
     g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, head)
+    if args.ordered:
+        g.set_flags(kf.KF_STAGE_ORDERED)
     span = max(args.steps, args.warmup)
     cap = max(ctx) + span + 1
     page = 64

@@ -1,7 +1,7 @@
 /*
  * kafila_planner.h -- the planner of Kafila (arxiv 2609.34045, Section V): the
  * stage-cost model, exact block placement, head placement by rotation,
- * admission, the two baseline divisions of Section VI-B, and the device probes
+ * admission, the two baseline divisions that open Section VII, and the device probes
  * that supply the cost model's measured terms.
  *
  * Members of a ring are numbered 0..m-1 in ring order; member `anchor` opened
@@ -84,7 +84,7 @@ kf_status kf_partition(int32_t k, int32_t m, const double* fixed, const double* 
 kf_status kf_place_head(int32_t k, int32_t m, const kf_member* members, const kf_model_costs* costs,
                         int32_t anchor, double mu, int32_t* head, int32_t* n, double* tau);
 
-/* Section VI-B baselines.  Uniform: k / m blocks each, one more for the first k % m
+/* The baselines that open Section VII.  Uniform: k / m blocks each, one more for the first k % m
  * members.  Memory-proportional: the boundary after member i (ring order from
  * member 0) at floor(k * (room_0 + .. + room_i) / (total room) + 1/2); a member
  * may get 0 blocks.  KF_EINVAL for k < 1, m < 1, NULL, a negative room or a zero total. */

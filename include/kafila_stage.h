@@ -41,8 +41,10 @@
 extern "C" {
 #endif
 
-#define KF_ABI_VERSION 3  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds;
-                            3: paged KV caches, kf_stage_describe, kf_kv_describe */
+#define KF_ABI_VERSION 4  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds;
+                            3: paged KV caches, kf_stage_describe, kf_kv_describe;
+                            4: kf_stage_set_flags / kf_stage_get_flags (KF_STAGE_ORDERED), range and
+                               NaN-logit errors reported by kf_stage_sync, token -1 for a row of NaN logits */
 #define KF_KV_PAGE 64     /* positions per KV cache page */
 #define KF_MAX_BATCH 4
 
@@ -126,7 +128,9 @@ kf_status kf_stage_bytes(const kf_model_config* cfg, int32_t layer_lo, int32_t l
 
 /*
  * Create a stage holding layers [layer_lo, layer_hi) of the model and, if has_head,
- * the head.  Weight tensors are copied to the current HIP device (the stage's
+ * the head (Section III and Fig. 1: a member's contiguous block range, and the
+ * head's embedding and unembedding on the member the rotation makes head;
+ * Section V-C places it).  Weight tensors are copied to the current HIP device (the stage's
  * device) before the call returns, so the caller may free them afterwards.  Every
  * layer tensor of every held layer must be present exactly once (kinds 0..8, plus
  * KF_W_Q_NORM and KF_W_K_NORM when qk_norm), plus the three head tensors when
@@ -146,8 +150,36 @@ kf_status kf_stage_destroy(kf_stage* stage);
 /* Replace the stream later work is enqueued on (the caller orders it after earlier work). */
 kf_status kf_stage_set_stream(kf_stage* stage, void* hip_stream);
 
-/* Wait for all enqueued work; KF_EDEVICE (with the HIP error text) if any of it failed. */
+/*
+ * Wait for all enqueued work; KF_EDEVICE (with the HIP error text) if any of it failed.
+ * Then reports, and clears, the stage's sticky data errors raised by enqueued work:
+ *   KF_EINVAL : a token id given to decode or prefill was outside [0, vocab); that row's
+ *               hidden state was set to NaN;
+ *   KF_ERANGE : a value the stage holds in fp16 (keys and values in the cache, and the
+ *               fp16 activations: from batch 2 the decode residual copy, SwiGLU output and
+ *               merged attention output; in prefill the normalised rows, queries, attention
+ *               output and SwiGLU output) reached 65520 in magnitude and was stored as
+ *               infinity; or a logit was NaN (skipped by the argmax; see kf_head_argmax).
+ * The message (kf_last_error) names every condition that occurred.
+ */
 kf_status kf_stage_sync(kf_stage* stage);
+
+/*
+ * Behaviour flags of a stage (0 after kf_stage_init).
+ *   KF_STAGE_ORDERED : batch-1 decode adds the query heads' output projections to each
+ *                      residual row in a fixed order (a separate merge of the split-KV
+ *                      partials, then a row-owning output GEMV), so that repeated runs are
+ *                      bit-identical and a stage split anywhere composes to the same bits.
+ *                      Without it, batch 1 fuses the merge into a head-split output
+ *                      projection whose fp32 additions arrive in any order (one launch
+ *                      fewer per layer; results vary run to run by fp32 reassociation).
+ *                      Greedy decoding at a fixed seed (Section VI-A) reproduces exactly
+ *                      only with this flag.  Batch 2-4 and prefill are always in fixed order.
+ * kf_stage_set_flags: KF_EINVAL for unknown bits.  Host-only; affects later calls.
+ */
+#define KF_STAGE_ORDERED 1
+kf_status kf_stage_set_flags(kf_stage* stage, int32_t flags);
+kf_status kf_stage_get_flags(const kf_stage* stage, int32_t* flags);
 
 /* What a stage holds: its config, layer range [layer_lo, layer_hi), whether it holds
  * the head, the stream it enqueues on (a hipStream_t) and its device ordinal.  Any
@@ -213,7 +245,12 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
                      float* v_dev);
 
 /*
- * Forward one token for each of `batch` (1..KF_MAX_BATCH) users (decode).
+ * Forward one token for each of `batch` (1..KF_MAX_BATCH) users (decode): the
+ * stage's part of one decode step, hidden state in, hidden state out (Section III:
+ * the token's hidden state passes through each member's block range around the
+ * ring; the head member embeds it first).  Its cost is one read of every held
+ * weight plus each user's cache (Section V-A, eq. (2)); batch > 1 serves several
+ * users' requests in one pass over the weights (Sections III and VII-C).
  *   users[b], positions[b] : host arrays; users distinct and < max_users;
  *                            positions[b] must equal the user's current length
  *                            (append-only; else KF_EINVAL) and be < max_ctx (else KF_ERANGE).
@@ -231,8 +268,10 @@ kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32
                           void* hidden_out_dev, kf_dtype io);
 
 /*
- * Forward a chunk of n_tokens consecutive tokens of one user starting at pos0 (prefill).
- * pos0 must equal the user's length and pos0 + n_tokens <= max_ctx.  Token i attends
+ * Forward a chunk of n_tokens consecutive tokens of one user starting at pos0 (prefill:
+ * the prompt phase of a request, which the paper separates from decode in its
+ * time-to-first-token accounting, Section VI; the per-user cache it fills is the
+ * reservation of Section V-C).  pos0 must equal the user's length and pos0 + n_tokens <= max_ctx.  Token i attends
  * slots 0..pos0+i.  tokens_dev int32 [n] or hidden_in_dev [n, H]; hidden_out_dev [n, H].
  * A paged cache lends the pages up to pos0 + n (KF_ENOMEM if it cannot).
  * Dense products run on the matrix cores with fp16 operands (the stage's fp16 weights)
@@ -243,11 +282,23 @@ kf_status kf_stage_prefill(kf_stage* stage, kf_kv* kv, int32_t user, int32_t pos
                            const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev,
                            kf_dtype io);
 
-/* logits_dev fp32 [rows, V] = RMSNorm(hidden; final gain) x LM_head^T.  Head stages only (else KF_ESTATE). */
+/*
+ * The head's unembedding (Section III and Fig. 1: the head member holds the
+ * embedding and unembedding and samples after the model's last block):
+ * logits_dev fp32 [rows, V] = RMSNorm(hidden; final gain) x LM_head^T, for hidden_dev
+ * [rows, H] in dtype (KF_F32 or KF_BF16), any rows >= 1.  Head stages only (else KF_ESTATE).
+ */
 kf_status kf_head_logits(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype, float* logits_dev);
 
-/* token_dev int32 [rows] = greedy argmax of the logits (lowest index on ties);
- * max_logit_dev fp32 [rows] (may be NULL) receives the winning logit.  rows <= KF_MAX_BATCH. */
+/*
+ * The head's sampler: greedy decoding (Section VI-A decodes greedily at a fixed
+ * seed).  token_dev int32 [rows] = argmax over the vocabulary of the logits of
+ * kf_head_logits, the lowest index winning exact ties; max_logit_dev fp32 [rows]
+ * (may be NULL) receives the winning logit.  A NaN logit is skipped and raises the
+ * stage's NaN-logit error (KF_ERANGE from kf_stage_sync); a row whose logits are all
+ * NaN gives token -1 and max logit NaN.  rows in [1, KF_MAX_BATCH] (else KF_EINVAL).
+ * Head stages only (else KF_ESTATE).
+ */
 kf_status kf_head_argmax(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype,
                          int32_t* token_dev, float* max_logit_dev);
 

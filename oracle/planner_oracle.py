@@ -7,7 +7,7 @@ of a ring in a fixed order so that the slowest stage is as fast as possible
 tries each member as the head by rotating the order and keeps the session's
 anchor unless another choice is better by a margin mu (Section V-C), degrades
 through three tiers of information and finally admits or rejects the division
-against every member's memory (Section V-D).  Section VI-B's baselines divide
+against every member's memory (Section V-D).  The baselines that open Section VII divide
 evenly (Uniform) or by working set (Memory-proportional).
 
 This module writes each of those out in the most direct way:
@@ -152,12 +152,12 @@ def place_head(k: int, devices, costs, anchor: int, mu: float):
 
 
 def uniform(k: int, m: int):
-    """Section VI-B's Uniform baseline (GPipe's equal block count)."""
+    """The Uniform baseline of Section VII's opening (GPipe's equal block count)."""
     return [k // m + (1 if i < k % m else 0) for i in range(m)]
 
 
 def memory_proportional(k: int, rooms):
-    """Section VI-B's Memory-proportional baseline: shares proportional to working set."""
+    """The Memory-proportional baseline of Section VII's opening: shares proportional to working set."""
     total = 0
     for r in rooms:
         total += r
@@ -214,7 +214,7 @@ def plan(k: int, devices, costs, anchor: int, mu: float):
 
 
 def bottleneck_stats(costs_per_stage):
-    """Section VI-B's table columns: imbalance (max/min), bottleneck, utilisation (mean/max)."""
+    """The columns of Section VII-B's table: imbalance (max/min), bottleneck, utilisation (mean/max)."""
     hi, lo = max(costs_per_stage), min(costs_per_stage)
     mean = sum(costs_per_stage) / len(costs_per_stage)
     return dict(imbalance=hi / lo, bottleneck=hi, utilisation=mean / hi)

@@ -65,10 +65,6 @@ __device__ __forceinline__ void f16x8(const v4u w, float (&f)[8]) {
   for (int i = 0; i < 8; ++i) f[i] = v[i];
 }
 
-#ifndef KF_GEMV_DOT
-#define KF_GEMV_DOT 0xF  // GEMV epilogues (bit per GemvEpi) whose fp16-input launches use packed dot products
-#endif
-
 // As f16x8, for products against fp32 inputs at batch > 1: the empty asm keeps
 // the conversions separate instructions, since folding each into every row's
 // FMA (a mixed-precision FMA per product) is several times slower.
@@ -80,9 +76,6 @@ __device__ __forceinline__ void f16x8_apart(const v4u w, float (&f)[8]) {
 
 // fp32 to fp16 bits, round to nearest even.
 __device__ __forceinline__ uint16_t f32_to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
-__device__ __forceinline__ uint32_t f16_pair(float lo, float hi) {
-  return (uint32_t)f32_to_f16(lo) | ((uint32_t)f32_to_f16(hi) << 16);
-}
 
 // Round to nearest even; NaN stays NaN.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
@@ -213,12 +206,15 @@ __device__ __forceinline__ EpiPre gemv_epi_prefetch(const GemvParams& p, int wg,
   return e;
 }
 
+constexpr int kNoRow = 0x7fffffff;  // argmax partial of a workgroup whose logits were all NaN
+
 // Epilogue of a workgroup's R x B dot products fin[r * B + b] (plus, when the
 // launch normalises its input, fin[R * B + b] = sum of x_b^2 over K).  Runs
 // on the T threads (index tid) that own the group, after fin is complete.
 template <int B, int R, int EPI, bool NORM, int T>
 __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const float* fin, int tid,
                                               const EpiPre& pre) {
+  bool bad = false;  // an fp16 store out of range
   float rs[B];
 #pragma unroll
   for (int b = 0; b < B; ++b) rs[b] = NORM ? 1.0f / sqrtf(fin[R * B + b] / (float)p.K + p.eps) : 1.0f;
@@ -244,13 +240,13 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
           q[i + half] = z2;
         } else {
           uint16_t* k = p.kc + kv_offset(p.kv, p.users[b], head - p.nq, pos, hd);
-          k[i] = f32_to_f16(z1);
-          k[i + half] = f32_to_f16(z2);
+          k[i] = f16_checked(z1, bad);
+          k[i + half] = f16_checked(z2, bad);
         }
       } else {
         uint16_t* v = p.vc + kv_offset(p.kv, p.users[b], head - p.nq - p.nkv, pos, hd);
-        v[i] = f32_to_f16(y1);
-        v[i + half] = f32_to_f16(y2);
+        v[i] = f16_checked(y1, bad);
+        v[i + half] = f16_checked(y2, bad);
       }
     }
   } else if (EPI == kEpiResid) {
@@ -263,7 +259,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
         p.x[at] = v;
         if (p.out2) {
           if (p.out2_type == kOut2F32) reinterpret_cast<float*>(p.out2)[at] = v;
-          else reinterpret_cast<uint16_t*>(p.out2)[at] = p.out2_type == kOut2BF16 ? f32_to_bf16(v) : f32_to_f16(v);
+          else reinterpret_cast<uint16_t*>(p.out2)[at] = p.out2_type == kOut2BF16 ? f32_to_bf16(v) : f16_checked(v, bad);
         }
       }
     }
@@ -274,7 +270,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       const float up = fin[(r + R / 2) * B + b] * rs[b];
       const float a = gt / (1.0f + expf(-gt)) * up;
       const int64_t at = (int64_t)b * p.N + wg * (R / 2) + r;
-      if (p.act16) reinterpret_cast<uint16_t*>(p.act)[at] = f32_to_f16(a);
+      if (p.act16) reinterpret_cast<uint16_t*>(p.act)[at] = f16_checked(a, bad);
       else p.act[at] = a;
     }
   } else {  // kEpiLMHead
@@ -285,20 +281,27 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       }
     }
     if (tid < B) {
+      // (max, lowest row) over the workgroup's rows; a NaN logit is skipped and
+      // reported, and a workgroup of NaN rows leaves (-inf, kNoRow)
       const int b = tid;
-      float best = fin[b] * rs[b];
-      int bidx = wg * R;
-      for (int r = 1; r < R; ++r) {
+      float best = -INFINITY;
+      int bidx = kNoRow;
+      bool nan = false;
+      for (int r = 0; r < R; ++r) {
         const float v = fin[r * B + b] * rs[b];
-        if (wg * R + r < p.N && v > best) {  // strict: the lower row keeps a tie
+        if (wg * R + r >= p.N) break;
+        if (v != v) nan = true;
+        else if (v > best || bidx == kNoRow) {  // strict: the lower row keeps a tie
           best = v;
           bidx = wg * R + r;
         }
       }
       p.part_val[(int64_t)b * p.n_wg + wg] = best;
       p.part_idx[(int64_t)b * p.n_wg + wg] = bidx;
+      raise_err(p.err_flag, nan, kErrNaNLogit);
     }
   }
+  raise_err(p.err_flag, bad, kErrF16Range);
 }
 
 // Vector-ALU GEMV: each thread multiplies its 16-byte weight chunks by the
@@ -356,7 +359,8 @@ void gemv_kernel(const GemvParams p) {
 #pragma unroll
   for (int r = 0; r < R; ++r) wrow[r] = reinterpret_cast<const v4u*>(gemv_row<R, EPI>(p, wg, r, rok[r]));
   const EpiPre pre = gemv_epi_prefetch<B, R, EPI>(p, wg, tid);
-  if (SRC && wg == 0 && p.tokens && tid < B && (p.tokens[tid] < 0 || p.tokens[tid] >= p.vocab)) atomicOr(p.err_flag, 1);
+  if (SRC && wg == 0 && p.tokens && tid < B && (p.tokens[tid] < 0 || p.tokens[tid] >= p.vocab))
+    atomicOr(p.err_flag, kErrToken);
 
   float acc[NVP];
 #pragma unroll
@@ -369,7 +373,13 @@ void gemv_kernel(const GemvParams p) {
   constexpr bool kInputFirst = B > 1 || EPI == kEpiQKV;
   // fp16 inputs (batch 2-4) meet the fp16 weights in packed dot products: two
   // products per instruction, summed in fp32.
-  constexpr bool kDot = IN16 && !SRC && ((KF_GEMV_DOT >> EPI) & 1);
+  constexpr bool kDot = IN16 && !SRC;
+  // From batch 2 the first layer's QKV launch rounds the stage input to fp16, as
+  // the residual copy every later layer's QKV launch reads was rounded, and takes
+  // the same packed products: a layer's result then does not depend on whether
+  // it starts the stage (a stage split anywhere composes to the same output).
+  constexpr bool kDotSrc = SRC && B > 1 && EPI == kEpiQKV;
+  bool bad_in = false;  // a stage input value beyond the fp16 range (kDotSrc)
   for (int c0 = tid; c0 < nch; c0 += T * U) {
     v4f xl[U][B], xh[U][B];
     v4u xr[U][B];
@@ -425,11 +435,23 @@ void gemv_kernel(const GemvParams p) {
             reinterpret_cast<v4f*>(p.x_init + (int64_t)b * K + c * 8)[1] = xh[u][b];
           }
         }
-        if constexpr (kDot) {
+        if constexpr (kDot || kDotSrc) {
           // input pairs in fp16; with the norm, x * gain rounded to fp16 (sum(x^2) in fp32)
           h2 xp[B][4];
           float gf[8];
           if (NORM) bf16x8(gv[u], gf);
+          if constexpr (kDotSrc) {
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+              const v4f lo = xl[u][b], hi = xh[u][b];
+              const float xs[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+              uint16_t x16[8];
+#pragma unroll
+              for (int i = 0; i < 8; ++i) x16[i] = f16_checked(xs[i], bad_in);
+              xr[u][b] = v4u{x16[0] | ((uint32_t)x16[1] << 16), x16[2] | ((uint32_t)x16[3] << 16),
+                             x16[4] | ((uint32_t)x16[5] << 16), x16[6] | ((uint32_t)x16[7] << 16)};
+            }
+          }
 #pragma unroll
           for (int b = 0; b < B; ++b) {
             if (NORM) {
@@ -497,6 +519,7 @@ void gemv_kernel(const GemvParams p) {
     }
   }
 
+  if (kDotSrc) raise_err(p.err_flag, bad_in && wg == 0, kErrF16Range);
   Butterfly<NVP, 32>::run(acc, lane);
   __shared__ float red[4][NVP];
   __shared__ float fin[NVP];
@@ -663,9 +686,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
       bf16x8(kgain, gkf);
       norm_rope(x, gkf);
       if (kgrp == 0) {
-        const v4u kv16 = v4u{f16_pair(x[0], x[1]), f16_pair(x[2], x[3]), f16_pair(x[4], x[5]), f16_pair(x[6], x[7])};
+        bool bad = false;
+        uint16_t k16[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) k16[i] = f16_checked(x[i], bad);
+        const v4u kv16 = v4u{k16[0] | ((uint32_t)k16[1] << 16), k16[2] | ((uint32_t)k16[3] << 16),
+                             k16[4] | ((uint32_t)k16[5] << 16), k16[6] | ((uint32_t)k16[7] << 16)};
         *reinterpret_cast<v4u*>(p.kc + kv_offset(p.kv, u, g, npos, HD) + d0) = kv16;
         *reinterpret_cast<v4u*>(&knew[d0]) = kv16;
+        raise_err(p.err_flag, bad, kErrF16Range);
       }
     }
     __syncthreads();
@@ -803,9 +832,11 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 // vectors summed and divided by the weighted partial sums.  The split weights are
 // computed by all threads at once and kept in LDS; then each wave sums every
 // fourth split's vector (independent loads) and the four sums are combined.  The
-// result goes out in fp16 for the output projection's GEMV (batch > 1).
+// result goes out for the output projection's GEMV: in fp16 (o16, batch > 1) or
+// fp32 (o32, the batch-1 launch sequence that adds the heads in a fixed order).
 template <int HD>
-__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams a, uint16_t* __restrict__ o16) {
+__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams a, uint16_t* __restrict__ o16,
+                                                         float* __restrict__ o32) {
   constexpr int DPL = HD / 64;
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ns = a.n_split;
@@ -848,12 +879,16 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams a, uin
   __syncthreads();
   if (wave == 0) {
     const float inv = 1.0f / ((sL[0] + sL[1]) + (sL[2] + sL[3]));  // every row has at least one key
-    uint16_t* dst = o16 + ((int64_t)b * a.nq + h) * HD + lane * DPL;
+    const int64_t at = ((int64_t)b * a.nq + h) * HD + lane * DPL;
+    bool bad = false;
 #pragma unroll
     for (int i = 0; i < DPL; ++i) {
       const int d = lane * DPL + i;
-      dst[i] = f32_to_f16(((red[0][d] + red[1][d]) + (red[2][d] + red[3][d])) * inv);
+      const float v = ((red[0][d] + red[1][d]) + (red[2][d] + red[3][d])) * inv;
+      if (o16) o16[at + i] = f16_checked(v, bad);
+      else o32[at + i] = v;
     }
+    raise_err(a.err_flag, bad, kErrF16Range);
   }
 }
 
@@ -997,7 +1032,7 @@ __global__ void prep_hidden_kernel(const void* __restrict__ in, int in_bf16, con
   if (tokens) {
     const int tok = tokens[row];
     if (tok < 0 || tok >= vocab) {
-      if (k == 0) atomicOr(err_flag, 1);
+      if (k == 0) atomicOr(err_flag, kErrToken);
       const float qn = __uint_as_float(0x7fc00000u);
       v = v4f{qn, qn, qn, qn};
     } else {
@@ -1032,7 +1067,7 @@ __global__ __launch_bounds__(1024) void argmax_final_kernel(const float* part_va
   const float* pv = part_val + (int64_t)b * n_wg;
   const int* pi = part_idx + (int64_t)b * n_wg;
   float best = -INFINITY;
-  int bidx = 0x7fffffff;
+  int bidx = kNoRow;
   for (int i0 = tid; i0 < n_wg; i0 += T * U) {
     float v[U];
     int ix[U];
@@ -1040,7 +1075,7 @@ __global__ __launch_bounds__(1024) void argmax_final_kernel(const float* part_va
     for (int u = 0; u < U; ++u) {
       const int i = i0 + u * T;
       v[u] = i < n_wg ? pv[i] : -INFINITY;
-      ix[u] = i < n_wg ? pi[i] : 0x7fffffff;
+      ix[u] = i < n_wg ? pi[i] : kNoRow;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) argmax_take(v[u], ix[u], best, bidx);
@@ -1056,12 +1091,12 @@ __global__ __launch_bounds__(1024) void argmax_final_kernel(const float* part_va
   __syncthreads();
   if (wave == 0) {
     best = lane < T / 64 ? sv[lane] : -INFINITY;
-    bidx = lane < T / 64 ? si[lane] : 0x7fffffff;
+    bidx = lane < T / 64 ? si[lane] : kNoRow;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) argmax_take(__shfl_xor(best, o), __shfl_xor(bidx, o), best, bidx);
     if (lane == 0) {
-      token[b] = bidx;
-      if (max_logit) max_logit[b] = best;
+      token[b] = bidx == kNoRow ? -1 : bidx;  // -1: every logit of the row was NaN (kErrNaNLogit is raised)
+      if (max_logit) max_logit[b] = bidx == kNoRow ? __builtin_nanf("") : best;
     }
   }
 }
@@ -1259,11 +1294,11 @@ static hipError_t oproj_dispatch(const AttnParams& a, const uint16_t* w, float* 
   return hipGetLastError();
 }
 
-hipError_t launch_attn_merge(const AttnParams& a, uint16_t* o16, int batch, hipStream_t s) {
-  if (batch < 1 || batch > kMaxBatch) return hipErrorInvalidValue;
+hipError_t launch_attn_merge(const AttnParams& a, uint16_t* o16, float* o32, int batch, hipStream_t s) {
+  if (batch < 1 || batch > kMaxBatch || (o16 == nullptr) == (o32 == nullptr)) return hipErrorInvalidValue;
   const dim3 grid(a.nq, batch);
-  if (a.hd == 128) hipLaunchKernelGGL(attn_merge_kernel<128>, grid, dim3(256), 0, s, a, o16);
-  else if (a.hd == 64) hipLaunchKernelGGL(attn_merge_kernel<64>, grid, dim3(256), 0, s, a, o16);
+  if (a.hd == 128) hipLaunchKernelGGL(attn_merge_kernel<128>, grid, dim3(256), 0, s, a, o16, o32);
+  else if (a.hd == 64) hipLaunchKernelGGL(attn_merge_kernel<64>, grid, dim3(256), 0, s, a, o16, o32);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -17,13 +17,10 @@
 //     MFMAs of the current one run;
 //   * narrow projections (few 256-wide column tiles) are split along K over
 //     several workgroups so that the grid covers the 256 CUs; the slices are
-//     either stored whole for the consuming kernel to add in order
-//     (kGemmPartialF32) or added with fp32 atomics.
+//     stored whole for the consuming kernel to add in order (kGemmPartialF32).
 // Operand fragment layout of v_mfma_f32_32x32x16_f16 (lane l of 64):
 //   A: row l%32, k = 8*(l/32) .. +7      B: column l%32, k = 8*(l/32) .. +7
 //   D: element v (0..15) at row 8*(v/4) + 4*(l/32) + v%4, column l%32
-#include <type_traits>
-
 #include "kernels.h"
 #include "prefill.h"
 
@@ -46,9 +43,6 @@ constexpr int kGemmThreads = 128 * kGemmWN;
 #ifndef KF_GEMM_READS_PER_SLOT
 #define KF_GEMM_READS_PER_SLOT 1  // fragment reads issued per MFMA slot
 #endif
-#ifndef KF_GEMM_STAGGER
-#define KF_GEMM_STAGGER 1  // rotate the split-K atomic epilogue per K slice
-#endif
 #ifndef KF_GEMM_SPLIT_FLOOR
 #define KF_GEMM_SPLIT_FLOOR 1  // K slices per tile: floor (1) or ceiling (0) of 256 / tiles
 #endif
@@ -60,7 +54,6 @@ static_assert(STAGES >= 3 && STAGES <= 5, "ring depth");
 constexpr int TILE_BYTES = BM * BK * 2;     // one operand's tile per stage (16 KB)
 constexpr int ROW_BYTES = BK * 2;           // 64 B: four 16-byte chunks per tile row
 
-__device__ __forceinline__ uint16_t to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
 __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b), c, 0, 0, 0);
 }
@@ -94,9 +87,10 @@ struct Params {
   const uint16_t* W;
   const uint16_t* W2;
   int M, N, K;
-  int splitk;  // K slices (1: plain store / read-modify-write epilogue)
+  int splitk;  // K slices (1: read-modify-write or SwiGLU epilogue)
   float* C;
   uint16_t* Cb;
+  int* err_flag;
 };
 
 template <int EPI>
@@ -241,38 +235,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
 
   // Epilogue.
   const int rq = 4 * (lane >> 5);
-  if ((EPI == kGemmStoreF32 || EPI == kGemmResidF32) && p.splitk > 1) {
-    // K slices of one tile finish together: each starts its atomic additions
-    // at a different row block so that they do not queue on the same lines.
-    auto atomic_epilogue = [&](auto rot_c) {
-      constexpr int ROT = decltype(rot_c)::value;
-#pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int i = (ii + ROT) & 3;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 128 + 32 * i + 8 * (v >> 2) + rq + (v & 3);
-          if (row >= p.M) continue;
-#pragma unroll
-          for (int j = 0; j < JW; ++j) {
-            const int col = n0 + wn * (32 * JW) + 32 * j + rl;
-            if (col < p.N) atomicAdd(p.C + (int64_t)row * p.N + col, acc[i][j][v]);
-          }
-        }
-      }
-    };
-#if KF_GEMM_STAGGER
-    switch (ks & 3) {
-      case 0: atomic_epilogue(std::integral_constant<int, 0>()); break;
-      case 1: atomic_epilogue(std::integral_constant<int, 1>()); break;
-      case 2: atomic_epilogue(std::integral_constant<int, 2>()); break;
-      default: atomic_epilogue(std::integral_constant<int, 3>()); break;
-    }
-#else
-    atomic_epilogue(std::integral_constant<int, 0>());
-#endif
-    return;
-  }
+  bool bad = false;  // an fp16 SwiGLU output out of range
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -285,7 +248,7 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
           const int j = (n0 >> 1) + wn * (16 * JW) + 32 * jj + rl;
           if (j < (p.N >> 1)) {
             const float g = acc[i][2 * jj][v], u = acc[i][2 * jj + 1][v];
-            p.Cb[(int64_t)row * (p.N >> 1) + j] = to_f16(g / (1.0f + expf(-g)) * u);
+            p.Cb[(int64_t)row * (p.N >> 1) + j] = f16_checked(g / (1.0f + expf(-g)) * u, bad);
           }
         }
       } else {
@@ -295,17 +258,12 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
           if (col >= p.N) continue;
           float* c = p.C + (int64_t)row * p.N + col;
           if (EPI == kGemmResidF32) *c += acc[i][j][v];
-          else if (EPI == kGemmPartialF32) c[(int64_t)ks * p.M * p.N] = acc[i][j][v];
-          else *c = acc[i][j][v];
+          else c[(int64_t)ks * p.M * p.N] = acc[i][j][v];
         }
       }
     }
   }
-}
-
-__global__ void zero_f32_kernel(float* p, int64_t n) {
-  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0.f;
+  if (EPI == kGemmSwiGLU) raise_err(p.err_flag, bad, kErrF16Range);
 }
 
 }  // namespace
@@ -314,8 +272,7 @@ __global__ void zero_f32_kernel(float* p, int64_t n) {
 #define KF_GEMM_MAX_SPLIT 8  // upper bound on K slices per output tile
 #endif
 
-int gemm_splitk(int epi, int M, int N, int K) {
-  if (epi == kGemmSwiGLU) return 1;  // the nonlinearity needs complete sums
+int gemm_splitk(int M, int N, int K) {
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const int nk = K / BK;
   if (tiles >= 192 || nk < 128) return 1;  // enough tiles, or a short (cheap) reduction
@@ -326,19 +283,13 @@ int gemm_splitk(int epi, int M, int N, int K) {
 }
 
 hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
-                       float* C, uint16_t* Cb, hipStream_t s) {
+                       float* C, uint16_t* Cb, int* err_flag, hipStream_t s) {
   if (M <= 0 || N <= 0 || K <= 0 || K % BK) return hipErrorInvalidValue;
   if (epi == kGemmSwiGLU && N % 2) return hipErrorInvalidValue;
-  Params p{A, W, W2, M, N, K, gemm_splitk(epi, M, N, K), C, Cb};
-  if (epi == kGemmStoreF32 && p.splitk > 1) {
-    const int64_t n = (int64_t)M * N;
-    hipLaunchKernelGGL(zero_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, C, n);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  // the nonlinearity and the residual update need complete sums: only the partial epilogue splits K
+  Params p{A, W, W2, M, N, K, epi == kGemmPartialF32 ? gemm_splitk(M, N, K) : 1, C, Cb, err_flag};
   const int grid = ((M + BM - 1) / BM) * ((N + BN - 1) / BN) * p.splitk;
   switch (epi) {
-    case kGemmStoreF32: hipLaunchKernelGGL(gemm256_kernel<kGemmStoreF32>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
     case kGemmResidF32: hipLaunchKernelGGL(gemm256_kernel<kGemmResidF32>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
     case kGemmSwiGLU: hipLaunchKernelGGL(gemm256_kernel<kGemmSwiGLU>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;
     case kGemmPartialF32: hipLaunchKernelGGL(gemm256_kernel<kGemmPartialF32>, dim3(grid), dim3(kGemmThreads), 0, s, p); break;

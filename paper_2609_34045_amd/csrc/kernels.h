@@ -13,6 +13,23 @@ constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound
 constexpr int kOprojRows = 256;     // output rows per workgroup of the head-split output projection
 constexpr int kAttnMaxSplitCount = 1024;  // split-KV workgroups per (row, KV head), upper bound
 
+// Bits of the stage's sticky device error flag (reported and cleared by kf_stage_sync).
+enum : int {
+  kErrToken = 1,      // a token id outside [0, vocab): its hidden row became NaN
+  kErrF16Range = 2,   // an activation, key or value stored in fp16 was at or beyond 65520 in magnitude
+  kErrNaNLogit = 4,   // a logit was NaN (the argmax skips it; a row of NaN gives token -1)
+};
+
+// fp32 to fp16 bits (round to nearest even), noting in `bad` a value that fp16
+// cannot hold (|v| >= 65520 rounds to infinity; an infinite input counts too).
+__device__ __forceinline__ uint16_t f16_checked(float v, bool& bad) {
+  bad |= __builtin_fabsf(v) >= 65520.0f;
+  return __builtin_bit_cast(uint16_t, (_Float16)v);
+}
+__device__ __forceinline__ void raise_err(int* flag, bool bad, int bit) {
+  if (bad && flag) atomicOr(flag, bit);
+}
+
 // KV cache pages.  One layer's K (and, alike, V) is an array of pages of kKvPage
 // positions, each page [kv_head][kKvPage][hd] fp16.  Position t of user u lies
 // at slot t % kKvPage of the page with id table[u * ppu + t / kKvPage] (a paged
@@ -99,7 +116,7 @@ struct GemvParams {
   const uint16_t* embed;
   int vocab;
   float* x_init;           // optional [B][K]: workgroup 0 stores the input rows here (residual stream)
-  int* err_flag;           // bit 1 set for a token outside [0, vocab) (its row becomes NaN)
+  int* err_flag;           // sticky error bits (kErrToken, kErrF16Range, kErrNaNLogit); every launch sets it
 
   // kEpiLMHead
   float* logits;       // optional [B][N]
@@ -134,6 +151,7 @@ struct AttnParams {
   const float* rope_cos;  // [max_ctx][hd/2]
   const float* rope_sin;
   float eps;
+  int* err_flag;          // sticky error bits: kErrF16Range for an fp16 store out of range
 };
 
 // Launchers (return hipGetLastError() of the launch).
@@ -143,8 +161,9 @@ hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
-// o16[b][h*hd:(h+1)*hd] (fp16) = head h of row b merged from the attention partials in p.
-hipError_t launch_attn_merge(const AttnParams& p, uint16_t* o16, int batch, hipStream_t s);
+// Head h of row b merged from the attention partials in p, to o16[b][h*hd:(h+1)*hd]
+// (fp16) or, with o16 NULL, to o32[b][h*hd:(h+1)*hd] (fp32).
+hipError_t launch_attn_merge(const AttnParams& p, uint16_t* o16, float* o32, int batch, hipStream_t s);
 // x[b][0:N) += W_o o_b with o_b merged from the attention partials in p (W_o [N][nq*hd] fp16).
 hipError_t launch_oproj_heads(const AttnParams& p, const uint16_t* w, float* x, int N, int batch, hipStream_t s);
 hipError_t launch_prep_hidden(const void* in, int in_bf16, const int32_t* tokens, const uint16_t* embed, int vocab,

@@ -1,6 +1,6 @@
 // The planner behind include/kafila_planner.h (paper Section V): eq. (2), the
 // exact chain-on-chain division of Algorithm 1, head placement by rotation,
-// the admission tiers and the Section VI-B baselines.  Host-only.
+// the admission tiers and the baselines that open Section VII.  Host-only.
 #include <algorithm>
 #include <cmath>
 #include <vector>

@@ -16,6 +16,7 @@ struct PrefillArgs {
   KvPages kv;
   const float* rope_cos;  // [max_ctx][hd/2]
   const float* rope_sin;
+  int* err_flag;  // sticky error bits (kErrF16Range for an fp16 activation, key or value out of range)
   hipStream_t stream;
 };
 
@@ -46,11 +47,13 @@ void prefill_free(PrefillWorkspace& ws);
 hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr);
 
 // Matrix-core GEMM of the prefill projections (gemm.hip).
-// kGemmPartialF32 writes K slice ks to C + ks*M*N (plain stores); the consumer
-// adds the gemm_splitk(kGemmPartialF32, ...) slices in order.
-enum GemmEpi : int { kGemmStoreF32 = 0, kGemmResidF32 = 1, kGemmSwiGLU = 2, kGemmPartialF32 = 3 };
-int gemm_splitk(int epi, int M, int N, int K);
+//   kGemmResidF32   C[M][N] += A W^T (unsplit; the residual stream)
+//   kGemmSwiGLU     Cb[M][N/2] = silu(gate) * up in fp16, W the gate rows and W2 the up rows
+//   kGemmPartialF32 K slice ks to C + ks*M*N (plain stores); the consumer adds the
+//                   gemm_splitk(M, N, K) slices in order
+enum GemmEpi : int { kGemmResidF32 = 1, kGemmSwiGLU = 2, kGemmPartialF32 = 3 };
+int gemm_splitk(int M, int N, int K);
 hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint16_t* W2, int M, int N, int K,
-                       float* C, uint16_t* Cb, hipStream_t s);
+                       float* C, uint16_t* Cb, int* err_flag, hipStream_t s);
 
 }  // namespace kf

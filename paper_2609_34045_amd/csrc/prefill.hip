@@ -3,11 +3,11 @@
 // With T in the hundreds the projections are dense contractions,
 // [T, K] x [N, K]^T, and run on the matrix cores (v_mfma_f32_32x32x16_f16:
 // fp16 operands, fp32 accumulation).  Activations are kept in fp16 (8x the
-// mantissa of bf16 at the same width); bf16 weights are converted to fp16 as
-// they are staged into LDS, which is exact for every bf16 value of magnitude
-// in [2^-14, 65504] (smaller ones keep an absolute error below 2^-25).  Both
-// operands are K-contiguous in HBM (activations row-major, weights
-// [out, in]), so every MFMA operand fragment is one 16-byte run of a row.
+// mantissa of bf16 at the same width), and the weights are held in fp16 since
+// the stage was created.  A value stored in fp16 that reaches 65520 in
+// magnitude raises the stage's range error bit.  Both operands are
+// K-contiguous in HBM (activations row-major, weights [out, in]), so every
+// MFMA operand fragment is one 16-byte run of a row.
 // Attention is causal flash attention over the fp16 cache [0, pos0) plus the
 // chunk, also on the matrix cores.
 //
@@ -38,19 +38,16 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 __device__ __forceinline__ float from_bf16(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
-__device__ __forceinline__ uint16_t to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
 
 // Two fp32 to packed fp16 (round to nearest even).
 __device__ __forceinline__ uint32_t pack_f16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, h2));
 }
 
-// 8 bf16 (16 bytes) to 8 fp16 (16 bytes).
-__device__ __forceinline__ v4u bf16x8_to_f16x8(v4u w) {
-  return v4u{pack_f16(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u)),
-             pack_f16(__uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)),
-             pack_f16(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xffff0000u)),
-             pack_f16(__uint_as_float(w.w << 16), __uint_as_float(w.w & 0xffff0000u))};
+// As pack_f16, noting in `bad` a value fp16 cannot hold (see f16_checked).
+__device__ __forceinline__ uint32_t pack_f16_checked(float a, float b, bool& bad) {
+  bad |= (__builtin_fabsf(a) >= 65520.0f) | (__builtin_fabsf(b) >= 65520.0f);
+  return pack_f16(a, b);
 }
 
 __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
@@ -69,7 +66,7 @@ constexpr int kMaxSlices = 8;
 
 __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const float* part, int nsplit,
                                                                 int64_t stride, const uint16_t* g, float eps,
-                                                                uint16_t* out, int H) {
+                                                                uint16_t* out, int H, int* err_flag) {
   const int row = blockIdx.x, tid = threadIdx.x, H4 = H / 4;
   v4f* xr = reinterpret_cast<v4f*>(x + (int64_t)row * H);
   const v4f* pr = reinterpret_cast<const v4f*>(part + (int64_t)row * H);
@@ -97,12 +94,14 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const f
   const float rs = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)H + eps);
   uint2* o = reinterpret_cast<uint2*>(out + (int64_t)row * H);
   const uint2* g4 = reinterpret_cast<const uint2*>(g);
+  bool bad = false;
   for (int k = tid; k < H4; k += 256) {
     const v4f v = xr[k] * rs;
     const uint2 gw = g4[k];
-    o[k] = uint2{pack_f16(v.x * __uint_as_float(gw.x << 16), v.y * __uint_as_float(gw.x & 0xffff0000u)),
-                 pack_f16(v.z * __uint_as_float(gw.y << 16), v.w * __uint_as_float(gw.y & 0xffff0000u))};
+    o[k] = uint2{pack_f16_checked(v.x * __uint_as_float(gw.x << 16), v.y * __uint_as_float(gw.x & 0xffff0000u), bad),
+                 pack_f16_checked(v.z * __uint_as_float(gw.y << 16), v.w * __uint_as_float(gw.y & 0xffff0000u), bad)};
   }
+  raise_err(err_flag, bad, kErrF16Range);
 }
 
 // ------------------------------------------------------------------ RoPE + KV append
@@ -115,10 +114,12 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* x, const f
 __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nsplit, int64_t stride, uint16_t* q,
                                                       uint16_t* kc, uint16_t* vc, const KvPages kp, int user,
                                                       const float* cosT, const float* sinT, int nq, int nkv, int hd,
-                                                      int pos0, const uint16_t* gq, const uint16_t* gk, float eps) {
+                                                      int pos0, const uint16_t* gq, const uint16_t* gk, float eps,
+                                                      int* err_flag) {
   const int i = blockIdx.x, half = hd / 2, q4 = half / 4, pos = pos0 + i;
   const int nh = nq + 2 * nkv;
   const float* src = qkv + (int64_t)i * nh * hd;
+  bool bad = false;
   for (int e = threadIdx.x; e < nh * q4; e += 256) {
     const int h = e / q4, j = (e % q4) * 4;
     v4f a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
@@ -161,9 +162,11 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
       z2 = b;
       dst = vc + kv_offset(kp, user, h - nq - nkv, pos, hd);
     }
-    *reinterpret_cast<uint2*>(dst + j) = uint2{pack_f16(z1.x, z1.y), pack_f16(z1.z, z1.w)};
-    *reinterpret_cast<uint2*>(dst + j + half) = uint2{pack_f16(z2.x, z2.y), pack_f16(z2.z, z2.w)};
+    *reinterpret_cast<uint2*>(dst + j) = uint2{pack_f16_checked(z1.x, z1.y, bad), pack_f16_checked(z1.z, z1.w, bad)};
+    *reinterpret_cast<uint2*>(dst + j + half) =
+        uint2{pack_f16_checked(z2.x, z2.y, bad), pack_f16_checked(z2.z, z2.w, bad)};
   }
+  raise_err(err_flag, bad, kErrF16Range);
 }
 
 // ------------------------------------------------------------------ causal flash attention
@@ -189,7 +192,8 @@ template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
                                                            const uint16_t* vc, const KvPages kp, int user,
                                                            uint16_t* out, float* part_acc, float* part_ml, int T,
-                                                           int nq, int nkv, int pos0, float scale_log2) {
+                                                           int nq, int nkv, int pos0, float scale_log2,
+                                                           int* err_flag) {
   constexpr int KB = KF_PF_ATTN_KB;  // keys per block: KB / 32 tiles of 32 keys
   constexpr int NT = KB / 32;
   static_assert(KB == 32 || KB == 64, "32 or 64 keys per block");
@@ -465,10 +469,13 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   if (qok) {
     const float inv = 1.0f / l_run;
     uint16_t* dst = out + ((int64_t)qi * nq + h) * HD;
+    bool bad = false;
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = to_f16(o[d][v] * inv);
+      for (int v = 0; v < 16; ++v)
+        dst[32 * d + 8 * (v >> 2) + 4 * half_sel + (v & 3)] = f16_checked(o[d][v] * inv, bad);
+    raise_err(err_flag, bad, kErrF16Range);
   }
 }
 
@@ -476,7 +483,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
 // (a split without keys has m = -inf, l = 0 and weight 0).  One thread per 4 dims.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_prefill_combine_kernel(const float* part_acc, const float* part_ml,
-                                                                   uint16_t* out, int rows, int Z) {
+                                                                   uint16_t* out, int rows, int Z, int* err_flag) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;  // over rows * HD/4
   if (e >= (int64_t)rows * (HD / 4)) return;
   const int64_t r = e / (HD / 4);
@@ -495,7 +502,10 @@ __global__ __launch_bounds__(256) void attn_prefill_combine_kernel(const float* 
     L += w * l;
   }
   acc *= 1.0f / L;
-  reinterpret_cast<uint2*>(out + r * HD)[d4] = uint2{pack_f16(acc.x, acc.y), pack_f16(acc.z, acc.w)};
+  bool bad = false;
+  reinterpret_cast<uint2*>(out + r * HD)[d4] =
+      uint2{pack_f16_checked(acc.x, acc.y, bad), pack_f16_checked(acc.z, acc.w, bad)};
+  raise_err(err_flag, bad, kErrF16Range);
 }
 
 // ------------------------------------------------------------------ final copy
@@ -523,9 +533,9 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   if (a.T <= ws.cap_T && ws.mem) return hipSuccess;
   const int64_t T = a.T, H = a.H, nqkv = (int64_t)(a.nq + 2 * a.nkv) * a.hd;
   // the split-K slices of the largest of the QKV, O and down projections
-  const int64_t part_qkv = (int64_t)gemm_splitk(kGemmPartialF32, a.T, (int)nqkv, H) * T * nqkv;
-  const int64_t part_o = (int64_t)gemm_splitk(kGemmPartialF32, a.T, H, a.nq * a.hd) * T * H;
-  const int64_t part_d = (int64_t)gemm_splitk(kGemmPartialF32, a.T, H, a.F) * T * H;
+  const int64_t part_qkv = (int64_t)gemm_splitk(a.T, (int)nqkv, H) * T * nqkv;
+  const int64_t part_o = (int64_t)gemm_splitk(a.T, H, a.nq * a.hd) * T * H;
+  const int64_t part_d = (int64_t)gemm_splitk(a.T, H, a.F) * T * H;
   const int64_t part_attn = (int64_t)KF_PF_ATTN_SPLIT * T * a.nq * (a.hd + 2);  // key-split attention partials
   const int64_t part = std::max(std::max(part_qkv, part_attn), std::max(part_o, part_d));
   const int64_t sz_x = a256(T * H * 4), sz_xn = a256(T * H * 2), sz_part = a256(part * 4),
@@ -568,21 +578,21 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   // The previous layer's down projection may still be pending as split-K slices.
   tr.begin(NORM);
   hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, ws.part, ws.pending, TH, l.g_attn,
-                     a.eps, ws.xn, H);
+                     a.eps, ws.xn, H, a.err_flag);
   tr.end(NORM);
   ws.pending = 0;
   if ((e = hipGetLastError()) != hipSuccess) return e;
   tr.begin(QKV);
-  const int s_qkv = gemm_splitk(kGemmPartialF32, T, nqkv, H);
-  if (s_qkv > kMaxSlices || gemm_splitk(kGemmPartialF32, T, H, a.nq * a.hd) > kMaxSlices ||
-      gemm_splitk(kGemmPartialF32, T, H, a.F) > kMaxSlices)
+  const int s_qkv = gemm_splitk(T, nqkv, H);
+  if (s_qkv > kMaxSlices || gemm_splitk(T, H, a.nq * a.hd) > kMaxSlices || gemm_splitk(T, H, a.F) > kMaxSlices)
     return hipErrorInvalidValue;  // more split-K slices than the consuming kernels add
-  e = launch_gemm(kGemmPartialF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.part, nullptr, s);
+  e = launch_gemm(kGemmPartialF32, ws.xn, l.wqkv, nullptr, T, nqkv, H, ws.part, nullptr, a.err_flag, s);
   tr.end(QKV);
   if (e != hipSuccess) return e;
   tr.begin(ROPE);
   hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, ws.part, s_qkv, (int64_t)T * nqkv, ws.q, l.kc, l.vc,
-                     a.kv, a.user, a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, l.g_qn, l.g_kn, a.eps);
+                     a.kv, a.user, a.rope_cos, a.rope_sin, a.nq, a.nkv, a.hd, a.pos0, l.g_qn, l.g_kn, a.eps,
+                     a.err_flag);
   tr.end(ROPE);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)a.hd));
@@ -595,10 +605,10 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   tr.begin(ATTN);
   if (a.hd == 128)
     hipLaunchKernelGGL(attn_prefill_kernel<128>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, a.kv, a.user, ws.o, pacc,
-                       pml, T, a.nq, a.nkv, a.pos0, sl2);
+                       pml, T, a.nq, a.nkv, a.pos0, sl2, a.err_flag);
   else if (a.hd == 64)
     hipLaunchKernelGGL(attn_prefill_kernel<64>, ag, dim3(256), 0, s, ws.q, l.kc, l.vc, a.kv, a.user, ws.o, pacc,
-                       pml, T, a.nq, a.nkv, a.pos0, sl2);
+                       pml, T, a.nq, a.nkv, a.pos0, sl2, a.err_flag);
   else
     return hipErrorInvalidValue;
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -606,18 +616,20 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
     const int rows = T * a.nq;
     const int64_t n = (int64_t)rows * (a.hd / 4);
     const dim3 cg((unsigned)((n + 255) / 256));
-    if (a.hd == 128) hipLaunchKernelGGL(attn_prefill_combine_kernel<128>, cg, dim3(256), 0, s, pacc, pml, ws.o, rows, Z);
-    else hipLaunchKernelGGL(attn_prefill_combine_kernel<64>, cg, dim3(256), 0, s, pacc, pml, ws.o, rows, Z);
+    if (a.hd == 128)
+      hipLaunchKernelGGL(attn_prefill_combine_kernel<128>, cg, dim3(256), 0, s, pacc, pml, ws.o, rows, Z, a.err_flag);
+    else
+      hipLaunchKernelGGL(attn_prefill_combine_kernel<64>, cg, dim3(256), 0, s, pacc, pml, ws.o, rows, Z, a.err_flag);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   tr.end(ATTN);
   // O and down: split along K into slices that the next norm (or the output
   // store) adds in order; an unsplit projection adds into x directly.
   auto resid_proj = [&](int cls, const uint16_t* A, const uint16_t* W, int K, int* pend) {
-    const int sp = gemm_splitk(kGemmPartialF32, T, H, K);
+    const int sp = gemm_splitk(T, H, K);
     tr.begin(cls);
-    const hipError_t le = sp > 1 ? launch_gemm(kGemmPartialF32, A, W, nullptr, T, H, K, ws.part, nullptr, s)
-                                 : launch_gemm(kGemmResidF32, A, W, nullptr, T, H, K, ws.x, nullptr, s);
+    const hipError_t le = sp > 1 ? launch_gemm(kGemmPartialF32, A, W, nullptr, T, H, K, ws.part, nullptr, a.err_flag, s)
+                                 : launch_gemm(kGemmResidF32, A, W, nullptr, T, H, K, ws.x, nullptr, a.err_flag, s);
     tr.end(cls);
     *pend = sp > 1 ? sp : 0;
     return le;
@@ -626,11 +638,11 @@ hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const Prefi
   if ((e = resid_proj(OPROJ, ws.o, l.wo, a.nq * a.hd, &pend_o)) != hipSuccess) return e;
   tr.begin(NORM);
   hipLaunchKernelGGL(rmsnorm_rows_f16_kernel, dim3(T), dim3(256), 0, s, ws.x, ws.part, pend_o, TH, l.g_mlp, a.eps,
-                     ws.xn, H);
+                     ws.xn, H, a.err_flag);
   tr.end(NORM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   tr.begin(GATEUP);
-  e = launch_gemm(kGemmSwiGLU, ws.xn, l.wg, l.wu, T, 2 * a.F, H, nullptr, ws.act, s);
+  e = launch_gemm(kGemmSwiGLU, ws.xn, l.wg, l.wu, T, 2 * a.F, H, nullptr, ws.act, a.err_flag, s);
   tr.end(GATEUP);
   if (e != hipSuccess) return e;
   if ((e = resid_proj(DOWN, ws.act, l.wd, a.F, &ws.pending)) != hipSuccess) return e;

@@ -65,6 +65,8 @@ struct kf_stage {
   float *x = nullptr, *q = nullptr, *act = nullptr;
   // batch > 1: merged attention output and the residual after the output projection, in fp16
   uint16_t *o16 = nullptr, *x16 = nullptr;
+  float* o32 = nullptr;   // batch 1 with KF_STAGE_ORDERED: the merged attention output, fp32
+  int flags = 0;          // KF_STAGE_* behaviour flags
   float* kraw = nullptr;  // [B][nkv][hd] new keys before their norm and RoPE (qk_norm blocks)
   float* part_val = nullptr;
   int* part_idx = nullptr;
@@ -241,6 +243,7 @@ static int64_t decode_ws_bytes(const kf_model_config& c, int has_head) {
   n += align256(B * c.n_q_heads * c.head_dim * 4);    // q
   n += align256(B * (int64_t)c.ffn * 4);              // act
   n += align256(B * c.n_q_heads * c.head_dim * 2);    // o16
+  n += align256((int64_t)c.n_q_heads * c.head_dim * 4); // o32 (batch 1)
   n += align256(B * H * 2);                           // x16
   if (c.qk_norm) n += align256(B * (int64_t)c.n_kv_heads * c.head_dim * 4);  // kraw
   if (has_head) {
@@ -436,6 +439,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->q = (float*)take(B * c.n_q_heads * hd * 4);
   s->act = (float*)take(B * F * 4);
   s->o16 = (uint16_t*)take(B * c.n_q_heads * hd * 2);
+  s->o32 = (float*)take((int64_t)c.n_q_heads * hd * 4);
   s->x16 = (uint16_t*)take(B * H * 2);
   if (c.qk_norm) s->kraw = (float*)take(B * c.n_kv_heads * hd * 4);
   if (has_head) {
@@ -507,8 +511,27 @@ kf_status kf_stage_sync(kf_stage* s) {
   if (flag) {
     int zero = 0;
     KF_HIP(hipMemcpy(s->err_flag, &zero, 4, hipMemcpyHostToDevice), "error flag clear");
-    return fail(KF_EINVAL, "a token id was outside [0, vocab); its hidden row was set to NaN");
+    std::string msg;
+    if (flag & kErrToken) msg += "a token id was outside [0, vocab) (its hidden row was set to NaN); ";
+    if (flag & kErrF16Range)
+      msg += "an activation, key or value held in fp16 reached 65520 in magnitude (stored as infinity); ";
+    if (flag & kErrNaNLogit) msg += "a logit was NaN (skipped by the argmax; a row of NaN logits gave token -1); ";
+    msg.resize(msg.size() - 2);
+    return fail((flag & kErrToken) ? KF_EINVAL : KF_ERANGE, "%s", msg.c_str());
   }
+  return KF_OK;
+}
+
+kf_status kf_stage_set_flags(kf_stage* s, int32_t flags) {
+  if (!s) return fail(KF_EINVAL, "stage is NULL");
+  if (flags & ~KF_STAGE_ORDERED) return fail(KF_EINVAL, "unknown flag bits 0x%x", flags & ~KF_STAGE_ORDERED);
+  s->flags = flags;
+  return KF_OK;
+}
+
+kf_status kf_stage_get_flags(const kf_stage* s, int32_t* flags) {
+  if (!s || !flags) return fail(KF_EINVAL, "NULL argument");
+  *flags = s->flags;
   return KF_OK;
 }
 
@@ -786,6 +809,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     g.rope_cos = kv->rcos;
     g.rope_sin = kv->rsin;
     g.kraw = s->kraw;  // set for qk_norm blocks: q and k are normalised and rotated below
+    g.err_flag = s->err_flag;
     for (int b = 0; b < kMaxBatch; ++b) {
       g.users[b] = b < batch ? users[b] : 0;
       g.pos[b] = b < batch ? positions[b] : 0;
@@ -799,7 +823,6 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.embed = s->embed;
       g.vocab = c.vocab;
       g.x_init = s->x;
-      g.err_flag = s->err_flag;
       g.in16 = 0;  // the input rows come from src / tokens
       le = launch_gemv_src(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
     } else {
@@ -830,6 +853,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     a.n_split = n_split;
     a.max_split = kv->max_split;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+    a.err_flag = s->err_flag;
     for (int b = 0; b < kMaxBatch; ++b) {
       a.users[b] = b < batch ? users[b] : 0;
       a.len[b] = b < batch ? positions[b] + 1 : 0;
@@ -841,28 +865,36 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       KF_HIP(le, "attention launch");
     }
 
-    if (batch == 1) {  // the merge fused into a head-split output projection (one launch)
+    if (batch == 1 && !(s->flags & KF_STAGE_ORDERED)) {
+      // the merge fused into a head-split output projection (one launch; the
+      // heads' contributions reach the residual in arrival order)
       tr.begin(KF_K_OPROJ);
       const hipError_t le = launch_oproj_heads(a, L.wo, s->x, H, batch, st);
       tr.end(KF_K_OPROJ);
       KF_HIP(le, "o-proj launch");
     } else {
-      // The merge on its own, then a row-owning GEMV that also leaves the updated
-      // residual in fp16 for the gate/up launch: at batch 2-4 the input rows in
-      // fp32 would crowd the vector cache the weights stream through.
+      // The merge on its own, then a row-owning GEMV: each residual row is
+      // updated by one workgroup in a fixed order.  From batch 2 the GEMV also
+      // leaves the updated residual in fp16 for the gate/up launch (the input
+      // rows in fp32 would crowd the vector cache the weights stream through);
+      // at batch 1 the merged output and the residual stay fp32.
       tr.begin(KF_K_OPROJ);
-      hipError_t le = launch_attn_merge(a, s->o16, batch, st);
+      hipError_t le = batch > 1 ? launch_attn_merge(a, s->o16, nullptr, batch, st)
+                                : launch_attn_merge(a, nullptr, s->o32, batch, st);
       if (le == hipSuccess) {
         GemvParams op{};
         op.batch = batch;
         op.w0 = L.wo;
-        op.in = reinterpret_cast<const float*>(s->o16);
-        op.in16 = 1;
+        op.in = batch > 1 ? reinterpret_cast<const float*>(s->o16) : s->o32;
+        op.in16 = batch > 1;
         op.K = c.n_q_heads * hd;
         op.N = H;
         op.x = s->x;
-        op.out2 = s->x16;
-        op.out2_type = kOut2F16;
+        if (batch > 1) {
+          op.out2 = s->x16;
+          op.out2_type = kOut2F16;
+        }
+        op.err_flag = s->err_flag;
         le = launch_gemv(kEpiResid, resid_rows(H, s->n_cu), kGemvChunks, false, op, st);
       }
       tr.end(KF_K_OPROJ);
@@ -884,6 +916,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     // prefill's down GEMM takes the same operand in fp16): the input rows of
     // batch 2-4 then fit the vector cache beside the weights stream.
     gu.act16 = batch > 1;
+    gu.err_flag = s->err_flag;
     {
       tr.begin(KF_K_GATEUP);
       const hipError_t le = launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
@@ -899,6 +932,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     d.K = c.ffn;
     d.N = H;
     d.x = s->x;
+    d.err_flag = s->err_flag;
     if (l == s->hi - 1) {
       d.out2 = hidden_out_dev;
       d.out2_type = io == KF_BF16 ? kOut2BF16 : kOut2F32;
@@ -942,6 +976,7 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.logits = logits;
   g.part_val = s->part_val;
   g.part_idx = s->part_idx;
+  g.err_flag = s->err_flag;
   g.n_wg = gemv_grid(kEpiLMHead, kGemvRows, g);
   s->lm_wg_used = g.n_wg;
   tr.begin(KF_K_LMHEAD);
@@ -1010,6 +1045,7 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
   pa.kv = kv->pages();
   pa.rope_cos = kv->rcos;
   pa.rope_sin = kv->rsin;
+  pa.err_flag = s->err_flag;
   pa.stream = s->stream;
   hipError_t e = prefill_reserve(s->pf, pa);
   if (e == hipErrorOutOfMemory) return fail(KF_ENOMEM, "device allocation of the prefill workspace");

@@ -31,7 +31,8 @@ EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init",
            "kf_stage_set_stream", "kf_stage_sync", "kf_kv_create", "kf_kv_destroy", "kf_kv_len", "kf_kv_set_len",
            "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax",
            "kf_stage_profile", "kf_stage_profile_read", "kf_stage_describe", "kf_kv_describe",
-           "kf_kv_create_paged", "kf_kv_pages")
+           "kf_kv_create_paged", "kf_kv_pages", "kf_stage_set_flags", "kf_stage_get_flags")
+KF_STAGE_ORDERED = 1  # batch-1 decode adds the heads' output projections in a fixed order
 
 # kf_kernel_class
 KERNEL_CLASSES = ("prep", "qkv", "attn", "oproj", "gateup", "down", "lmhead", "argmax", "pf_norm", "pf_qkv", "pf_rope",
@@ -103,6 +104,8 @@ def load_library(path: str = LIB_PATH):
         "kf_kv_describe": (I32, [P, ctypes.POINTER(P), I32P, I32P]),
         "kf_kv_create_paged": (I32, [P, I32, I32, I32, ctypes.POINTER(P)]),
         "kf_kv_pages": (I32, [P, I32P, I32P]),
+        "kf_stage_set_flags": (I32, [P, I32]),
+        "kf_stage_get_flags": (I32, [P, I32P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -206,6 +209,15 @@ class Stage:
 
     def sync(self):
         _check(self._lib.kf_stage_sync(self.handle), "kf_stage_sync")
+
+    def set_flags(self, flags: int):
+        """KF_STAGE_* behaviour flags (kf_stage_set_flags)."""
+        _check(self._lib.kf_stage_set_flags(self.handle, int(flags)), "kf_stage_set_flags")
+
+    def flags(self) -> int:
+        f = ctypes.c_int32()
+        _check(self._lib.kf_stage_get_flags(self.handle, ctypes.byref(f)), "kf_stage_get_flags")
+        return f.value
 
     def describe(self) -> dict:
         """The library's own record of the stage (kf_stage_describe)."""

@@ -54,3 +54,22 @@ class SeededModel:
         if self._head is None:
             self._head = synth.head_weights(self.shape, self.cfg_id, self.seed)
         return self._head
+
+
+def f32_to_bf16_bits(a) -> np.ndarray:
+    """float values to bf16 bit patterns, rounded to nearest even (finite inputs)."""
+    u = np.asarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = u + 0x7FFF + ((u >> 16) & 1)
+    return (u >> 16).astype(np.uint16)
+
+
+def plant_lm_rows(head: dict, xhat: np.ndarray, rows, scale: float = 10.0) -> dict:
+    """A copy of the head weights whose LM-head rows `rows` all hold scale * xhat / |xhat| (bf16),
+    so that their logits on the normalised hidden row xhat are equal and far above the others."""
+    h = dict(head)
+    lm = np.array(head["lm_head"], copy=True)
+    bits = f32_to_bf16_bits(scale * xhat / np.linalg.norm(xhat))
+    for r in rows:
+        lm[r] = bits
+    h["lm_head"] = lm
+    return h

@@ -46,7 +46,21 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.kf_abi_version() == 3
+    assert lib.kf_abi_version() == 4
+
+
+def _comment_before(text: str, name: str) -> str:
+    """The block comment that ends closest above the declaration of `name`."""
+    at = re.search(r"\bkf_status\s+" + name + r"\s*\(", text).start()
+    return text[:at][text[:at].rfind("/*"):]
+
+
+@pytest.mark.parametrize("name", ["kf_stage_init", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits",
+                                  "kf_head_argmax", "kf_kv_create", "kf_stage_bytes"])
+def test_boundary_declarations_cite_the_paper(name):
+    """Each call of the stage boundary names the passage of the paper that defines it."""
+    text = open(os.path.join(ROOT, "include", "kafila_stage.h")).read()
+    assert re.search(r"Section [IVX]+(-[A-D])?", _comment_before(text, name)), name
 
 
 def test_stage_bytes_matches_shape_arithmetic():

@@ -9,8 +9,8 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import OracleStage
-from tests.helpers import argmax_agrees, assert_hidden_close
+from oracle import OracleStage, bf16_to_f64, rms_norm
+from tests.helpers import argmax_agrees, assert_hidden_close, plant_lm_rows
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(170)]
 
@@ -98,6 +98,30 @@ def test_8b_head_argmax_on_identical_hidden(torch, head_stage):
     assert_hidden_close(lg, lr, rtol=1e-3, what="logits")
     assert np.array_equal(t_gpu.cpu().numpy(), np.argmax(lr, axis=1))
     np.testing.assert_allclose(mx.cpu().numpy(), lr.max(axis=1), rtol=1e-4)
+
+
+def test_8b_head_planted_ties_at_full_vocab(torch, kf):
+    """V = 128256: batch row 0 gets an exact tie between LM-head rows 1003 and 127000 (different
+    workgroups, so the final reduction must keep the lower index), row 1 a tie inside one 8-row
+    workgroup (72002 and 72007), row 2 a planted maximum in the last row (128255, the tail workgroup);
+    row 3 is unplanted.  GPU tokens equal the oracle's, which are the lowest planted indices."""
+    wl = synth.WORKLOADS["8b_head"]
+    s = wl.shape
+    hw = synth.head_weights(s, wl.cfg_id, wl.seed)
+    h = synth.hidden_states(wl.cfg_id, synth.STREAM_DECODE_HIDDEN, 901, 4, s.hidden, wl.seed)
+    xh = rms_norm(h.astype(np.float64), bf16_to_f64(hw["final_norm"]), s.rms_eps)
+    plants = {0: [127000, 1003], 1: [72007, 72002], 2: [128255]}
+    for b, rows in plants.items():
+        hw = plant_lm_rows(hw, xh[b], rows)
+    lw = synth.layer_weights(s, wl.cfg_id, 0, wl.seed)
+    g = kf.Stage(s, 0, 1, {0: lw}, hw)
+    o = OracleStage(s, 0, 1, {0: lw}.__getitem__, hw, max_users=1, max_ctx=4)
+    t = g.head_argmax(dev(torch, h)).cpu().numpy()
+    want = o.argmax(h)
+    assert [int(want[b]) for b in plants] == [1003, 72002, 128255]
+    assert np.array_equal(t, want), (t, want)
+    g.sync()
+    g.close()
 
 
 def test_8b_head_prefill_then_teacher_forced_decode(torch, head_stage):

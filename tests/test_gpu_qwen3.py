@@ -111,3 +111,21 @@ def test_full_shape_decode_batch_and_prefill_chunk(torch, st, shape, cfg_id):
     print(shape, "max row rel err", worst)
     kv.close()
     g.close()
+
+
+@pytest.mark.timeout(170)
+def test_qwen3_32b_prefill_chunk_as_benched(torch, st):
+    """Layer 16 of the Qwen3-32B shape, the benchmark's chunk: 512 tokens at positions [3584, 4096)
+    over an injected cache for [0, 3584) (all 512 rows compared), then one decode step."""
+    wl = synth.WORKLOADS["qwen3_32b_b1"]
+    shape, cfg_id = wl.shape, wl.cfg_id
+    g, kv, o = _full(torch, st, shape, cfg_id, 16, 17, 1, 4096 + 8, (3584,))
+    h = synth.hidden_states(cfg_id, synth.STREAM_PREFILL_HIDDEN, 7, 512, shape.hidden)
+    y = g.prefill(kv, 0, 3584, hidden=dev(torch, h))
+    worst = assert_hidden_close(host(y), o.prefill(0, 3584, hidden=h), what="qwen3-32b chunk")
+    x = synth.hidden_states(cfg_id, synth.STREAM_DECODE_HIDDEN, 3, 1, shape.hidden)
+    y = g.decode(kv, [0], [4096], hidden=dev(torch, x))
+    worst = max(worst, assert_hidden_close(host(y), o.decode([0], [4096], hidden=x), what="decode after chunk"))
+    print("qwen3-32b chunk max row rel err", worst)
+    kv.close()
+    g.close()

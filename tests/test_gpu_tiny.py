@@ -9,8 +9,8 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import OracleStage, bf16_to_f64
-from tests.helpers import SeededModel, argmax_agrees, assert_hidden_close, row_rel_err
+from oracle import OracleStage, bf16_to_f64, rms_norm
+from tests.helpers import SeededModel, argmax_agrees, assert_hidden_close, f32_to_bf16_bits, plant_lm_rows, row_rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -163,46 +163,160 @@ def test_argmax_on_identical_hidden_batch(torch, st, model):
     h = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 50, 4, SHAPE.hidden)
     t = g.head_argmax(dev(torch, h)).cpu().numpy()
     assert np.array_equal(t, o.argmax(h))
-    # a planted exact tie between two LM-head rows: the lower index wins on both sides
     kv.close()
     g.close()
 
 
-def test_embedding_gather_is_exact(torch, st, model):
-    """Token input equals hidden input of the exact fp32 embedding rows; the two decodes agree
-    to fp32 summation-order rounding (the output projection adds heads in arrival order)."""
+def xhat_of(model, h):
+    """The final-normed hidden rows the LM head multiplies (oracle arithmetic)."""
+    return rms_norm(h.astype(np.float64), bf16_to_f64(model.head()["final_norm"]), SHAPE.rms_eps)
+
+
+# (planted rows per batch row): a maximum alone, exact ties inside one 8-row LM-head workgroup
+# (rows 8k+1 and 8k+6; 8k+1 must win), and ties across workgroups (the lower index must win)
+PLANTS = [([301],), ([8 * 37 + 6, 8 * 37 + 1],), ([905, 17],), ([640, 648, 999],)]
+
+
+@pytest.mark.parametrize("plant", PLANTS, ids=["max", "tie_in_wg", "tie_across_wg", "three_way"])
+def test_argmax_planted_maximum_and_ties(torch, st, model, plant):
+    """LM-head rows set to 10 x_hat/|x_hat| for one hidden row make that row's logits there equal
+    (identical weights, identical arithmetic) and far above the rest: the lowest planted index wins
+    on the GPU and in the oracle."""
+    (rows,) = plant
+    h = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 60, 4, SHAPE.hidden)
+    b = 2  # the batch row the plant is aimed at
+    head = plant_lm_rows(model.head(), xhat_of(model, h[b:b + 1])[0], rows)
+    g = st.Stage(SHAPE, 0, 1, model.layer, head)
+    o = OracleStage(SHAPE, 0, 1, model.layer, head, max_users=1, max_ctx=4)
+    t, mx = g.head_argmax(dev(torch, h), with_max=True)
+    t = t.cpu().numpy()
+    want = o.argmax(h)
+    assert want[b] == min(rows)
+    assert np.array_equal(t, want), (t, want)
+    lg = host(g.head_logits(dev(torch, h)))
+    assert np.all(lg[b, rows] == lg[b, rows[0]])  # the tie is exact on the GPU
+    assert float(mx.cpu().numpy()[b]) == lg[b, min(rows)]
+    g.sync()
+    g.close()
+
+
+def test_argmax_skips_nan_logits_and_reports_them(torch, st, model):
+    """A NaN LM-head row at the start of a workgroup whose later row holds the planted maximum:
+    the maximum still wins, and sync reports the NaN logit; an all-NaN hidden row gives token -1."""
+    h = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 61, 4, SHAPE.hidden)
+    head = plant_lm_rows(model.head(), xhat_of(model, h[0:1])[0], [8 * 20 + 5])
+    head["lm_head"][8 * 20] = 0x7FC0  # bf16 quiet NaN in the workgroup's first row
+    g = st.Stage(SHAPE, 0, 1, model.layer, head)
+    t = g.head_argmax(dev(torch, h)).cpu().numpy()
+    assert t[0] == 8 * 20 + 5
+    with pytest.raises(st.KFError) as e:
+        g.sync()
+    assert e.value.status == st.KF_ERANGE and "NaN" in e.value.message
+    g.sync()  # cleared once reported
+    hn = h.copy()
+    hn[1] = np.nan
+    t, mx = g.head_argmax(dev(torch, hn), with_max=True)
+    t = t.cpu().numpy()
+    assert t[1] == -1 and np.isnan(mx.cpu().numpy()[1])
+    assert t[0] == 8 * 20 + 5
+    with pytest.raises(st.KFError):
+        g.sync()
+    g.close()
+
+
+def test_fp16_activation_overflow_is_reported(torch, st, model):
+    """A residual row beyond the fp16 range at batch 2 (the decode keeps an fp16 copy of the residual
+    from batch 2) and an attention-norm gain that drives the prefill's fp16 normalised rows past
+    65504 both raise the range error; batch 1 keeps the residual in fp32 and raises nothing."""
+    g, kv, _ = make(st, model, users=2, ctx=16)
+    x = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 70, 2, SHAPE.hidden)
+    x[1] *= 1e5
+    g.decode(kv, [1], [0], hidden=dev(torch, x[1:2]))
+    g.sync()  # batch 1: fp32 residual, normalised inputs
+    g.decode(kv, [0, 1], [0, 1], hidden=dev(torch, x))
+    with pytest.raises(st.KFError) as e:
+        g.sync()
+    assert e.value.status == st.KF_ERANGE and "65520" in e.value.message
+    g.sync()
+    kv.close()
+    g.close()
+    big = dict(model.layer(0))
+    big["attn_norm"] = np.full_like(big["attn_norm"], f32_to_bf16_bits(np.float32(7e4)))
+    g = st.Stage(SHAPE, 0, 1, lambda l: big)
+    kv = g.kv(1, 16)
+    g.prefill(kv, 0, 0, hidden=dev(torch, synth.hidden_states(CFG, synth.STREAM_PREFILL_HIDDEN, 71, 8, SHAPE.hidden)))
+    with pytest.raises(st.KFError) as e:
+        g.sync()
+    assert e.value.status == st.KF_ERANGE
+    kv.close()
+    g.close()
+
+
+@pytest.mark.parametrize("users", [[0, 1, 2, 3], [0]])
+def test_embedding_gather_is_exact(torch, st, model, users):
+    """Token input equals hidden input of the exact fp32 embedding rows, bit for bit (batch 1 with
+    the ordered output projection)."""
     g, kv, o = make(st, model, head=True)
-    toks = np.array([0, 999, 5, 5], dtype=np.int32)
-    a = g.decode(kv, [0, 1, 2, 3], [0, 0, 0, 0], tokens=dev(torch, toks))
+    g.set_flags(st.KF_STAGE_ORDERED)
+    toks = np.array([0, 999, 5, 5][:len(users)], dtype=np.int32)
+    pos = [0] * len(users)
+    a = g.decode(kv, users, pos, tokens=dev(torch, toks))
     kv2 = g.kv(4, 16)
     emb = bf16_to_f64(model.head()["embed"][toks]).astype(np.float32)
-    b = g.decode(kv2, [0, 1, 2, 3], [0, 0, 0, 0], hidden=dev(torch, emb))
-    assert float(row_rel_err(host(b), host(a)).max()) <= 1e-4
+    b = g.decode(kv2, users, pos, hidden=dev(torch, emb))
+    assert torch.equal(a, b)
     kv2.close()
     kv.close()
     g.close()
 
 
 def test_stage_composition(torch, st, model):
-    """Layers [0,2) as one stage equal [0,1) then [1,2): bit-exact for prefill (no split
-    reductions at this shape); decode adds the heads' output projections into the residual
-    with atomics in arrival order, so two runs agree to fp32 summation-order rounding."""
+    """Layers [0,2) as one stage equal [0,1) then [1,2), bit for bit: prefill, and decode at batch
+    1 (ordered output projection), 2, 3 and 4 (the first layer of a stage rounds its input rows to
+    fp16 from batch 2 as every later layer does)."""
     whole = st.Stage(SHAPE, 0, 2, model.layer)
     first = st.Stage(SHAPE, 0, 1, model.layer)
     second = st.Stage(SHAPE, 1, 2, model.layer)
-    kw, k1, k2 = whole.kv(2, 64), first.kv(2, 64), second.kv(2, 64)
+    for g in (whole, first, second):
+        g.set_flags(st.KF_STAGE_ORDERED)
+    kw, k1, k2 = whole.kv(4, 64), first.kv(4, 64), second.kv(4, 64)
     h = synth.hidden_states(CFG, synth.STREAM_PREFILL_HIDDEN, 3, 20, SHAPE.hidden)
     a = whole.prefill(kw, 0, 0, hidden=dev(torch, h))
     b = second.prefill(k2, 0, 0, hidden=first.prefill(k1, 0, 0, hidden=dev(torch, h)))
     assert torch.equal(a, b)
-    for step in range(3):
-        x = dev(torch, synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 300 + step, 2, SHAPE.hidden))
-        users, pos = [0, 1], [20 + step, step]
+    for step, users in enumerate(([0, 1], [1], [2, 0, 1], [3, 1, 0, 2], [0])):
+        x = dev(torch, synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 300 + step, len(users), SHAPE.hidden))
+        pos = [kw.len(u) for u in users]
         a = whole.decode(kw, users, pos, hidden=x)
         b = second.decode(k2, users, pos, hidden=first.decode(k1, users, pos, hidden=x))
-        assert float(row_rel_err(host(b), host(a)).max()) <= 1e-4
+        assert torch.equal(a, b), f"batch {len(users)}: max diff {float((a - b).abs().max())}"
     for x in (kw, k1, k2, whole, first, second):
         x.close()
+
+
+def test_batch1_ordered_decode_is_reproducible(torch, st, model):
+    """With the ordered output projection, the same batch-1 decode run twice from the same cache is
+    bit-identical; the fused (arrival-order) projection agrees with it to fp32 reassociation."""
+    g, kv, o = make(st, model, users=3)
+    g.set_flags(st.KF_STAGE_ORDERED)
+    assert g.flags() == st.KF_STAGE_ORDERED
+    h = synth.hidden_states(CFG, synth.STREAM_PREFILL_HIDDEN, 5, 100, SHAPE.hidden)
+    for u in range(3):
+        g.prefill(kv, u, 0, hidden=dev(torch, h))
+    o.prefill(0, 0, hidden=h)
+    xh = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 500, 1, SHAPE.hidden)
+    x = dev(torch, xh)
+    a = g.decode(kv, [0], [100], hidden=x)
+    assert_hidden_close(host(a), o.decode([0], [100], hidden=xh), what="ordered batch-1 decode")
+    b = g.decode(kv, [1], [100], hidden=x)
+    assert torch.equal(a, b)
+    g.set_flags(0)
+    c = g.decode(kv, [2], [100], hidden=x)
+    assert float(row_rel_err(host(c), host(a)).max()) <= 1e-4
+    with pytest.raises(st.KFError):
+        g.set_flags(2)
+    kv.close()
+    g.close()
 
 
 def test_prefill_equals_sequential_decode(torch, st, model):

@@ -65,3 +65,14 @@ def test_gains_centre_on_one_and_layers_are_global():
     g = synth.bf16_bits_to_f32(w8["attn_norm"])
     assert abs(float(g.mean()) - 1.0) < 5e-3 and float(g.std()) > 0.01
     assert w8["wq"].shape == (512, 512) and w8["wk"].shape == (128, 512) and w8["wd"].shape == (512, 1408)
+
+
+def test_bf16_test_helper_matches_torch_rounding():
+    """The tests' float-to-bf16 helper rounds to nearest even exactly as torch does."""
+    import torch
+
+    from tests.helpers import f32_to_bf16_bits
+    x = np.random.default_rng(0).standard_normal(4096).astype(np.float32) * np.float32(300.0)
+    x[:4] = [7e4, -1e-30, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8]  # ties round to even
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(f32_to_bf16_bits(x), want)
