@@ -44,7 +44,8 @@ extern "C" {
 #define KF_ABI_VERSION 4  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds;
                             3: paged KV caches, kf_stage_describe, kf_kv_describe;
                             4: kf_stage_set_flags / kf_stage_get_flags (KF_STAGE_ORDERED), range and
-                               NaN-logit errors reported by kf_stage_sync, token -1 for a row of NaN logits */
+                               NaN-logit errors reported by kf_stage_sync, token -1 for a row of NaN logits,
+                               kf_stage_prefill_noalloc */
 #define KF_KV_PAGE 64     /* positions per KV cache page */
 #define KF_MAX_BATCH 4
 
@@ -281,6 +282,24 @@ kf_status kf_stage_decode(kf_stage* stage, kf_kv* kv, int32_t batch, const int32
 kf_status kf_stage_prefill(kf_stage* stage, kf_kv* kv, int32_t user, int32_t pos0, int32_t n_tokens,
                            const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev,
                            kf_dtype io);
+
+/*
+ * kf_stage_prefill without any device allocation, for callers that cannot allocate:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, checks, results and state changes as
+ * kf_stage_prefill; the chunk's workspace (residual rows, normalised rows,
+ * split-K partial sums, queries, attention output, SwiGLU output) lives in a static
+ * per-device scratch array of KF_PREFILL_SCRATCH_BYTES instead of the stage's own
+ * grown buffer.  A chunk whose workspace exceeds it is KF_ERANGE (nothing enqueued);
+ * a 512-token chunk of every shape used here fits (the largest, hidden 8192 with
+ * ffn 28672, needs 132 MiB).  All no-allocation prefills on one device share the
+ * array: calls on one device whose work overlaps (other streams, other stages, other
+ * threads) race, so the caller orders them.  No per-kernel timing is recorded.
+ */
+#define KF_PREFILL_SCRATCH_BYTES (144LL << 20)
+kf_status kf_stage_prefill_noalloc(kf_stage* stage, kf_kv* kv, int32_t user, int32_t pos0, int32_t n_tokens,
+                                   const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev,
+                                   kf_dtype io);
 
 /*
  * The head's unembedding (Section III and Fig. 1: the head member holds the

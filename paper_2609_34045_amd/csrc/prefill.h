@@ -42,8 +42,13 @@ struct PrefillWorkspace {
   uint16_t* act = nullptr; // [T][F] SwiGLU output, fp16
 };
 
+// Grows ws (hipMalloc) to hold a chunk of a.T tokens.
 hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a);
 void prefill_free(PrefillWorkspace& ws);
+// Device bytes a chunk of a.T tokens needs, and the workspace laid out from `base`
+// (at least that many bytes, 256-byte aligned; ws does not own it).
+int64_t prefill_ws_bytes(const PrefillArgs& a);
+void prefill_carve(PrefillWorkspace& ws, char* base, const PrefillArgs& a);
 hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr);
 
 // Matrix-core GEMM of the prefill projections (gemm.hip).

@@ -529,8 +529,9 @@ void prefill_free(PrefillWorkspace& ws) {
   ws = PrefillWorkspace{};
 }
 
-hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
-  if (a.T <= ws.cap_T && ws.mem) return hipSuccess;
+// Bytes of each workspace buffer for a chunk of a.T tokens, in layout order:
+// x, xn, part, q, o, act.
+static void prefill_sizes(const PrefillArgs& a, int64_t (&sz)[6]) {
   const int64_t T = a.T, H = a.H, nqkv = (int64_t)(a.nq + 2 * a.nkv) * a.hd;
   // the split-K slices of the largest of the QKV, O and down projections
   const int64_t part_qkv = (int64_t)gemm_splitk(a.T, (int)nqkv, H) * T * nqkv;
@@ -538,9 +539,41 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   const int64_t part_d = (int64_t)gemm_splitk(a.T, H, a.F) * T * H;
   const int64_t part_attn = (int64_t)KF_PF_ATTN_SPLIT * T * a.nq * (a.hd + 2);  // key-split attention partials
   const int64_t part = std::max(std::max(part_qkv, part_attn), std::max(part_o, part_d));
-  const int64_t sz_x = a256(T * H * 4), sz_xn = a256(T * H * 2), sz_part = a256(part * 4),
-                sz_q = a256(T * a.nq * a.hd * 2), sz_o = a256(T * a.nq * a.hd * 2), sz_act = a256(T * a.F * 2);
-  const int64_t total = sz_x + sz_xn + sz_part + sz_q + sz_o + sz_act;
+  sz[0] = a256(T * H * 4);
+  sz[1] = a256(T * H * 2);
+  sz[2] = a256(part * 4);
+  sz[3] = a256(T * a.nq * a.hd * 2);
+  sz[4] = a256(T * a.nq * a.hd * 2);
+  sz[5] = a256(T * a.F * 2);
+}
+
+int64_t prefill_ws_bytes(const PrefillArgs& a) {
+  int64_t sz[6];
+  prefill_sizes(a, sz);
+  return sz[0] + sz[1] + sz[2] + sz[3] + sz[4] + sz[5];
+}
+
+void prefill_carve(PrefillWorkspace& ws, char* base, const PrefillArgs& a) {
+  int64_t sz[6];
+  prefill_sizes(a, sz);
+  char* p = base;
+  ws.x = (float*)p;
+  p += sz[0];
+  ws.xn = (uint16_t*)p;
+  p += sz[1];
+  ws.part = (float*)p;
+  p += sz[2];
+  ws.q = (uint16_t*)p;
+  p += sz[3];
+  ws.o = (uint16_t*)p;
+  p += sz[4];
+  ws.act = (uint16_t*)p;
+  ws.pending = 0;
+}
+
+hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
+  if (a.T <= ws.cap_T && ws.mem) return hipSuccess;
+  const int64_t total = prefill_ws_bytes(a);
   char* mem = nullptr;
   // Drain work that may still use the old buffer before freeing it.
   hipError_t e = hipStreamSynchronize(a.stream);
@@ -553,18 +586,7 @@ hipError_t prefill_reserve(PrefillWorkspace& ws, const PrefillArgs& a) {
   prefill_free(ws);
   ws.mem = mem;
   ws.cap_T = a.T;
-  char* p = mem;
-  ws.x = (float*)p;
-  p += sz_x;
-  ws.xn = (uint16_t*)p;
-  p += sz_xn;
-  ws.part = (float*)p;
-  p += sz_part;
-  ws.q = (uint16_t*)p;
-  p += sz_q;
-  ws.o = (uint16_t*)p;
-  p += sz_o;
-  ws.act = (uint16_t*)p;
+  prefill_carve(ws, mem, a);
   return hipSuccess;
 }
 

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -46,6 +47,39 @@ static int resid_rows(int n, int n_cu) {
 
 static int64_t align256(int64_t n) { return (n + 255) & ~(int64_t)255; }
 
+// Prefill workspace of kf_stage_prefill_noalloc: a file-scope device array, one
+// copy per device, held from the library's first use on a device until the
+// process ends.  In host code the name `scratch` is a stand-in symbol, not a
+// device address: the address comes from hipGetSymbolAddress, taken once per
+// device (with that device current) when a stage is created there, and only that
+// address is passed to kernels.  Every no-allocation prefill on a device shares
+// the array, so such calls must not overlap on one device.
+constexpr int64_t kPrefillScratchBytes = 144LL << 20;  // a 512-token chunk of the 70B shape needs 132 MiB
+static __device__ __align__(256) char scratch[kPrefillScratchBytes];
+static_assert(kPrefillScratchBytes == KF_PREFILL_SCRATCH_BYTES, "the header states the scratch size");
+constexpr int kMaxDevices = 64;
+
+static char* scratch_address(int device, hipError_t* err) {
+  static std::mutex mu;
+  static char* addr[kMaxDevices] = {};
+  std::lock_guard<std::mutex> lock(mu);
+  *err = hipSuccess;
+  if (device < 0 || device >= kMaxDevices) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  if (!addr[device]) {
+    void* p = nullptr;
+    *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*err != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    addr[device] = static_cast<char*>(p);
+  }
+  return addr[device];
+}
+
 struct LayerW {
   uint16_t *wqkv, *wo, *wg, *wu, *wd, *g_attn, *g_mlp;
   uint16_t *g_qn = nullptr, *g_kn = nullptr;  // per-head q / k norm gains (qk_norm blocks)
@@ -75,6 +109,7 @@ struct kf_stage {
   int* err_flag = nullptr;
   int live_kv = 0;
   PrefillWorkspace pf;
+  char* scratch = nullptr;  // this device's copy of the static prefill scratch (device address)
   // instrumentation: event pairs around launches while profiling is enabled
   int prof_mask = 0;
   std::vector<hipEvent_t> ev;   // 2 per recorded launch
@@ -351,6 +386,14 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, s->device) == hipSuccess && n > 0) s->n_cu = n;
+  }
+  {
+    hipError_t e;
+    s->scratch = scratch_address(s->device, &e);
+    if (!s->scratch) {
+      delete s;
+      return fail(KF_EDEVICE, "device address of the prefill scratch: %s", hipGetErrorString(e));
+    }
   }
 
   const kf_model_config& c = *cfg;
@@ -1017,8 +1060,13 @@ kf_status kf_head_argmax(kf_stage* s, int32_t rows, const void* hidden, kf_dtype
 }
 
 // ------------------------------------------------------------------ prefill
-kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, int32_t n, const int32_t* tokens_dev,
-                           const void* hidden_in_dev, void* hidden_out_dev, kf_dtype io) {
+// The allocating prefill grows the stage's own workspace (hipMalloc) to the largest
+// chunk seen; the no-allocation variant lays the same workspace out in the
+// device's static scratch array instead (stage->scratch, at most
+// kPrefillScratchBytes) and records no timing events.
+static kf_status prefill_impl(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, int32_t n,
+                              const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev, kf_dtype io,
+                              bool no_alloc) {
   if (!s || !kv) return fail(KF_EINVAL, "stage or kv is NULL");
   if (kv->st != s) return fail(KF_EINVAL, "kv belongs to another stage");
   if (n < 1) return fail(KF_EINVAL, "n_tokens must be >= 1");
@@ -1047,19 +1095,31 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
   pa.rope_sin = kv->rsin;
   pa.err_flag = s->err_flag;
   pa.stream = s->stream;
-  hipError_t e = prefill_reserve(s->pf, pa);
-  if (e == hipErrorOutOfMemory) return fail(KF_ENOMEM, "device allocation of the prefill workspace");
-  KF_HIP(e, "prefill workspace");
+  PrefillWorkspace scratch_ws;
+  PrefillWorkspace* ws = &s->pf;
+  if (no_alloc) {
+    const int64_t need = prefill_ws_bytes(pa);
+    if (need > kPrefillScratchBytes)
+      return fail(KF_ERANGE, "a chunk of %d tokens needs %lld bytes of prefill scratch, above the %lld held per device",
+                  n, (long long)need, (long long)kPrefillScratchBytes);
+    if (!s->scratch) return fail(KF_EDEVICE, "the device's prefill scratch has no address");
+    prefill_carve(scratch_ws, s->scratch, pa);
+    ws = &scratch_ws;
+  } else {
+    hipError_t e = prefill_reserve(s->pf, pa);
+    if (e == hipErrorOutOfMemory) return fail(KF_ENOMEM, "device allocation of the prefill workspace");
+    KF_HIP(e, "prefill workspace");
+  }
   const int64_t upto = (int64_t)pos0 + n;
   const kf_status gst = kv_grant(kv, 1, &user, &upto);
   if (gst != KF_OK) return gst;
-  const Tracer tr = s->tracer();
+  const Tracer tr = no_alloc ? Tracer{} : s->tracer();  // event records may create events
   tr.begin(KF_K_PREP);
-  e = launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, s->pf.x, n, c.hidden, s->err_flag,
-                         s->stream);
+  hipError_t e = launch_prep_hidden(hidden_in_dev, io == KF_BF16, tokens_dev, s->embed, c.vocab, ws->x, n, c.hidden,
+                                    s->err_flag, s->stream);
   tr.end(KF_K_PREP);
   KF_HIP(e, "prefill prep launch");
-  s->pf.pending = 0;  // x now holds the whole input; no split-K slices are pending
+  ws->pending = 0;  // x now holds the whole input; no split-K slices are pending
   for (int l = s->lo; l < s->hi; ++l) {
     const LayerW& L = s->layers[l - s->lo];
     const int64_t loff = (l - s->lo) * kv->layer_stride;
@@ -1077,10 +1137,21 @@ kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, i
     pl.vc = kv->v + loff;
     pl.out = l == s->hi - 1 ? hidden_out_dev : nullptr;
     pl.out_bf16 = io == KF_BF16;
-    KF_HIP(prefill_layer(s->pf, pa, pl, tr), "prefill layer");
+    KF_HIP(prefill_layer(*ws, pa, pl, tr), "prefill layer");
   }
   kv->len[user] += n;
   return KF_OK;
+}
+
+kf_status kf_stage_prefill(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, int32_t n, const int32_t* tokens_dev,
+                           const void* hidden_in_dev, void* hidden_out_dev, kf_dtype io) {
+  return prefill_impl(s, kv, user, pos0, n, tokens_dev, hidden_in_dev, hidden_out_dev, io, false);
+}
+
+kf_status kf_stage_prefill_noalloc(kf_stage* s, kf_kv* kv, int32_t user, int32_t pos0, int32_t n,
+                                   const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev,
+                                   kf_dtype io) {
+  return prefill_impl(s, kv, user, pos0, n, tokens_dev, hidden_in_dev, hidden_out_dev, io, true);
 }
 
 // ------------------------------------------------------------------ instrumentation

@@ -31,7 +31,9 @@ EXPORTS = ("kf_abi_version", "kf_last_error", "kf_stage_bytes", "kf_stage_init",
            "kf_stage_set_stream", "kf_stage_sync", "kf_kv_create", "kf_kv_destroy", "kf_kv_len", "kf_kv_set_len",
            "kf_kv_write", "kf_kv_read", "kf_stage_decode", "kf_stage_prefill", "kf_head_logits", "kf_head_argmax",
            "kf_stage_profile", "kf_stage_profile_read", "kf_stage_describe", "kf_kv_describe",
-           "kf_kv_create_paged", "kf_kv_pages", "kf_stage_set_flags", "kf_stage_get_flags")
+           "kf_kv_create_paged", "kf_kv_pages", "kf_stage_set_flags", "kf_stage_get_flags",
+           "kf_stage_prefill_noalloc")
+PREFILL_SCRATCH_BYTES = 144 << 20  # KF_PREFILL_SCRATCH_BYTES: the no-allocation prefill's workspace limit
 KF_STAGE_ORDERED = 1  # batch-1 decode adds the heads' output projections in a fixed order
 
 # kf_kernel_class
@@ -96,6 +98,7 @@ def load_library(path: str = LIB_PATH):
         "kf_kv_read": (I32, [P, I32, I32, I32, I32, VP, VP]),
         "kf_stage_decode": (I32, [P, P, I32, I32P, I32P, VP, VP, VP, I32]),
         "kf_stage_prefill": (I32, [P, P, I32, I32, I32, VP, VP, VP, I32]),
+        "kf_stage_prefill_noalloc": (I32, [P, P, I32, I32, I32, VP, VP, VP, I32]),
         "kf_head_logits": (I32, [P, I32, VP, I32, VP]),
         "kf_head_argmax": (I32, [P, I32, VP, I32, VP, VP]),
         "kf_stage_profile": (I32, [P, I32]),
@@ -283,7 +286,9 @@ class Stage:
                "kf_stage_decode")
         return out
 
-    def prefill(self, kv: "KV", user: int, pos0: int, tokens=None, hidden=None, out=None):
+    def prefill(self, kv: "KV", user: int, pos0: int, tokens=None, hidden=None, out=None, noalloc: bool = False):
+        """kf_stage_prefill, or with ``noalloc`` kf_stage_prefill_noalloc (the library allocates nothing;
+        pass ``out`` as well to keep the call free of allocations on the Python side too)."""
         import torch
         src = hidden if hidden is not None else tokens
         n = 0 if src is None else int(src.shape[0])
@@ -298,8 +303,9 @@ class Stage:
                 raise TypeError("tokens must be int32")
         if out is None:
             out = torch.empty((max(n, 1), self.shape.hidden), dtype=odt, device=src.device if src is not None else "cuda")
-        _check(self._lib.kf_stage_prefill(self.handle, kv.handle, user, pos0, n, _ptr(tokens), _ptr(hidden),
-                                          _ptr(out), io), "kf_stage_prefill")
+        fn, name = ((self._lib.kf_stage_prefill_noalloc, "kf_stage_prefill_noalloc") if noalloc
+                    else (self._lib.kf_stage_prefill, "kf_stage_prefill"))
+        _check(fn(self.handle, kv.handle, user, pos0, n, _ptr(tokens), _ptr(hidden), _ptr(out), io), name)
         return out
 
     def head_logits(self, hidden, out=None):
