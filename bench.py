@@ -1,16 +1,18 @@
 #!/usr/bin/env python3
 """Stage decode benchmark on one MI355X.
 
-Times K decode steps of one pipeline stage (a contiguous range of decoder
-layers, optionally with the head) at the workload's batch and context, and
-prints one JSON line: tokens/s, the step's algorithmic HBM bytes per second
-against the 8 TB/s peak, the dominant kernel's roofline figure (HIP-event
-durations of its launches inside the timed region), and the CPU oracle's
-throughput on a bounded sample of the same workload.
+Default line: the 32B-shaped stage (layers [16, 32) of a 64-layer model, H5120,
+40 q / 8 KV heads x 128, F27648) decoding at context 4096 (KV cache injected for
+positions [0, 4096)), at batch 1 (`value`) and batch 4 (`batch4`): tokens/s, the
+step's algorithmic HBM bytes per second against the 8 TB/s peak, the dominant
+kernel's roofline figure (HIP-event durations of its launches), the 70B-shaped
+stage's 512-token prefill chunk against the matrix-core peak (`prefill_70b`), the
+streaming-read probe's attainable bandwidth, and the CPU oracle's throughput on a
+bounded sample of the same workload.  Timing follows the paper's rule (Section
+VI): five runs of K steps, the first discarded as cold, the median of the rest.
+All inputs are seeded and synthetic.
 
-Default workload: layers [8, 16) of a Llama-3-8B-shaped model (H4096,
-32 q / 8 KV heads x 128, F14336), batch 1, KV cache injected for positions
-[0, 2048), decode at positions 2048.. .  All inputs are seeded and synthetic.
+`--workload W` prints the same kind of line for one other workload.
 """
 from __future__ import annotations
 
@@ -19,6 +21,7 @@ import hashlib
 import json
 import os
 import re
+import subprocess
 import sys
 import time
 
@@ -32,7 +35,7 @@ import synth  # noqa: E402
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 METRIC = "stage decode tokens/s + achieved HBM GB/s (% of peak), batch 1 and 4"
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_decode_gateup_8b_mid.txt")
+RUNS = 5  # timed runs per measurement; the first is discarded, the median of the rest reported
 DECODE_SRC = os.path.join(ROOT, "paper_2609_34045_amd", "csrc", "decode.hip")
 
 
@@ -45,8 +48,11 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default="8b_mid", choices=[k for k in synth.WORKLOADS])
+    ap.add_argument("--workload", default=None, choices=[k for k in synth.WORKLOADS],
+                    help="one workload's line instead of the default (32B-shaped stage, batch 1 and 4)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="CPU oracle sample budget (0 disables)")
+    ap.add_argument("--no-prefill-key", action="store_true",
+                    help="leave the 70B-shaped prefill chunk out of the default line")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="skip the per-launch HIP-event pass (no roofline figure)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -98,14 +104,24 @@ def source_hash(path: str) -> str:
     return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
+def counters_file(wl_name: str) -> str:
+    return os.path.join(ROOT, "profiles", f"counters_decode_gateup_{wl_name}.txt")
+
+
 def traffic_from_counters(wl_name: str):
     """HBM bytes per gate/up launch from committed rocprofv3 counter runs, or None if absent or stale."""
-    if not os.path.exists(COUNTERS_FILE):
+    path = counters_file(wl_name)
+    if not os.path.exists(path):
         return None
-    rec = json.load(open(COUNTERS_FILE))
+    rec = json.load(open(path))
     if rec.get("workload") != wl_name or rec.get("decode_hip_sha256_16") != source_hash(DECODE_SRC):
         return None
     return rec.get("bytes_per_launch")
+
+
+def median_rule(times):
+    """Section VI's rule: the first run is cold and discarded; the median of the rest."""
+    return float(np.median(times[1:])) if len(times) > 1 else float(times[0])
 
 
 def prefill_flops(wl, T: int, pos0: int) -> float:
@@ -118,69 +134,106 @@ def prefill_flops(wl, T: int, pos0: int) -> float:
     return proj + attn
 
 
-def bench_prefill(args, wl, torch, kf):
-    """Time the chunk [ctx - T, ctx) on top of an injected cache [0, ctx - T), K times."""
+def measure_prefill(args, wl, torch, kf, kernel_events: bool = True) -> dict:
+    """The chunk [ctx - T, ctx) on top of an injected cache [0, ctx - T): RUNS runs of K chunks."""
     s = wl.shape
     T = wl.prefill_chunk
     ctx = wl.contexts[0]
     pos0 = ctx - T
+    t0 = time.perf_counter()
     layers = {l: synth.layer_weights(s, wl.cfg_id, l, wl.seed) for l in range(wl.layer_lo, wl.layer_hi)}
     g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, None)
+    del layers
     kv = g.kv(1, ctx + 8)
     for l in range(wl.layer_lo, wl.layer_hi):
         kb, vb = synth.injected_kv(s, wl.cfg_id, l, 0, pos0, wl.seed)
         kv.write(l, 0, 0, torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
-    del layers
     h = torch.from_numpy(synth.hidden_states(wl.cfg_id, synth.STREAM_PREFILL_HIDDEN, 0, T, s.hidden, wl.seed)).cuda()
     out = torch.empty_like(h)
+    torch.cuda.synchronize()
+    log(f"[bench] {wl.name} prefill stage ready in {time.perf_counter() - t0:.1f} s")
 
     def run(n):
         for _ in range(n):
             kv.set_len(0, pos0)
             g.prefill(kv, 0, pos0, hidden=h, out=out)
 
-    run(args.warmup)
+    steps = max(1, args.steps // 8)  # chunks per run (a chunk is ~10 ms at the 70B shape)
+    run(max(1, args.warmup // 4))
     g.sync()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    run(args.steps)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    times = []
+    for _ in range(RUNS):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(steps)
+        torch.cuda.synchronize()
+        times.append((time.perf_counter() - t0) / steps)
+    g.sync()
     prof = {}
-    if not args.no_kernel_events:
+    if kernel_events:
         g.profile(True)
-        run(args.steps)
+        run(steps)
         g.profile(False)
         prof = g.profile_read()
     fl = prefill_flops(wl, T, pos0)
-    ms = 1e3 * wall / args.steps
+    ms = 1e3 * median_rule(times)
     tf = fl / (ms * 1e-3) / 1e12
     dom = prof.get("pf_gateup", (0, 0.0))
     gu_fl = 2.0 * T * 2 * s.ffn * s.hidden
     gu_tf = gu_fl / (dom[1] / dom[0] * 1e-3) / 1e12 if dom[0] else None
-    line = {
-        "metric": "stage prefill TFLOP/s (% of bf16/fp16 matrix-core peak)",
-        "value": round(tf, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16", "data": "synthetic",
-        "config": {"workload": f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}), prefill chunk of {T} tokens at "
-                               f"positions [{pos0},{ctx}) over an injected cache", "chunk": T, "pos0": pos0},
-        "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+    kv.close()
+    g.close()
+    return {
+        "workload": f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}) of a {s.n_layers}-layer model, H{s.hidden}, "
+                    f"{s.n_q_heads}q/{s.n_kv_heads}kv x {s.head_dim}, F{s.ffn}; prefill chunk of {T} tokens at "
+                    f"positions [{pos0},{ctx}) over an injected cache",
+        "tflops": round(tf, 1), "ms_per_chunk": round(ms, 3), "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+        "peak_tflops": PEAK_BF16_TFLOPS, "algorithmic_flops_per_chunk": fl, "chunks_per_run": steps,
+        "run_ms": [round(1e3 * t, 3) for t in times],
         "roofline": {"kernel": "gate/up GEMM + SwiGLU (prefill)", "bound": "mfma",
                      "achieved": round(gu_tf, 1) if gu_tf else None, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(gu_tf / PEAK_BF16_TFLOPS, 4) if gu_tf else None, "traffic": None,
                      "algorithmic_flops_per_launch": gu_fl,
                      "avg_launch_us": round(1e3 * dom[1] / dom[0], 2) if dom[0] else None},
         "per_kernel": {k: {"launches": n, "avg_us": round(1e3 * t / n, 2)} for k, (n, t) in prof.items()},
-        "algorithmic_flops_per_chunk": fl,
+    }
+
+
+def bench_prefill(args, wl, torch, kf):
+    r = measure_prefill(args, wl, torch, kf, kernel_events=not args.no_kernel_events)
+    line = {
+        "metric": "stage prefill TFLOP/s (% of bf16/fp16 matrix-core peak)",
+        "value": r["tflops"], "unit": "TFLOP/s", "n_gpus": 1, "steps": r["chunks_per_run"], "warmup": args.warmup,
+        "ms_per_step": r["ms_per_chunk"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": r["workload"], "chunk": wl.prefill_chunk, "pos0": wl.contexts[0] - wl.prefill_chunk},
+        "timing": f"{RUNS} runs, first discarded, median",
+        "frac_of_peak": r["frac_of_peak"], "roofline": r["roofline"], "per_kernel": r["per_kernel"],
+        "algorithmic_flops_per_chunk": r["algorithmic_flops_per_chunk"], "run_ms": r["run_ms"],
     }
     print(json.dumps(line), flush=True)
-    kv.close()
-    g.close()
 
 
 # ------------------------------------------------------------------ CPU oracle baseline
-def cpu_baseline(wl, model_layers, kv_inject, hidden_steps, budget_s: float):
+def host_cpu() -> dict:
+    model = ""
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in out.splitlines():
+            if ln.startswith("Model name:"):
+                model = ln.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return {"host_cpus": os.cpu_count(), "cpu_model": model}
+
+
+def cpu_baseline(wl, layer_fn, kv_inject, hidden_steps, budget_s: float):
+    """The float64 oracle on this host's cores over the same decode steps, taken layer by layer: each layer
+    is widened once (outside the timed region), given its injected cache, and then decodes every step's
+    input, which is the previous layer's output for that step.  A layer's step depends only on the previous
+    layer's output for that step and on its own cache, so this is the stage's computation with one layer's
+    float64 weights in memory at a time.  Layers stop once `budget_s` of timed work is spent; the time per
+    step is then scaled from the layers done to the whole stage."""
     from threadpoolctl import threadpool_info
 
     from oracle import OracleStage
@@ -188,32 +241,42 @@ def cpu_baseline(wl, model_layers, kv_inject, hidden_steps, budget_s: float):
     s = wl.shape
     B = wl.batch
     ctx = list(wl.contexts)
-    o = OracleStage(s, wl.layer_lo, wl.layer_hi, model_layers, None, max_users=B,
-                    max_ctx=max(ctx) + len(hidden_steps) + 1, cache_weights=True)
-    t0 = time.perf_counter()
+    L = wl.layer_hi - wl.layer_lo
+    steps = len(hidden_steps)
+    xs = [np.asarray(h[:B], dtype=np.float64) for h in hidden_steps]
+    timed, widen_s, done_layers = 0.0, 0.0, 0
     for l in range(wl.layer_lo, wl.layer_hi):
-        o.weights(l)  # widen to float64 outside the timed region
-    widen_s = time.perf_counter() - t0
-    for (l, u), (kb, vb) in kv_inject.items():
-        o.kv.inject(l, u, 0, kb, vb)
-    for u in range(B):
-        o.kv.set_len(u, ctx[u])
-    done, t0 = 0, time.perf_counter()
-    while done < len(hidden_steps):
-        o.decode(list(range(B)), [ctx[u] + done for u in range(B)], hidden=hidden_steps[done])
-        done += 1
-        if time.perf_counter() - t0 >= budget_s:
+        o = OracleStage(s, l, l + 1, layer_fn, None, max_users=B, max_ctx=max(ctx) + steps + 1, cache_weights=True)
+        t0 = time.perf_counter()
+        o.weights(l)
+        widen_s += time.perf_counter() - t0
+        for u in range(B):
+            kb, vb = kv_inject[(l, u)]
+            o.kv.inject(l, u, 0, kb, vb)
+            o.kv.set_len(u, ctx[u])
+        t0 = time.perf_counter()
+        for i in range(steps):
+            xs[i] = o.decode(list(range(B)), [ctx[u] + i for u in range(B)], hidden=xs[i])
+        timed += time.perf_counter() - t0
+        done_layers += 1
+        del o
+        if timed >= budget_s:
             break
-    el = time.perf_counter() - t0
     threads = max([d.get("num_threads", 1) for d in threadpool_info() if d.get("user_api") == "blas"] or [1])
-    return {
-        "value": round(B * done / el, 3),
+    per_step = timed / steps * (L / done_layers)
+    rec = {
+        "value": round(B / per_step, 4),
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"{done} decode step(s) of the same stage, batch {B}, from the injected context "
-                  f"(float64 numpy oracle; {widen_s:.1f} s of weight widening excluded)",
+        "sample": f"{steps} decode steps at batch {B} from context {ctx[0]} through {done_layers} of the stage's "
+                  f"{L} layers, taken layer by layer ({timed:.1f} s timed"
+                  + (f", scaled by {L}/{done_layers} to the whole stage" if done_layers < L else "")
+                  + f"); float64 numpy oracle on the same weights, injected cache and hidden inputs; "
+                  f"{widen_s:.1f} s of weight widening excluded",
     }
+    rec.update(host_cpu())
+    return rec
 
 
 # ------------------------------------------------------------------ main
@@ -361,6 +424,144 @@ def bench_ring(args, torch, kf):
     }), flush=True)
 
 
+def setup_decode(args, torch, kf, wl, users_cap: int):
+    """The workload's stage with a cache of `users_cap` users, each holding its injected context."""
+    s = wl.shape
+    ctx = list(wl.contexts) + [wl.contexts[0]] * (users_cap - len(wl.contexts))
+    t0 = time.perf_counter()
+    layers = {l: synth.layer_weights(s, wl.cfg_id, l, wl.seed) for l in range(wl.layer_lo, wl.layer_hi)}
+    head = synth.head_weights(s, wl.cfg_id, wl.seed) if wl.has_head else None
+    log(f"[bench] generated {wl.name} weights in {time.perf_counter() - t0:.1f} s")
+    t0 = time.perf_counter()
+    g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, head)
+    if args.ordered:
+        g.set_flags(kf.KF_STAGE_ORDERED)
+    span = max(args.steps, args.warmup)
+    cap = max(ctx) + span + 1
+    page = 64
+    n_pages = sum((c + span + 1 + page - 1) // page for c in ctx) if args.paged else None
+    kv = g.kv(users_cap, cap, pages=n_pages)
+    inject = {}
+    for l in range(wl.layer_lo, wl.layer_hi):
+        for u in range(users_cap):
+            inject[(l, u)] = synth.injected_kv(s, wl.cfg_id, l, u, ctx[u], wl.seed)
+    # A paged cache gets its contexts one page per user in turn, so that each user's pages are scattered.
+    step_pos = page if args.paged else max(ctx)
+    for p0 in range(0, max(ctx), step_pos):
+        for u in range(users_cap):
+            m = min(step_pos, ctx[u] - p0)
+            if m <= 0:
+                continue
+            for l in range(wl.layer_lo, wl.layer_hi):
+                kb, vb = inject[(l, u)]
+                kv.write(l, u, p0, torch.from_numpy(kb[p0:p0 + m].view(np.int16)).cuda(),
+                         torch.from_numpy(vb[p0:p0 + m].view(np.int16)).cuda())
+            kv.set_len(u, p0 + m)
+    for u in range(users_cap):
+        kv.set_len(u, ctx[u])
+    torch.cuda.synchronize()
+    log(f"[bench] stage init + KV injection {time.perf_counter() - t0:.1f} s")
+    return g, kv, layers, inject, ctx
+
+
+def measure_decode(args, torch, g, kv, wl, B: int, ctx) -> dict:
+    """Decode at batch B (users 0..B-1 from their injected contexts): RUNS runs of K steps, each bracketed
+    by device synchronisations, the first discarded, the median of the rest; then HIP-event passes for the
+    dominant kernel and the per-kernel breakdown."""
+    s = wl.shape
+    users = list(range(B))
+    span = max(args.steps, args.warmup)
+    hs = [synth.hidden_states(wl.cfg_id, synth.STREAM_DECODE_HIDDEN, i, B, s.hidden, wl.seed) for i in range(span)]
+    hid = torch.from_numpy(np.stack(hs)).cuda()  # resident before the timed region
+    toks0 = torch.from_numpy(synth.tokens(wl.cfg_id, 0, B, s.vocab, wl.seed)).cuda() if wl.has_head else None
+    out = torch.empty((B, s.hidden), dtype=torch.float32, device="cuda")
+    toks = toks0
+
+    def run(n: int):
+        nonlocal toks
+        for i in range(n):
+            pos = [ctx[u] + i for u in users]
+            if wl.has_head:
+                g.decode(kv, users, pos, tokens=toks, out=out)
+                toks = g.head_argmax(out)  # closed-loop greedy decode
+            else:
+                g.decode(kv, users, pos, hidden=hid[i], out=out)
+
+    def reset():
+        nonlocal toks
+        toks = toks0
+        for u in users:
+            kv.set_len(u, ctx[u])
+
+    run(args.warmup)
+    g.sync()
+    times, gpu_times = [], []
+    for _ in range(RUNS):
+        reset()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        run(args.steps)
+        ev1.record()
+        torch.cuda.synchronize()
+        times.append((time.perf_counter() - t0) / args.steps)
+        gpu_times.append(ev0.elapsed_time(ev1) * 1e-3 / args.steps)
+    g.sync()
+    ms_step = 1e3 * median_rule(times)
+
+    # Kernel-timing passes: the same K steps again with HIP event pairs around
+    # launches on the stage's stream (each pair adds a few microseconds to the
+    # stream, so they stay out of the timed runs).  The roofline pass brackets
+    # only the dominant kernel; the breakdown pass brackets every launch.
+    prof, dom = {}, {}
+    if not args.no_kernel_events:
+        reset()
+        g.profile(True, classes=["gateup"])
+        run(args.steps)
+        g.profile(False)
+        dom = g.profile_read()
+        reset()
+        g.profile(True)
+        run(args.steps)
+        g.profile(False)
+        prof = g.profile_read()
+        g.sync()
+    reset()
+    sb = step_bytes(wl, [ctx[u] + args.steps // 2 for u in users])
+    hbm = sb / (ms_step * 1e-3) / 1e9
+    n_gu, t_gu = dom.get("gateup", (0, 0.0))
+    avg_gu_ms = t_gu / max(n_gu, 1)
+    gu_bytes = gateup_bytes(wl, B)
+    achieved = gu_bytes / (avg_gu_ms * 1e-3) / 1e9 if n_gu else None
+    total = max(sum(v[1] for v in prof.values()), 1e-9)
+    return {
+        "tokens_per_s": B / (ms_step * 1e-3),
+        "ms_per_step": ms_step,
+        "gpu_ms_per_step": 1e3 * median_rule(gpu_times),
+        "run_ms_per_step": [round(1e3 * t, 4) for t in times],
+        "hbm": {"algorithmic_bytes_per_step": sb, "achieved_gbps": round(hbm, 1),
+                "frac_of_peak": round(hbm / PEAK_HBM_GBPS, 4), "peak_gbps": PEAK_HBM_GBPS},
+        "roofline": {
+            "kernel": "gemv gate/up + RMSNorm + SwiGLU (decode)", "bound": "hbm",
+            "achieved": round(achieved, 1) if achieved else None, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4) if achieved else None,
+            "traffic": None, "algorithmic_bytes_per_launch": gu_bytes,
+            "avg_launch_us": round(avg_gu_ms * 1e3, 2), "launches": n_gu,
+        },
+        "per_kernel": {k: {"launches": n, "avg_us": round(1e3 * t / n, 2), "share": round(t / total, 4)}
+                       for k, (n, t) in prof.items()},
+        "hidden_steps": hs,
+    }
+
+
+def workload_text(wl, batches) -> str:
+    s = wl.shape
+    return (f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}) of a {s.n_layers}-layer model, H{s.hidden}, "
+            f"{s.n_q_heads}q/{s.n_kv_heads}kv x {s.head_dim}, F{s.ffn}" + (f", head V{s.vocab}" if wl.has_head else "")
+            + f"; decode at batch {' and '.join(str(b) for b in batches)}, contexts {list(wl.contexts)}")
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -382,171 +583,93 @@ def main():
         torch.cuda.synchronize()
         del a, b
         log(f"[bench] copied {args.copy_calibration_mb} MiB three times (calibration)")
+    torch.cuda.set_device(0)
     if args.cost_model:
-        torch.cuda.set_device(0)
         return bench_cost_model(args, torch, kf)
     if args.ring:
-        torch.cuda.set_device(0)
         return bench_ring(args, torch, kf)
-    wl = synth.WORKLOADS[args.workload]
     if args.prefill:
+        wl = synth.WORKLOADS[args.workload or "70b"]
         if not wl.prefill_chunk:
             sys.exit(f"workload {wl.name} has no prefill chunk")
-        torch.cuda.set_device(0)
         return bench_prefill(args, wl, torch, kf)
-    s, B = wl.shape, wl.batch
-    ctx = list(wl.contexts)
-    torch.cuda.set_device(0)
-    t0 = time.perf_counter()
-    layers = {l: synth.layer_weights(s, wl.cfg_id, l, wl.seed) for l in range(wl.layer_lo, wl.layer_hi)}
-    head = synth.head_weights(s, wl.cfg_id, wl.seed) if wl.has_head else None
-    log(f"[bench] generated {wl.name} weights in {time.perf_counter() - t0:.1f} s")
-    t0 = time.perf_counter()
-    g = kf.Stage(s, wl.layer_lo, wl.layer_hi, layers, head)
-    if args.ordered:
-        g.set_flags(kf.KF_STAGE_ORDERED)
-    span = max(args.steps, args.warmup)
-    cap = max(ctx) + span + 1
-    page = 64
-    n_pages = sum((c + span + 1 + page - 1) // page for c in ctx) if args.paged else None
-    kv = g.kv(B, cap, pages=n_pages)
-    inject = {}
-    for l in range(wl.layer_lo, wl.layer_hi):
-        for u in range(B):
-            inject[(l, u)] = synth.injected_kv(s, wl.cfg_id, l, u, ctx[u], wl.seed)
-    # A paged cache gets its contexts one page per user in turn, so that each user's pages are scattered.
-    step_pos = page if args.paged else max(ctx)
-    for p0 in range(0, max(ctx), step_pos):
-        for u in range(B):
-            m = min(step_pos, ctx[u] - p0)
-            if m <= 0:
-                continue
-            for l in range(wl.layer_lo, wl.layer_hi):
-                kb, vb = inject[(l, u)]
-                kv.write(l, u, p0, torch.from_numpy(kb[p0:p0 + m].view(np.int16)).cuda(),
-                         torch.from_numpy(vb[p0:p0 + m].view(np.int16)).cuda())
-            kv.set_len(u, p0 + m)
-    for u in range(B):
-        kv.set_len(u, ctx[u])
-    torch.cuda.synchronize()
-    log(f"[bench] stage init + KV injection {time.perf_counter() - t0:.1f} s")
 
-    hs = [synth.hidden_states(wl.cfg_id, synth.STREAM_DECODE_HIDDEN, i, B, s.hidden, wl.seed) for i in range(span)]
-    hid = torch.from_numpy(np.stack(hs)).cuda()  # resident before the timed region
-    toks = torch.from_numpy(synth.tokens(wl.cfg_id, 0, B, s.vocab, wl.seed)).cuda() if wl.has_head else None
-    out = torch.empty((B, s.hidden), dtype=torch.float32, device="cuda")
-    users = list(range(B))
-
-    def run(n: int):
-        nonlocal toks
-        for i in range(n):
-            pos = [ctx[u] + i for u in users]
-            if wl.has_head:
-                g.decode(kv, users, pos, tokens=toks, out=out)
-                toks = g.head_argmax(out)  # closed-loop greedy decode
-            else:
-                g.decode(kv, users, pos, hidden=hid[i], out=out)
-
-    def reset():
-        for u in users:
-            kv.set_len(u, ctx[u])
-
-    run(args.warmup)
-    g.sync()
-    reset()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    run(args.steps)
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms_step = ev0.elapsed_time(ev1) / args.steps
-    ms_step = 1e3 * wall / args.steps
-    tok_s = B * args.steps / (wall if wall > 0 else 1e-9)
-    g.sync()
-
-    # Kernel-timing passes: the same K steps again with HIP event pairs around
-    # launches (each pair adds a few microseconds to the stream, so they stay out
-    # of the timed region above).  The roofline pass brackets only the dominant
-    # kernel; the breakdown pass brackets every launch.
-    prof, dom = {}, {}
-    if not args.no_kernel_events:
-        reset()
-        g.profile(True, classes=["gateup"])
-        run(args.steps)
-        g.profile(False)
-        dom = g.profile_read()
-        reset()
-        g.profile(True)
-        run(args.steps)
-        g.profile(False)
-        prof = g.profile_read()
-        g.sync()
-    positions_mid = [ctx[u] + args.steps // 2 for u in users]
-    sb = step_bytes(wl, positions_mid)
-    hbm = sb / (ms_step * 1e-3) / 1e9
-
-    # dominant kernel: the fused RMSNorm + gate/up + SwiGLU GEMV
-    n_gu, t_gu = dom.get("gateup", (0, 0.0))
-    avg_gu_ms = t_gu / max(n_gu, 1)
-    gu_bytes = gateup_bytes(wl, B)
-    achieved = gu_bytes / (avg_gu_ms * 1e-3) / 1e9 if n_gu else None
-    per_kernel = {k: {"launches": n, "avg_us": round(1e3 * t / n, 2), "share": round(t / max(sum(v[1] for v in
-                  prof.values()), 1e-9), 4)} for k, (n, t) in prof.items()}
+    # The default line: the 32B-shaped stage at batch 1 (value) and batch 4; otherwise one workload.
+    combined = args.workload is None
+    wl = synth.WORKLOADS["32b_b1" if combined else args.workload]
+    wl4 = synth.WORKLOADS["32b_b4"] if combined else None
+    B = wl.batch
+    g, kv, layers, inject, ctx = setup_decode(args, torch, kf, wl4 if combined else wl, 4 if combined else B)
+    r1 = measure_decode(args, torch, g, kv, wl, B, ctx)
+    log(f"[bench] {wl.name} batch {B}: {r1['tokens_per_s']:.1f} tokens/s, {r1['ms_per_step']:.3f} ms/step")
+    r4 = None
+    if combined:
+        r4 = measure_decode(args, torch, g, kv, wl4, 4, ctx)
+        log(f"[bench] {wl4.name} batch 4: {r4['tokens_per_s']:.1f} tokens/s, {r4['ms_per_step']:.3f} ms/step")
+    kv.close()
+    g.close()
+    torch.cuda.empty_cache()
 
     cpu = None
     if args.cpu_seconds > 0:
-        cpu = cpu_baseline(wl, lambda l: layers[l], inject, hs, args.cpu_seconds)
+        cpu = cpu_baseline(wl, lambda l: layers[l], inject, r1["hidden_steps"], args.cpu_seconds)
         log(f"[bench] cpu oracle {cpu['value']} tokens/s on {cpu['cores']} threads")
+    del layers, inject
 
-    traffic = traffic_from_counters(wl.name)
+    from paper_2609_34045_amd import planner
+    probe_bw = planner.probe_bandwidth(4 << 30, reps=5)
+
+    pf = None
+    if combined and not args.no_prefill_key:
+        pf = measure_prefill(args, synth.WORKLOADS["70b"], torch, kf)
+        log(f"[bench] 70b prefill chunk {pf['tflops']} TFLOP/s ({pf['frac_of_peak']:.3f} of peak)")
+
+    r1["roofline"]["traffic"] = traffic_from_counters(wl.name)
     line = {
         "metric": METRIC,
-        "value": round(tok_s, 2),
+        "value": round(r1["tokens_per_s"], 2),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
-        "gpu_ms_per_step": round(gpu_ms_step, 4),
+        "ms_per_step": round(r1["ms_per_step"], 4),
+        "gpu_ms_per_step": round(r1["gpu_ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f16",  # fp16 weight matrices and KV cache, fp32 sums
         "data": "synthetic",
         "config": {
-            "workload": f"{wl.name}: layers [{wl.layer_lo},{wl.layer_hi}) of a {s.n_layers}-layer model, H{s.hidden}, "
-                        f"{s.n_q_heads}q/{s.n_kv_heads}kv x {s.head_dim}, F{s.ffn}"
-                        + (f", head V{s.vocab}" if wl.has_head else "") + f"; batch {B}, contexts {ctx}, decode",
-            "batch": B,
-            "contexts": ctx,
+            "workload": workload_text(wl4 if combined else wl, [1, 4] if combined else [B])
+                        + ("; value = batch 1, batch4 = batch 4" if combined else ""),
+            "batch": [1, 4] if combined else B,
+            "contexts": ctx if combined else list(wl.contexts),
             "layers": wl.layer_hi - wl.layer_lo,
             "has_head": wl.has_head,
             "kv_cache": "paged: 64-position pages from a shared pool, scattered" if args.paged else "reserved per user",
+            "output_projection": "ordered (fixed-order sums)" if args.ordered else "fused (arrival-order sums)",
             "parallelism": "single GPU (one stage)",
         },
-        "hbm": {"algorithmic_bytes_per_step": sb, "achieved_gbps": round(hbm, 1),
-                "frac_of_peak": round(hbm / PEAK_HBM_GBPS, 4), "peak_gbps": PEAK_HBM_GBPS},
-        "roofline": {
-            "kernel": "gemv gate/up + RMSNorm + SwiGLU (decode)",
-            "bound": "hbm",
-            "achieved": round(achieved, 1) if achieved else None,
-            "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBPS, 4) if achieved else None,
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": gu_bytes,
-            "avg_launch_us": round(avg_gu_ms * 1e3, 2),
-            "launches": n_gu,
-        },
-        "per_kernel": per_kernel,
-        "cpu_baseline": cpu,
+        "timing": f"{RUNS} runs of {args.steps} steps after {args.warmup} warmup steps, each run bracketed by device "
+                  f"synchronisations, the first run discarded, the median of the rest (paper, Section VI)",
+        "run_ms_per_step": r1["run_ms_per_step"],
+        "hbm": r1["hbm"],
+        "roofline": r1["roofline"],
+        "per_kernel": r1["per_kernel"],
     }
+    if r4 is not None:
+        r4["roofline"]["traffic"] = traffic_from_counters(wl4.name)
+        line["batch4"] = {
+            "value": round(r4["tokens_per_s"], 2), "unit": "tokens/s", "ms_per_step": round(r4["ms_per_step"], 4),
+            "gpu_ms_per_step": round(r4["gpu_ms_per_step"], 4), "run_ms_per_step": r4["run_ms_per_step"],
+            "hbm": r4["hbm"], "roofline": r4["roofline"], "per_kernel": r4["per_kernel"],
+        }
+    if pf is not None:
+        line["prefill_70b"] = pf
+    line["probe"] = {"attainable_read_gbps": round(probe_bw / 1e9, 1), "buffer_gib": 4,
+                     "note": "streaming-read probe on this GPU (context; fractions are against 8 TB/s)"}
+    line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
-    kv.close()
-    g.close()
 
 
 if __name__ == "__main__":
