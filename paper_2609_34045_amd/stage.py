@@ -194,6 +194,15 @@ class Stage:
         self.handle = handle
         self._lib = lib
 
+    @classmethod
+    def adopt(cls, shape, lo: int, hi: int, has_head: bool, handle, stream) -> "Stage":
+        """A Stage object for a kf_stage the library created elsewhere (e.g. kf_shard_stage_init)."""
+        self = cls.__new__(cls)
+        self.shape, self.lo, self.hi, self.has_head = shape, lo, hi, bool(has_head)
+        self._cfg = ModelConfig.of(shape)
+        self.stream, self.handle, self._lib = stream, handle, load_library()
+        return self
+
     # -- lifetime
     def close(self):
         if self.handle:

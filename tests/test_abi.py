@@ -38,9 +38,9 @@ def test_header_declares_the_boundary():
 
 
 def test_library_exports_every_declared_symbol(lib):
-    from paper_2609_34045_amd import planner, ring, stage
+    from paper_2609_34045_amd import planner, ring, shard, stage
     names = declared_functions()
-    assert set(names) == set(stage.EXPORTS) | set(planner.EXPORTS) | set(ring.EXPORTS)
+    assert set(names) == set(stage.EXPORTS) | set(planner.EXPORTS) | set(ring.EXPORTS) | set(shard.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
 
