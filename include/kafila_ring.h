@@ -80,6 +80,9 @@ kf_status kf_ring_prefill(kf_ring* ring, int32_t user, int32_t n_tokens, const i
  *     ready when the call is made.
  *   tokens_out_dev int32 [steps, U]: row t receives the tokens sampled at step t, which
  *     are the inputs of step t + 1.
+ *   hidden_out_dev [steps, U, H] in the ring's io type, or NULL: row (t, j) receives the
+ *     hidden state user j's token of step t returned to the head with (the last member's
+ *     output, from which the head sampled row (t, j) of tokens_out_dev).
  * Every user's length advances by `steps` in every member.  A member with a paged
  * cache must have free pages for every user's `steps` more positions, counted from
  * the user's length (KF_ENOMEM otherwise, nothing enqueued).  Work is enqueued in the
@@ -88,7 +91,8 @@ kf_status kf_ring_prefill(kf_ring* ring, int32_t user, int32_t n_tokens, const i
  * the call enqueues is ordered before the last work it puts on stages[0]'s stream.
  */
 kf_status kf_ring_generate(kf_ring* ring, int32_t n_groups, const int32_t* group_size, const int32_t* users,
-                           const int32_t* tokens_in_dev, int32_t steps, int32_t* tokens_out_dev);
+                           const int32_t* tokens_in_dev, int32_t steps, int32_t* tokens_out_dev,
+                           void* hidden_out_dev);
 
 /* Wait for every member's stream; KF_EDEVICE if any enqueued work failed. */
 kf_status kf_ring_sync(kf_ring* ring);

@@ -45,7 +45,8 @@ extern "C" {
                             3: paged KV caches, kf_stage_describe, kf_kv_describe;
                             4: kf_stage_set_flags / kf_stage_get_flags (KF_STAGE_ORDERED), range and
                                NaN-logit errors reported by kf_stage_sync, token -1 for a row of NaN logits,
-                               kf_stage_prefill_noalloc */
+                               kf_stage_prefill_noalloc; kf_ring_generate's hidden_out_dev (kafila_ring.h);
+                               the kf_shard_* loader (kafila_shard.h) */
 #define KF_KV_PAGE 64     /* positions per KV cache page */
 #define KF_MAX_BATCH 4
 

@@ -229,7 +229,8 @@ kf_status kf_ring_prefill(kf_ring* r, int32_t user, int32_t n_tokens, const int3
 }
 
 kf_status kf_ring_generate(kf_ring* r, int32_t n_groups, const int32_t* group_size, const int32_t* users,
-                           const int32_t* tokens_in_dev, int32_t steps, int32_t* tokens_out_dev) {
+                           const int32_t* tokens_in_dev, int32_t steps, int32_t* tokens_out_dev,
+                           void* hidden_out_dev) {
   if (!r) return fail(KF_EINVAL, "ring is NULL");
   if (!group_size || !users || !tokens_in_dev || !tokens_out_dev) return fail(KF_EINVAL, "NULL argument");
   if (n_groups < 1 || n_groups > r->max_groups)
@@ -254,6 +255,12 @@ kf_status kf_ring_generate(kf_ring* r, int32_t n_groups, const int32_t* group_si
   // The return leg of group g's previous step: the head samples from the last member's rows.
   auto sample = [&](int g, int t) -> kf_status {
     KF_RING_HIP(hipStreamWaitEvent(r->stream[0], r->ev[(size_t)g * m + m - 1], 0), "return-leg wait");
+    if (hidden_out_dev) {
+      const size_t row = (size_t)r->hidden * r->esize;
+      KF_RING_HIP(hipMemcpyAsync(static_cast<char*>(hidden_out_dev) + ((size_t)t * U + off[g]) * row, r->hid(g, m - 1),
+                                 (size_t)group_size[g] * row, hipMemcpyDeviceToDevice, r->stream[0]),
+                  "return-leg copy");
+    }
     return kf_head_argmax(r->st[0], group_size[g], r->hid(g, m - 1), r->io, tokens_out_dev + (size_t)t * U + off[g],
                           nullptr);
   };

@@ -27,7 +27,7 @@ def _lib():
         "kf_ring_create": (I32, [I32, ctypes.POINTER(P), ctypes.POINTER(P), I32, I32, I32, ctypes.POINTER(P)]),
         "kf_ring_destroy": (I32, [P]),
         "kf_ring_prefill": (I32, [P, I32, I32, VP, VP]),
-        "kf_ring_generate": (I32, [P, I32, I32P, I32P, VP, I32, VP]),
+        "kf_ring_generate": (I32, [P, I32, I32P, I32P, VP, I32, VP, VP]),
         "kf_ring_sync": (I32, [P]),
     }
     for name, (res, args) in sig.items():
@@ -61,7 +61,7 @@ class Ring:
         h = ctypes.c_void_p()
         dtype = _stage.KF_F32 if io == torch.float32 else _stage.KF_BF16
         _stage._check(lib.kf_ring_create(m, st, kv, max_groups, max_prefill, dtype, ctypes.byref(h)), "kf_ring_create")
-        self.handle, self._lib = h, lib
+        self.handle, self._lib, self.io = h, lib, io
 
     def close(self):
         if self.handle:
@@ -89,10 +89,11 @@ class Ring:
         self._in_use(tokens, nxt)
         return nxt
 
-    def generate(self, groups, tokens_in, steps: int, out=None):
+    def generate(self, groups, tokens_in, steps: int, out=None, hidden_out=None):
         """``groups``: lists of user ids; ``tokens_in``: device int32 [U] in the same order (ready).
 
-        Returns device int32 [steps, U]: the tokens sampled at each step.
+        Returns device int32 [steps, U]: the tokens sampled at each step.  ``hidden_out`` (optional device
+        tensor [steps, U, H] of the ring's io dtype) receives the hidden rows each token was sampled from.
         """
         import torch
         sizes = [len(g) for g in groups]
@@ -105,9 +106,13 @@ class Ring:
             out = torch.empty((max(steps, 0), U), dtype=torch.int32, device=tokens_in.device)
         gs = (ctypes.c_int32 * max(len(sizes), 1))(*sizes)
         us = (ctypes.c_int32 * max(U, 1))(*users)
+        if hidden_out is not None:
+            _stage._require_device(hidden_out, "hidden_out")
+            if tuple(hidden_out.shape) != (steps, U, self.stages[0].shape.hidden) or hidden_out.dtype != self.io:
+                raise ValueError("hidden_out must be [steps, U, H] of the ring's hand-off dtype")
         _stage._check(self._lib.kf_ring_generate(self.handle, len(sizes), gs, us, _stage._ptr(tokens_in), steps,
-                                                 _stage._ptr(out)), "kf_ring_generate")
-        self._in_use(tokens_in, out)
+                                                 _stage._ptr(out), _stage._ptr(hidden_out)), "kf_ring_generate")
+        self._in_use(tokens_in, out, *([hidden_out] if hidden_out is not None else []))
         return out
 
     def _in_use(self, *tensors):

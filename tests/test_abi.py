@@ -208,7 +208,7 @@ def test_ring_rejects_before_touching_the_device(lib):
     assert b"stages[0]" in lib.kf_last_error()
     assert r.kf_ring_create(1, (P * 1)(), (P * 1)(), 4, 8, 0, None) == 1
     one = (ctypes.c_int32 * 1)(1)
-    assert r.kf_ring_generate(None, 1, one, one, P(8), 1, P(8)) == 1
+    assert r.kf_ring_generate(None, 1, one, one, P(8), 1, P(8), None) == 1
     assert r.kf_ring_prefill(None, 0, 1, P(8), P(8)) == 1
     assert r.kf_ring_sync(None) == 1
     assert r.kf_ring_destroy(None) == 1
