@@ -530,146 +530,6 @@ void gemv_kernel(const GemvParams p) {
   gemv_epilogue<B, R, EPI, NORM, T>(p, wg, fin, tid, pre);
 }
 
-// ------------------------------------------------------------------ batch 2-4 GEMV, rows per wave
-// From batch 2 the row-owning workgroups above re-read every input row once per
-// R weight rows, which at batch 4 moves half as many bytes through the caches as
-// the weights themselves (a timing probe with cache-resident inputs ran the 32B-
-// shaped batch-4 step 7% faster).  Here each wave owns RW weight rows and walks
-// the whole of K (lane l takes chunk 64 s + l of each row at step s, so each load
-// is 1 KB contiguous per row), and the workgroup's four waves share the input
-// rows: each step's input chunks, and the norm gain, are copied once into an LDS
-// tile by direct global-to-LDS loads, KF_WAVE_TS steps per tile, double-buffered.
-// The input bytes per weight byte drop fourfold, and a lane holds one batch row's
-// input at a time.  A wave's RW x B sums are reduced within the wave; the
-// epilogues are those of the row-owning kernel, applied to the wave's rows as a
-// workgroup of RW rows (virtual workgroup 4 * blockIdx + wave).
-typedef __attribute__((address_space(3))) void* lds_ptr;
-
-// Wait until at most N vector-memory operations of this wave are outstanding.
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
-}
-
-// Workgroup barrier that orders LDS accesses without waiting on outstanding
-// global loads (the compiler may not move memory operations across it).
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-#ifndef KF_WAVE_TS
-#define KF_WAVE_TS 2
-#endif
-#ifndef KF_WAVE_MIN_WAVES
-#define KF_WAVE_MIN_WAVES 4
-#endif
-template <int B, int RW, int EPI, bool NORM>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KF_WAVE_MIN_WAVES)))
-void gemv_wave_kernel(const GemvParams p) {
-  constexpr int TS = KF_WAVE_TS;            // K steps per LDS tile
-  constexpr int UPS = B + (NORM ? 1 : 0);   // 1 KB load units per step: one per batch row, then the gain
-  constexpr int NV = RW * B + (NORM ? B : 0);
-  constexpr int NVP = NV <= 8 ? 8 : NV <= 16 ? 16 : NV <= 32 ? 32 : 64;
-  static_assert(NV <= 64, "too many partial sums per wave");
-  static_assert(B >= 2 && B <= kMaxBatch, "batch 2-4");
-  constexpr int LPI = 64 / NVP;  // lanes sharing one reduced value
-  __shared__ __attribute__((aligned(1024))) uint8_t tile[2][TS * UPS * 1024];
-  __shared__ float fin[4][NVP];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int vwg = blockIdx.x * 4 + wave;
-  const int K = p.K, nch = K >> 3;
-  const int nsteps = (nch + 63) >> 6, ntiles = (nsteps + TS - 1) / TS;
-
-  const v4u* wrow[RW];
-  bool rok[RW];
-#pragma unroll
-  for (int r = 0; r < RW; ++r) wrow[r] = reinterpret_cast<const v4u*>(gemv_row<RW, EPI>(p, vwg, r, rok[r]));
-  const EpiPre pre = gemv_epi_prefetch<B, RW, EPI>(p, vwg, lane);
-  const uint16_t* in16 = reinterpret_cast<const uint16_t*>(p.in);
-
-  // Unit j of tile t: step t * TS + j / UPS, batch row j % UPS (UPS - 1: the gain).
-  // Lanes past the last chunk copy chunk 0 of the row (their products are skipped).
-  auto load_tile = [&](int t, int buf) {
-    for (int j = wave; j < TS * UPS; j += 4) {
-      const int st = j / UPS, q = j % UPS, s = t * TS + st;
-      if (s >= nsteps) break;
-      int c = s * 64 + lane;
-      if (c >= nch) c = 0;
-      const uint16_t* src = (NORM && q == B) ? p.gain + c * 8 : in16 + (int64_t)q * K + c * 8;
-      __builtin_amdgcn_global_load_lds(src, (lds_ptr)(tile[buf] + j * 1024), 16, 0, 0);
-    }
-  };
-
-  float acc[NVP];
-#pragma unroll
-  for (int i = 0; i < NVP; ++i) acc[i] = 0.f;
-
-  load_tile(0, 0);
-  wait_vm<0>();
-  lds_barrier();
-  for (int t = 0; t < ntiles; ++t) {
-    if (t + 1 < ntiles) load_tile(t + 1, (t + 1) & 1);
-    const uint8_t* tb = tile[t & 1];
-#pragma unroll
-    for (int st = 0; st < TS; ++st) {
-      const int s = t * TS + st;
-      if (s >= nsteps) break;
-      const int c = s * 64 + lane;
-      const bool cok = c < nch;
-      v4u wv[RW];
-#pragma unroll
-      for (int r = 0; r < RW; ++r) wv[r] = cok && rok[r] ? ld_stream(wrow[r] + c) : v4u{0u, 0u, 0u, 0u};
-      // every weight load is issued before the arithmetic on the chunk
-      __builtin_amdgcn_sched_barrier(0);
-      if (!cok) continue;
-      float gf[8];
-      if (NORM) bf16x8(*reinterpret_cast<const v4u*>(tb + (st * UPS + B) * 1024 + lane * 16), gf);
-#pragma unroll
-      for (int b = 0; b < B; ++b) {
-        const v4u xr = *reinterpret_cast<const v4u*>(tb + (st * UPS + b) * 1024 + lane * 16);
-        h2 xp[4];
-        if (NORM) {  // x * gain rounded to fp16; sum(x^2) in fp32
-          float f[8];
-          f16x8_apart(xr, f);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) acc[RW * B + b] += f[i] * f[i];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) xp[j] = __builtin_convertvector(f2{f[2 * j] * gf[2 * j], f[2 * j + 1] * gf[2 * j + 1]}, h2);
-        } else {
-          const h8 x8 = __builtin_bit_cast(h8, xr);
-          xp[0] = __builtin_shufflevector(x8, x8, 0, 1);
-          xp[1] = __builtin_shufflevector(x8, x8, 2, 3);
-          xp[2] = __builtin_shufflevector(x8, x8, 4, 5);
-          xp[3] = __builtin_shufflevector(x8, x8, 6, 7);
-        }
-#pragma unroll
-        for (int r = 0; r < RW; ++r) {
-          const h8 w8 = __builtin_bit_cast(h8, wv[r]);
-          float a = acc[r * B + b];
-          a = __builtin_amdgcn_fdot2(__builtin_shufflevector(w8, w8, 0, 1), xp[0], a, false);
-          a = __builtin_amdgcn_fdot2(__builtin_shufflevector(w8, w8, 2, 3), xp[1], a, false);
-          a = __builtin_amdgcn_fdot2(__builtin_shufflevector(w8, w8, 4, 5), xp[2], a, false);
-          acc[r * B + b] = __builtin_amdgcn_fdot2(__builtin_shufflevector(w8, w8, 6, 7), xp[3], a, false);
-        }
-      }
-    }
-    // this wave's copies into the next tile have landed, and every wave is done
-    // with this tile before it is overwritten two tiles on
-    wait_vm<0>();
-    lds_barrier();
-  }
-
-  Butterfly<NVP, 32>::run(acc, lane);
-  if ((lane & (LPI - 1)) == 0) fin[wave][lane / LPI] = acc[0];
-  __syncthreads();
-  gemv_epilogue<B, RW, EPI, NORM, 64>(p, vwg, fin[wave], lane, pre);
-}
-
 // ------------------------------------------------------------------ attention
 // Workgroup (split s, KV head g, row b) covers keys [s*split, min((s+1)*split, len_b)).
 // A key's hd elements are read by hd/8 lanes, 16 bytes each; all G query heads of
@@ -732,7 +592,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   // previous kernel has just written.  DEPTH chunks per wave are in flight:
   // slot s holds the chunk processed at steps s, s + DEPTH, ... and is reloaded
   // with the chunk DEPTH steps ahead once its values are in registers.
-  static_assert(DEPTH >= 1 && DEPTH <= 4, "one to four chunks in flight");
+  static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
   int c0 = wave * CH;
   v4u kw[DEPTH][J], vw[DEPTH][J];
   bool ok[DEPTH][J];
@@ -749,13 +609,9 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
     }
   };
   using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, (DEPTH > 1 ? 1 : 0)>;
-  using S2 = std::integral_constant<int, (DEPTH > 2 ? 2 : 0)>;
-  using S3 = std::integral_constant<int, (DEPTH > 3 ? 3 : 0)>;
+  using S1 = std::integral_constant<int, DEPTH - 1>;
   if (c0 < nk) load_chunk(c0, S0{});
   if (DEPTH > 1 && c0 + 4 * CH < nk) load_chunk(c0 + 4 * CH, S1{});
-  if (DEPTH > 2 && c0 + 8 * CH < nk) load_chunk(c0 + 8 * CH, S2{});
-  if (DEPTH > 3 && c0 + 12 * CH < nk) load_chunk(c0 + 12 * CH, S3{});
 
   // Blocks with q/k norms: the workgroup whose split holds row b's new key
   // requests that key's raw projection now, so that its latency overlaps the
@@ -919,20 +775,12 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
       }
     }
   };
-  while (c0 < nk) {  // slots in rotation: slot i holds the chunks processed at steps i, i + DEPTH, ...
+  while (c0 < nk) {
     step(S0{});
     c0 += 4 * CH;
     if (DEPTH > 1 && c0 < nk) {
       step(S1{});
       c0 += 4 * CH;
-      if (DEPTH > 2 && c0 < nk) {
-        step(S2{});
-        c0 += 4 * CH;
-        if (DEPTH > 3 && c0 < nk) {
-          step(S3{});
-          c0 += 4 * CH;
-        }
-      }
     }
   }
 
@@ -1355,32 +1203,6 @@ static hipError_t gemv_dispatch_b(int epi, bool norm, const GemvParams& p, int g
   }
 }
 
-template <int B, int RW>
-static hipError_t wave_launch_b(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
-  if (epi == kEpiQKV && norm) hipLaunchKernelGGL((gemv_wave_kernel<B, RW, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
-  else if (epi == kEpiSwiGLU && norm)
-    hipLaunchKernelGGL((gemv_wave_kernel<B, RW, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
-  else if (epi == kEpiResid && !norm)
-    hipLaunchKernelGGL((gemv_wave_kernel<B, RW, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
-int gemv_grid(int epi, int R, const GemvParams& p);
-
-hipError_t launch_gemv_wave(int epi, int RW, bool norm, const GemvParams& p, hipStream_t s) {
-  if (p.batch < 2 || p.batch > kMaxBatch || !p.in16 || p.src || p.tokens) return hipErrorInvalidValue;
-  const int nv = gemv_grid(epi, RW, p);  // waves: virtual workgroups of RW rows
-  if (epi != kEpiResid && nv % 4) return hipErrorInvalidValue;  // QKV and SwiGLU rows come in whole workgroups
-  const int grid = (nv + 3) / 4;
-#define KF_WAVE_CASE(BB, RR) \
-  if (p.batch == BB && RW == RR) return wave_launch_b<BB, RR>(epi, norm, p, grid, s);
-  KF_WAVE_CASE(2, 8) KF_WAVE_CASE(3, 8) KF_WAVE_CASE(4, 8)
-  KF_WAVE_CASE(2, 4) KF_WAVE_CASE(3, 4) KF_WAVE_CASE(4, 4)
-#undef KF_WAVE_CASE
-  return hipErrorInvalidValue;
-}
-
 int gemv_grid(int epi, int R, const GemvParams& p) {
   switch (epi) {
     case kEpiQKV: return (p.nq + 2 * p.nkv) * (p.hd / R);
@@ -1418,44 +1240,23 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
       default: return hipErrorInvalidValue;
     }
   }
-  // QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups of the
-  // 8-row launch (batch 1: 0.1 us faster per layer at the 8B shape).
-  if (R == 4 && U == 1 && epi == kEpiQKV && norm) {
-    if ((p.batch > 1) != (p.in16 != 0)) return hipErrorInvalidValue;  // fp16 input rows exactly from batch 2
-    switch (p.batch) {
-      case 1:
-        hipLaunchKernelGGL((gemv_kernel<1, 4, 1, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
-        break;
-      case 2: hipLaunchKernelGGL((gemv_kernel<2, 4, 1, kEpiQKV, true, false, true>), dim3(grid), dim3(256), 0, s, p); break;
-      case 3: hipLaunchKernelGGL((gemv_kernel<3, 4, 1, kEpiQKV, true, false, true>), dim3(grid), dim3(256), 0, s, p); break;
-      case 4: hipLaunchKernelGGL((gemv_kernel<4, 4, 1, kEpiQKV, true, false, true>), dim3(grid), dim3(256), 0, s, p); break;
-      default: return hipErrorInvalidValue;
-    }
+  // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
+  // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.
+  if (R == 4 && U == 1 && epi == kEpiQKV && p.batch == 1 && norm && !p.in16) {
+    hipLaunchKernelGGL((gemv_kernel<1, 4, 1, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;
 }
 
-#ifndef KF_ATTN_DEPTH_B1
-#define KF_ATTN_DEPTH_B1 0  // 0: two chunks in flight from 512 keys per split, else one
-#endif
-#ifndef KF_ATTN_DEPTH_BATCHED
-#define KF_ATTN_DEPTH_BATCHED 1
-#endif
 template <int HD, int G>
 static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
   const dim3 grid(p.n_split, p.nkv, batch);
   // Two chunks in flight per wave pay off only where few workgroups stream long
   // splits (batch 1, 512 keys or more: 8B-shaped 32K context 33.9 -> 29.8 us);
   // elsewhere the 36 extra VGPRs cost more in occupancy than they gain.
-  const int depth = batch > 1 ? KF_ATTN_DEPTH_BATCHED : KF_ATTN_DEPTH_B1 ? KF_ATTN_DEPTH_B1 : p.split >= 512 ? 2 : 1;
-  switch (depth) {
-    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, G, 2>), grid, dim3(256), 0, s, p); break;
-#if KF_ATTN_DEPTH_BATCHED == 4 || KF_ATTN_DEPTH_B1 == 4
-    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, G, 4>), grid, dim3(256), 0, s, p); break;
-#endif
-    default: hipLaunchKernelGGL((attn_decode_kernel<HD, G, 1>), grid, dim3(256), 0, s, p); break;
-  }
+  if (batch == 1 && p.split >= 512) hipLaunchKernelGGL((attn_decode_kernel<HD, G, 2>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((attn_decode_kernel<HD, G, 1>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

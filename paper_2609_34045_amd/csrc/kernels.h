@@ -157,9 +157,6 @@ struct AttnParams {
 // Launchers (return hipGetLastError() of the launch).
 int gemv_grid(int epi, int rows_per_wg, const GemvParams& p);
 hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p, hipStream_t s);
-// Batch 2-4 GEMV over fp16 input rows (p.in16) in which each wave owns RW rows and
-// the workgroup's four waves share the input rows through LDS (QKV, SwiGLU, residual).
-hipError_t launch_gemv_wave(int epi, int rows_per_wave, bool norm, const GemvParams& p, hipStream_t s);
 // The same launch with the stage input (p.src or p.tokens) as its input rows.
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);

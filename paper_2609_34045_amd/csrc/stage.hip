@@ -23,19 +23,6 @@ using namespace kf;
 // flight per thread (other shapes were measured slower at every batch).
 constexpr int kGemvRows = 8, kGemvChunks = 1;
 constexpr int kQkvRowsBatch1 = 4;  // the batch-1 QKV launch (after the first layer) takes 4-row workgroups
-#ifndef KF_WAVE_GATEUP
-#define KF_WAVE_GATEUP 0  // batch 2-4 gate/up through the per-wave GEMV (measured slower; off)
-#endif
-#ifndef KF_WAVE_QKV
-#define KF_WAVE_QKV 0
-#endif
-#ifndef KF_WAVE_RW
-#define KF_WAVE_RW 8
-#endif
-#ifndef KF_QKV_ROWS_BATCHED
-#define KF_QKV_ROWS_BATCHED 8
-#endif
-constexpr int kQkvRowsBatched = KF_QKV_ROWS_BATCHED;  // rows per workgroup of the batch 2-4 QKV launch
 
 // Rows per workgroup of a residual GEMV with n output rows: 8, unless that
 // leaves the grid a fraction of a round over the compute units and 4 rows do
@@ -882,9 +869,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
       g.in16 = 0;  // the input rows come from src / tokens
       le = launch_gemv_src(kEpiQKV, kGemvRows, kGemvChunks, true, g, st);
     } else {
-      le = batch > 1 && (KF_WAVE_QKV) ? launch_gemv_wave(kEpiQKV, KF_WAVE_RW, true, g, st)
-                                       : launch_gemv(kEpiQKV, batch == 1 ? kQkvRowsBatch1 : kQkvRowsBatched, kGemvChunks,
-                                                     true, g, st);
+      le = launch_gemv(kEpiQKV, batch == 1 ? kQkvRowsBatch1 : kGemvRows, kGemvChunks, true, g, st);
     }
     tr.end(KF_K_QKV);
     KF_HIP(le, "qkv launch");
@@ -977,8 +962,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.err_flag = s->err_flag;
     {
       tr.begin(KF_K_GATEUP);
-      const hipError_t le = batch > 1 && (KF_WAVE_GATEUP) ? launch_gemv_wave(kEpiSwiGLU, KF_WAVE_RW, true, gu, st)
-                                                         : launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
+      const hipError_t le = launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
       tr.end(KF_K_GATEUP);
       KF_HIP(le, "gate/up launch");
     }
