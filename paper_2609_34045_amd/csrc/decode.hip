@@ -909,7 +909,8 @@ __global__ __launch_bounds__(256) void oproj_heads_kernel(const AttnParams a, co
   constexpr int RPI = 64 / LPR;          // rows per wave-wide load
   constexpr int RPW = kOprojRows / 4;    // rows per wave
   constexpr int IT = RPW / RPI;          // loads per lane
-  static_assert(IT == LPR, "one reduced row per lane");
+  static_assert(IT >= 1 && IT <= LPR && (IT & (IT - 1)) == 0, "a power of two of reduced rows per row group");
+  constexpr int LPV = LPR / IT;          // lanes holding each reduced row
   constexpr int DPL = HD / 64, PRE = 32;
   const int rb = blockIdx.x, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1010,12 +1011,12 @@ __global__ __launch_bounds__(256) void oproj_heads_kernel(const AttnParams a, co
       sum[bb][i] = t;
     }
   }
-  // lane j of a row group ends with the group total of load j: row row0 + j * RPI
-  const int j = lane % LPR, row = row0 + j * RPI;
+  // lanes LPV j .. LPV j + LPV - 1 of a row group end with the group total of load j: row row0 + j * RPI
+  const int j = (lane % LPR) / LPV, row = row0 + j * RPI;
 #pragma unroll
   for (int bb = 0; bb < B; ++bb) {
     Butterfly<IT, LPR / 2>::run(sum[bb], lane);
-    if (row < N) atomicAdd(x + (int64_t)bb * N + row, sum[bb][0]);
+    if (row < N && lane % LPV == 0) atomicAdd(x + (int64_t)bb * N + row, sum[bb][0]);
   }
 }
 

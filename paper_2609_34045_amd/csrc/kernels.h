@@ -10,7 +10,9 @@ constexpr int kMaxBatch = 4;
 constexpr int kMaxGroup = 8;     // query heads per KV head
 constexpr int kAttnMinSplit = 16;   // keys per split-KV workgroup, lower bound
 constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound
-constexpr int kOprojRows = 256;     // output rows per workgroup of the head-split output projection
+// Output rows per workgroup of the head-split output projection (128 and 64 measured
+// slower: every workgroup repeats its head's merge of the split partials).
+constexpr int kOprojRows = 256;
 constexpr int kAttnMaxSplitCount = 1024;  // split-KV workgroups per (row, KV head), upper bound
 
 // Bits of the stage's sticky device error flag (reported and cleared by kf_stage_sync).
