@@ -51,7 +51,8 @@ int64_t prefill_ws_bytes(const PrefillArgs& a);
 void prefill_carve(PrefillWorkspace& ws, char* base, const PrefillArgs& a);
 hipError_t prefill_layer(PrefillWorkspace& ws, const PrefillArgs& a, const PrefillLayer& l, const Tracer& tr);
 
-// Matrix-core GEMM of the prefill projections (gemm.hip).
+// Matrix-core GEMM of the prefill projections (gemm.hip); K must be a multiple
+// of 64 (the stage's hidden, ffn and query widths are), else hipErrorInvalidValue.
 //   kGemmResidF32   C[M][N] += A W^T (unsplit; the residual stream)
 //   kGemmSwiGLU     Cb[M][N/2] = silu(gate) * up in fp16, W the gate rows and W2 the up rows
 //   kGemmPartialF32 K slice ks to C + ks*M*N (plain stores); the consumer adds the
