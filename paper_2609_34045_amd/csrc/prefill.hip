@@ -188,6 +188,10 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
 #define KF_PF_ATTN_RING 4
 #endif
 constexpr int kRing = KF_PF_ATTN_RING;  // LDS fragment reads in flight ahead of the MFMAs
+#ifndef KF_PF_ATTN_LAZY
+#define KF_PF_ATTN_LAZY 8.0f
+#endif
+constexpr float kLazy = KF_PF_ATTN_LAZY;
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
                                                            const uint16_t* vc, const KvPages kp, int user,
@@ -383,7 +387,13 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
         }
     }
     mb = fmaxf(mb, __shfl_xor(mb, 32));
-    const float m_new = fmaxf(m_run, mb * scale_log2);
+    // The reference maximum moves only when the block's maximum exceeds it by
+    // more than kLazy (log2 units): probabilities then stay below 2^kLazy,
+    // which fp16 holds as exactly as values below 1, and the rescale of O
+    // (and its multiplies) is skipped in nearly every block.  The result
+    // O / l does not depend on the reference.
+    const float m_blk = mb * scale_log2;
+    const float m_new = m_blk > m_run + kLazy ? m_blk : m_run;
     // Until a visible key has been seen (possible in a later key split) the
     // maximum is -inf; 0 then stands in as reference so that every
     // probability, and the rescale of the empty state, is exactly 0.

@@ -96,6 +96,68 @@ def test_decode_at_the_last_slot_of_the_largest_cache(torch, st, paged):
     g.close()
 
 
+def test_prefill_with_late_dominant_keys(torch, st):
+    """Chunked prefill over an injected cache whose later keys dominate chosen queries.
+
+    The prefill attention keeps, per query, a reference maximum for its
+    exponentials and moves it only when a key block's maximum exceeds it by
+    more than 8 (log2 units), so probabilities may reach 2^8 and O is rescaled
+    only on such a jump.  Random keys never jump that far, so four needles per
+    target query are planted in the cache, aligned with that query's rotated
+    vector (computed on the host from the oracle's definitions), at scores
+    7.5, 15, 12 and 17 log2 units above the query's largest ordinary score:
+    the first stays under the threshold (probabilities near 2^7.5), the
+    second moves the reference, the third and fourth sit in the second key
+    split (a fresh reference there, a jump, then a rise under the threshold),
+    so the merge of the two splits weighs references set both ways.  The last
+    two needles carry most of the weight between them, and the needles move
+    the target rows by tens of percent, so a misweighted needle or split
+    breaks the 1e-2 bound.  Targets sit in both 128-query tiles and both KV
+    groups; every row of the chunk is compared with the oracle.
+    """
+    cfg_id = 43
+    model = SeededModel(TINY, cfg_id)
+    nq, nkv, hd = TINY.n_q_heads, TINY.n_kv_heads, TINY.head_dim
+    grp = nq // nkv
+    n0, T = 1024, 256
+    kb, vb = synth.injected_kv(TINY, cfg_id, 0, 0, n0)
+    h = synth.hidden_states(cfg_id, synth.STREAM_PREFILL_HIDDEN, 0, T, TINY.hidden)
+    w = {k: bf16_to_f64(v) for k, v in model.layer(0).items()}
+    q = rope((rms_norm(h, w["attn_norm"], TINY.rms_eps) @ w["wq"].T).reshape(T, nq, hd), n0 + np.arange(T),
+             TINY.rope_theta)
+    log2e = 1.0 / np.log(2.0)
+    rng = np.random.default_rng(11)
+    kb0, vb0 = kb.copy(), vb.copy()
+    for i, head in ((3, 0), (140, 6)):  # (query of the chunk, query head): both tiles, both KV groups
+        g_kv = head // grp
+        qv = q[i, head]
+        ordinary = np.max(bf16_to_f64(kb[:, g_kv]) @ qv) / np.sqrt(hd) * log2e  # largest random score, log2 units
+        for pos, delta in ((100, 7.5), (400, 15.0), (700, 12.0), (900, 17.0)):
+            alpha = (ordinary + delta) / log2e * np.sqrt(hd) / np.linalg.norm(qv)
+            kb[pos, g_kv] = to_bf16(alpha * qv / np.linalg.norm(qv))
+            vb[pos, g_kv] = to_bf16(4.0 * rng.standard_normal(hd))
+
+    def oracle(k_bits, v_bits):
+        o = OracleStage(TINY, 0, 1, model.layer, None, max_users=1, max_ctx=n0 + T)
+        o.kv.inject(0, 0, 0, k_bits, v_bits)
+        o.kv.set_len(0, n0)
+        return o.prefill(0, n0, hidden=h)
+
+    ref = oracle(kb, vb)
+    plain = oracle(kb0, vb0)
+    for i in (3, 140):  # the needles move the target rows far beyond the tolerance
+        assert np.max(np.abs(ref[i] - plain[i])) > 0.2 * np.max(np.abs(plain[i]))
+    g = st.Stage(TINY, 0, 1, model.layer, None)
+    kv = g.kv(1, n0 + T)
+    kv.write(0, 0, 0, torch.from_numpy(kb.view(np.int16)).cuda(), torch.from_numpy(vb.view(np.int16)).cuda())
+    kv.set_len(0, n0)
+    y = g.prefill(kv, 0, n0, hidden=torch.from_numpy(h).cuda())
+    err = assert_hidden_close(y.float().cpu().numpy().astype(np.float64), ref, what="prefill with needles")
+    print("needle prefill max row rel err", err)
+    kv.close()
+    g.close()
+
+
 def test_weight_matrices_beyond_the_fp16_range_are_refused(torch, st):
     """The stage keeps its matrices in fp16: a finite bf16 weight fp16 cannot hold fails init.
 
