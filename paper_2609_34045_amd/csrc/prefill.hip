@@ -171,19 +171,24 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(const float* qkv, int nspl
 
 // ------------------------------------------------------------------ causal flash attention
 // Workgroup = (128 queries, one query head); wave w owns queries 32w .. 32w+31.
-// Per block of 32 keys each wave computes S^T = K Q^T (keys x queries) so that
+// Per block of 64 keys each wave computes S^T = K Q^T (keys x queries) so that
 // every lane holds one query's column; the online softmax is then per lane, and
 // the lane's probabilities are already a B fragment of O^T += V^T P^T once the
-// MFMA's k index is mapped to the keys the lane holds.  V^T is written to LDS
-// transposed when the block is staged.
+// MFMA's k index is mapped to the keys the lane holds.
+//
+// K and V blocks go from the cache straight into LDS (global_load_lds) in their
+// [key][d] layout, 16-byte chunks XOR-swizzled within a key row.  The V^T
+// operand fragments are read with ds_read_b64_tr_b16: within each group of 16
+// lanes, lane 4r + j reads 4 consecutive d of key row r and lane c receives
+// element c of the group's four rows, i.e. d = d0 + c over 4 consecutive keys.
+// The loop is software-pipelined: the S MFMAs of block j+1 are issued among
+// the softmax of block j.  K and V have 2-stage rings of their own, each
+// loaded one iteration ahead, right after the barrier that frees its stage.
 //
 // The keys may be split over gridDim.z workgroups (more workgroups in flight,
 // two per CU): split z takes key blocks [z nblk / Z, (z+1) nblk / Z) and, when
 // Z > 1, writes its unnormalised output and (max, sum) per query to part_acc /
 // part_ml for attn_prefill_combine_kernel.
-#ifndef KF_PF_ATTN_KB
-#define KF_PF_ATTN_KB 64
-#endif
 #ifndef KF_PF_ATTN_RING
 #define KF_PF_ATTN_RING 4
 #endif
@@ -192,20 +197,57 @@ constexpr int kRing = KF_PF_ATTN_RING;  // LDS fragment reads in flight ahead of
 #define KF_PF_ATTN_LAZY 8.0f
 #endif
 constexpr float kLazy = KF_PF_ATTN_LAZY;
+constexpr int kAttnKB = 64;  // keys per block
+typedef __attribute__((address_space(3))) void* lds_ptr;
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s* lds_v4s;
+
+// Slot of 16-byte chunk c of key row r.  A K fragment read takes one chunk of
+// 16 consecutive rows (HD 128) or of 8 same-parity rows among 16 (HD 64) per
+// LDS cycle; a V transpose read takes 4 consecutive rows x 4 consecutive
+// chunks.  f(r) puts both on distinct 16-byte bank groups of a 64-bank LDS.
+template <int HD>
+__device__ __forceinline__ int kv_slot(int r, int c) {
+  return HD == 128 ? c ^ (((r & 3) << 2) | ((r >> 2) & 3)) : c ^ ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+
+// max / sum of x over lanes l and l ^ 32: v_permlane32_swap with x in both
+// operands leaves x[l] in one result and x[l ^ 32] in the other.
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Wait until this wave's global loads (and the LDS writes of direct loads) are complete.
+__device__ __forceinline__ void attn_wait_loads() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xF << 8)); }
+// Workgroup barrier across which the compiler may not move memory operations.
+__device__ __forceinline__ void attn_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q, const uint16_t* kc,
                                                            const uint16_t* vc, const KvPages kp, int user,
                                                            uint16_t* out, float* part_acc, float* part_ml, int T,
                                                            int nq, int nkv, int pos0, float scale_log2,
                                                            int* err_flag) {
-  constexpr int KB = KF_PF_ATTN_KB;  // keys per block: KB / 32 tiles of 32 keys
-  constexpr int NT = KB / 32;
-  static_assert(KB == 32 || KB == 64, "32 or 64 keys per block");
-  constexpr int LDK = HD + 8;       // K tile row stride (fp16 elements)
-  constexpr int LDV = KB + 4;       // V^T tile row stride (fp16 elements), keeps 8-byte alignment
-  constexpr int DB = HD / 32;       // 32-row d-blocks of O^T
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KB * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][HD * LDV];
+  constexpr int KB = kAttnKB, NT = KB / 32;  // keys per block, 32-key tiles per block
+  constexpr int NS = HD / 16, DB = HD / 32;  // 16-wide d slices of S, 32-row d blocks of O^T
+  constexpr int CPR = HD / 8;                // 16-byte chunks per key row
+  constexpr int ROWB = HD * 2;               // bytes per key row
+  constexpr int TILEB = KB * ROWB;           // one block of K (or V): 16 KB (HD 128) or 8 KB
+  constexpr int RPI = 64 / CPR;              // key rows per 1 KB direct load
+  constexpr int LPW = TILEB / 1024 / 4;      // direct loads per wave per tile
+  static_assert(HD == 64 || HD == 128, "head dim");
+  static_assert(kKvPage % KB == 0, "key blocks within pages");
+  // K stages 0 and 1, then V stages 0 and 1.
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * TILEB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // Workgroups go to the 8 XCDs round-robin by linear id.  Numbering the work
@@ -234,18 +276,17 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   const int Z = gridDim.z, z = bz;
   const int blk0 = (int)((int64_t)nblk_all * z / Z), blk1 = (int)((int64_t)nblk_all * (z + 1) / Z);
   // A block of KB keys lies in one cache page (KB divides kKvPage, blocks start at multiples of KB).
-  static_assert(kKvPage % KF_PF_ATTN_KB == 0, "key blocks within pages");
   auto block_off = [&](int blk) -> int64_t {
-    const int k0 = blk * KF_PF_ATTN_KB;
+    const int k0 = blk * KB;
     return (int64_t)kv_page(kp, user, k0 / kKvPage) * kp.page_stride + ((int64_t)g * kKvPage + k0 % kKvPage) * HD;
   };
 
   // Q^T fragments: lane holds query qi, d = 16 s + 8 half_sel .. +7.
-  v4u qf[HD / 16];
+  v4u qf[NS];
   {
     const uint16_t* qr = q + ((int64_t)(qok ? qi : 0) * nq + h) * HD;
 #pragma unroll
-    for (int s = 0; s < HD / 16; ++s) {
+    for (int s = 0; s < NS; ++s) {
       v4u v = *reinterpret_cast<const v4u*>(qr + 16 * s + 8 * half_sel);
       qf[s] = qok ? v : v4u{0u, 0u, 0u, 0u};
     }
@@ -258,135 +299,90 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     for (int v = 0; v < 16; ++v) o[d][v] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Staging: 32 keys x HD elements for K and V.  K: a thread moves 16-byte
-  // chunks (key, ch).  V is stored transposed (Vt[d][key]): a thread loads the
-  // same 16-byte chunk of two adjacent keys and writes, for each of its 8 d, one
-  // 32-bit word holding both keys (consecutive lanes: consecutive key pairs).
-  // Global loads for the next block are issued before this block's MFMAs and
-  // written to the other LDS buffer after them.
-  constexpr int CH = HD / 8;               // 16-byte chunks per key
-  constexpr int PER = (KB * CH + 255) / 256;
-  constexpr int VPER = (KB / 2 * CH + 255) / 256;
-  v4u rk[PER], rv0[VPER], rv1[VPER];
-  // Keys at or past nkeys come after every query of the workgroup, so the
-  // causal mask gives them weight 0; they are loaded from key nkeys - 1 (a
-  // written, finite row) instead of being branched around.
-  // (Thread chunks past the tile, possible only when 256 does not divide the
-  // chunk count, are skipped; the test folds away otherwise.)
-  constexpr bool kFullK = KB * CH % 256 == 0, kFullV = KB / 2 * CH % 256 == 0;
-  // (nkeys - 1 is in block blk whenever a key of blk is clamped to it, so every
-  // load stays in the block's page.)
-  auto gload = [&](int blk) {
-    const int kb0 = blk * KB, last = nkeys - 1 - kb0;  // keys of the block relative to kb0
-    const int64_t boff = block_off(blk);
-    const uint16_t* kbase = kc + boff;
-    const uint16_t* vbase = vc + boff;
+  auto kst = [&](int blk) { return smem + ((blk - blk0) & 1) * TILEB; };
+  auto vst = [&](int blk) { return smem + (2 + ((blk - blk0) & 1)) * TILEB; };
+  // Direct loads of block blk's K or V rows into a stage: load j of this wave
+  // fills rows RPI (4 j + wave) ..; lane l writes row RPI (4 j + wave) + l / CPR,
+  // slot l % CPR, so it fetches the chunk that belongs in that slot (byte
+  // offset dma_off[j] within the block).  Keys at or past nkeys come after
+  // every query of the workgroup, so the causal mask gives them weight 0; in
+  // the block that holds nkeys - 1 they are loaded from that key instead, a
+  // written row of the same page.
+  int dma_row[LPW], dma_chunk[LPW];
 #pragma unroll
-    for (int r = 0; r < PER; ++r) {
-      const int idx = tid + 256 * r;
-      const int key = idx / CH, ch = idx % CH;
-      if (kFullK || idx < KB * CH) rk[r] = *reinterpret_cast<const v4u*>(kbase + (int64_t)min(key, last) * HD + ch * 8);
-    }
-#pragma unroll
-    for (int r = 0; r < VPER; ++r) {
-      const int idx = tid + 256 * r;
-      const int kp2 = idx % (KB / 2), ch = idx / (KB / 2);
-      if (kFullV || idx < KB / 2 * CH) {
-        rv0[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(2 * kp2, last) * HD + ch * 8);
-        rv1[r] = *reinterpret_cast<const v4u*>(vbase + (int64_t)min(2 * kp2 + 1, last) * HD + ch * 8);
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-      const int idx = tid + 256 * r;
-      if (kFullK || idx < KB * CH) {
-        const int key = idx / CH, ch = idx % CH;
-        *reinterpret_cast<v4u*>(&Ks[buf][key * LDK + ch * 8]) = rk[r];
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < VPER; ++r) {
-      const int idx = tid + 256 * r;
-      if (kFullV || idx < KB / 2 * CH) {
-        const int kp2 = idx % (KB / 2), ch = idx / (KB / 2);
-        const uint32_t a[4] = {rv0[r].x, rv0[r].y, rv0[r].z, rv0[r].w};
-        const uint32_t b[4] = {rv1[r].x, rv1[r].y, rv1[r].z, rv1[r].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          // d = ch*8 + 2e holds the low halves, d + 1 the high halves
-          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * LDV + 2 * kp2]) =
-              (a[e] & 0xffffu) | (b[e] << 16);
-          *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * LDV + 2 * kp2]) =
-              (a[e] >> 16) | (b[e] & 0xffff0000u);
-        }
-      }
-    }
-  };
-
-  if (blk0 < blk1) {
-    gload(blk0);
-    lstore(0);
+  for (int j = 0; j < LPW; ++j) {
+    dma_row[j] = RPI * (4 * j + wave) + lane / CPR;
+    dma_chunk[j] = kv_slot<HD>(dma_row[j], lane % CPR) * 16;
   }
-  __syncthreads();
-  for (int blk = blk0; blk < blk1; ++blk) {
-    const int buf = (blk - blk0) & 1;
-    if (blk + 1 < blk1) gload(blk + 1);
+  auto issue = [&](const uint16_t* cache, int blk, uint8_t* dst) {
+    const int last = nkeys - 1 - blk * KB;
+    const char* base = reinterpret_cast<const char*>(cache + block_off(blk));
+    if (last >= KB - 1) {
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) {
+        const char* src = base + (dma_row[j] * ROWB + dma_chunk[j]);
+        uint8_t* d = dst + 1024 * (4 * j + wave);
+        __builtin_amdgcn_global_load_lds(src, (lds_ptr)d, 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) {
+        const char* src = base + (min(dma_row[j], last) * ROWB + dma_chunk[j]);
+        uint8_t* d = dst + 1024 * (4 * j + wave);
+        __builtin_amdgcn_global_load_lds(src, (lds_ptr)d, 16, 0, 0);
+      }
+    }
+  };
 
-    // S^T[key][query] for each 32-key tile of this block.  The K fragments
-    // go through a ring of kRing registers: the read for MFMA i + kRing is
-    // issued before MFMA i, so LDS latency hides behind the MFMAs in flight.
-    f32x16 st[NT];
+  // Lane byte offsets of the fragment reads within a stage.  The row swizzle
+  // depends only on a row's low four bits, so the key tile and step add a
+  // constant (an immediate of the read).
+  //   K, slice s: row lane % 32 (+ 32 t), chunk 2 s + half_sel.
+  //   V^T, d-block d and half e: key row 8 e + 4 (gq / 2) + r (+ 32 t + 16 sidx),
+  //   d = 32 d + 16 (gq % 2) + 4 j, with lane = 16 gq + 4 r + j.
+  int koff[NS], voff[DB][2];
+  {
+    const int rl = lane & 31;
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) koff[s2] = rl * ROWB + kv_slot<HD>(rl, 2 * s2 + half_sel) * 16;
+    const int gq = lane >> 4, tr_r = (lane >> 2) & 3, tr_j = lane & 3;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int key = 8 * e + 4 * (gq >> 1) + tr_r, dd = 32 * d + 16 * (gq & 1) + 4 * tr_j;
+        voff[d][e] = key * ROWB + kv_slot<HD>(key, dd >> 3) * 16 + (dd & 7) * 2;
+      }
+  }
+  constexpr int NI_S = NT * NS;
+  auto kread = [&](const uint8_t* ks, int i) {
+    return *reinterpret_cast<const v4u*>(ks + (i / NS) * 32 * ROWB + koff[i % NS]);
+  };
+
+  // Causal mask of block blk's scores (only blocks that reach past the wave's
+  // first query have masked keys).  Lane holds keys 32 t + 8 (v/4) + 4 half_sel
+  // + v%4 of its query.
+  auto mask = [&](int blk, f32x16 (&st)[NT]) {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) st[t][v] = 0.f;
-    {
-      constexpr int NS = HD / 16, NI = NT * NS;
-      auto kread = [&](int i) {
-        const int t = i / NS, s = i % NS;
-        return *reinterpret_cast<const v4u*>(&Ks[buf][(32 * t + (lane & 31)) * LDK + 16 * s + 8 * half_sel]);
-      };
-      v4u ring[kRing];
-#pragma unroll
-      for (int i = 0; i < kRing; ++i) ring[i] = kread(i);
-#pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const v4u cur = ring[i % kRing];
-        if (i + kRing < NI) ring[i % kRing] = kread(i + kRing);
-        st[i / NS] = mfma32(cur, qf[i % NS], st[i / NS]);
+      for (int v = 0; v < 16; ++v) {
+        const int key = blk * KB + 32 * t + 8 * (v >> 2) + 4 * half_sel + (v & 3);
+        if (key > qpos) st[t][v] = -INFINITY;
       }
-      // Order: the kRing prologue reads, then MFMA i followed by the read for i + kRing.
-      __builtin_amdgcn_sched_group_barrier(0x100, kRing, 0);
-#pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (i + kRing < NI) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-    }
-    // Lane holds keys 32 t + 8 (v/4) + 4 half_sel + v%4 of its query.  Scores
-    // stay unscaled here: the scale (> 0) commutes with the maximum and is
-    // folded into the exponent's fma below.  Only blocks that reach past the
-    // wave's first query need the causal mask.
+  };
+
+  // Online softmax of a block's (masked, unscaled) scores st into the P^T
+  // fragments pf; returns the factor O must be rescaled by.  The scale (> 0)
+  // commutes with the maximum and is folded into the exponent's fma.  The row
+  // sum is taken over the fp16 probabilities that the P V product uses.
+  auto softmax = [&](f32x16 (&st)[NT], v4u (&pf)[NT][2]) {
     float mb = -INFINITY;
-    if (blk * KB + KB - 1 <= pos0 + i0 + wave * 32) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) mb = fmaxf(mb, st[t][v]);
-    } else {
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = blk * KB + 32 * t + 8 * (v >> 2) + 4 * half_sel + (v & 3);
-          const float sv = key <= qpos ? st[t][v] : -INFINITY;
-          st[t][v] = sv;
-          mb = fmaxf(mb, sv);
-        }
-    }
-    mb = fmaxf(mb, __shfl_xor(mb, 32));
+      for (int v = 0; v < 16; ++v) mb = fmaxf(mb, st[t][v]);
+    mb = pair_max(mb);
     // The reference maximum moves only when the block's maximum exceeds it by
     // more than kLazy (log2 units): probabilities then stay below 2^kLazy,
     // which fp16 holds as exactly as values below 1, and the rescale of O
@@ -400,66 +396,174 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     const float m_ref = m_new == -INFINITY ? 0.f : m_new;
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);  // 0 while m_run = -inf
     float ls = 0.f;
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(st[t][v], scale_log2, -m_ref));
-        st[t][v] = pv;
-        ls += pv;
-      }
-    ls += __shfl_xor(ls, 32);
-    l_run = l_run * alpha + ls;
-    m_run = m_new;
-    if (__ballot(alpha != 1.0f)) {  // no lane's maximum moved: nothing to rescale
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
-    }
-
     // P^T fragments of tile t: step 0 takes v = 0..7, step 1 takes v = 8..15 (the
     // MFMA's k index runs over the keys this lane holds, in that order).
-    v4u pf[NT][2];
+    const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int sidx = 0; sidx < 2; ++sidx) {
         uint32_t w[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_f16(st[t][8 * sidx + 2 * e], st[t][8 * sidx + 2 * e + 1]);
+        for (int e = 0; e < 4; ++e) {
+          const int v = 8 * sidx + 2 * e;
+          w[e] = pack_f16(__builtin_amdgcn_exp2f(fmaf(st[t][v], scale_log2, -m_ref)),
+                          __builtin_amdgcn_exp2f(fmaf(st[t][v + 1], scale_log2, -m_ref)));
+          ls = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w[e]), ones, ls, false);
+        }
         pf[t][sidx] = v4u{w[0], w[1], w[2], w[3]};
       }
-    // V^T fragments with the same key order: keys 32 t + 16 sidx + 4 half_sel + {0..3}
-    // and 32 t + 16 sidx + 8 + 4 half_sel + {0..3}; read through the same kind of ring.
-    {
-      constexpr int NP = NT * 2, NI = DB * NP;  // MFMA i: d-block i / NP, (t, sidx) = i % NP
-      auto vread = [&](int i) {
-        const int d = i / NP, t = (i % NP) / 2, sidx = i % 2;
-        const uint16_t* vrow = &Vt[buf][(32 * d + (lane & 31)) * LDV];
-        const v2u lo = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 4 * half_sel);
-        const v2u hi = *reinterpret_cast<const v2u*>(vrow + 32 * t + 16 * sidx + 8 + 4 * half_sel);
-        return v4u{lo.x, lo.y, hi.x, hi.y};
-      };
-      v4u ring[kRing];
+    l_run = l_run * alpha + pair_sum(ls);
+    m_run = m_new;
+    return alpha;
+  };
+
+  // O^T += V^T P^T from block blk's V stage.  MFMA i: d-block i / NP, key step
+  // (t, sidx) = i % NP, whose keys are 32 t + 16 sidx + 4 half_sel + {0..3} and
+  // + 8 + {0..3} in the MFMA's k order: two transpose reads.
+  auto pv_mfma = [&](const uint8_t* vs, const v4u (&pf)[NT][2]) {
+    constexpr int NP = NT * 2, NI = DB * NP;
+    auto vread = [&](int i) {
+      const int d = i / NP, t = (i % NP) / 2, sidx = i % 2;
+      // (named operands: the host pass drops the kernel's launch stub when a
+      // builtin's pointer argument is a compound expression)
+      const uint8_t* b = vs + (32 * t + 16 * sidx) * ROWB;
+      const uint8_t* a0 = b + voff[d][0];
+      const uint8_t* a1 = b + voff[d][1];
+      const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)a0);
+      const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)a1);
+      const v2u l2 = __builtin_bit_cast(v2u, lo), h2v = __builtin_bit_cast(v2u, hi);
+      return v4u{l2.x, l2.y, h2v.x, h2v.y};
+    };
+    v4u ring[kRing];
 #pragma unroll
-      for (int i = 0; i < kRing; ++i) ring[i] = vread(i);
+    for (int i = 0; i < kRing; ++i) ring[i] = vread(i);
 #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const v4u cur = ring[i % kRing];
-        if (i + kRing < NI) ring[i % kRing] = vread(i + kRing);
-        o[i / NP] = mfma32(cur, pf[(i % NP) / 2][i % 2], o[i / NP]);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x100, 2 * kRing, 0);  // two LDS reads per fragment
-#pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (i + kRing < NI) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
+    for (int i = 0; i < NI; ++i) {
+      const v4u cur = ring[i % kRing];
+      if (i + kRing < NI) ring[i % kRing] = vread(i + kRing);
+      o[i / NP] = mfma32(cur, pf[(i % NP) / 2][i % 2], o[i / NP]);
     }
-    if (blk + 1 < blk1) lstore(buf ^ 1);
-    __syncthreads();
+  };
+
+  // S^T[key][query] of one block from its K stage.  The K fragments go through
+  // a ring of kRing registers: the read for MFMA i + kRing is issued before
+  // MFMA i, so LDS latency hides behind the MFMAs in flight.
+  auto s_mfma = [&](const uint8_t* ks, f32x16 (&st)[NT]) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) st[t][v] = 0.f;
+    v4u ring[kRing];
+#pragma unroll
+    for (int i = 0; i < kRing; ++i) ring[i] = kread(ks, i);
+#pragma unroll
+    for (int i = 0; i < NI_S; ++i) {
+      const v4u cur = ring[i % kRing];
+      if (i + kRing < NI_S) ring[i % kRing] = kread(ks, i + kRing);
+      st[i / NS] = mfma32(cur, qf[i % NS], st[i / NS]);
+    }
+  };
+
+  // The same S MFMAs with the softmax of the previous block's scores sc (as
+  // softmax() computes it) spread over the MFMA slots, pinned in order, so
+  // that the wave issues vector work while its MFMAs run: the block maximum
+  // over the first quarter of the slots, the reference update in one slot,
+  // the probabilities (exponent, fp16 pack, running sum) over the next half,
+  // the row sum in one more.
+  auto s_mfma_softmax = [&](const uint8_t* ks, f32x16 (&st)[NT], f32x16 (&sc)[NT], v4u (&pf)[NT][2]) {
+    constexpr int NV = NT * 16;                 // scores per lane
+    constexpr int MAXS = NI_S / 4, EXPS = NI_S / 2;
+    constexpr int MPS = NV / MAXS, EPS = NV / EXPS;  // scores per slot in the max and exponent phases
+    static_assert(MAXS + 1 + EXPS + 1 <= NI_S && NV % MAXS == 0 && NV % EXPS == 0 && EPS % 2 == 0, "phases");
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) st[t][v] = 0.f;
+    float mb = -INFINITY, m_new = 0.f, m_ref = 0.f, alpha = 1.f, ls = 0.f;
+    uint32_t w[NV / 2];
+    const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+    v4u ring[kRing];
+#pragma unroll
+    for (int i = 0; i < kRing; ++i) ring[i] = kread(ks, i);
+#pragma unroll
+    for (int i = 0; i < NI_S; ++i) {
+      const v4u cur = ring[i % kRing];
+      if (i + kRing < NI_S) ring[i % kRing] = kread(ks, i + kRing);
+      st[i / NS] = mfma32(cur, qf[i % NS], st[i / NS]);
+      if (i < MAXS) {
+#pragma unroll
+        for (int u = i * MPS; u < (i + 1) * MPS; ++u) mb = fmaxf(mb, sc[u / 16][u % 16]);
+      } else if (i == MAXS) {
+        mb = pair_max(mb);
+        const float m_blk = mb * scale_log2;
+        m_new = m_blk > m_run + kLazy ? m_blk : m_run;
+        m_ref = m_new == -INFINITY ? 0.f : m_new;
+        alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+      } else if (i <= MAXS + EXPS) {
+        const int k = i - MAXS - 1;
+#pragma unroll
+        for (int u = k * EPS; u < (k + 1) * EPS; u += 2) {
+          w[u / 2] = pack_f16(__builtin_amdgcn_exp2f(fmaf(sc[u / 16][u % 16], scale_log2, -m_ref)),
+                              __builtin_amdgcn_exp2f(fmaf(sc[(u + 1) / 16][(u + 1) % 16], scale_log2, -m_ref)));
+          ls = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w[u / 2]), ones, ls, false);
+        }
+      } else if (i == MAXS + EXPS + 1) {
+        l_run = l_run * alpha + pair_sum(ls);
+        m_run = m_new;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // word u/2 holds scores u, u+1 = (t, v) with v = 8 sidx + 2 e
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const int b0 = (16 * t + 8 * sidx) / 2;
+        pf[t][sidx] = v4u{w[b0], w[b0 + 1], w[b0 + 2], w[b0 + 3]};
+      }
+    return alpha;
+  };
+
+  // Iteration blk: on entry K(blk + 1) and V(blk) were loaded (by this wave)
+  // an iteration ago, and S(blk) is in sc.  After the barrier every wave's
+  // loads have landed and every wave is done with K(blk) (read for S(blk))
+  // and V(blk - 1), so their stages take K(blk + 2) and V(blk + 1).
+  auto iteration = [&](int blk, f32x16 (&sc)[NT], f32x16 (&sn)[NT]) {
+    attn_wait_loads();
+    attn_barrier();
+    if (blk + 2 < blk1) issue(kc, blk + 2, kst(blk + 2));
+    if (blk + 1 < blk1) issue(vc, blk + 1, vst(blk + 1));
+    if (blk * KB + KB - 1 > pos0 + i0 + wave * 32) mask(blk, sc);
+    v4u pf[NT][2];
+    float alpha;
+    if (blk + 1 < blk1) alpha = s_mfma_softmax(kst(blk + 1), sn, sc, pf);
+    else alpha = softmax(sc, pf);
+    if (__ballot(alpha != 1.0f)) {  // no lane's reference moved: nothing to rescale
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
+    }
+    pv_mfma(vst(blk), pf);
+  };
+
+  f32x16 sa[NT], sb[NT];
+  if (blk0 < blk1) {
+    issue(kc, blk0, kst(blk0));
+    issue(vc, blk0, vst(blk0));
+    attn_wait_loads();
+    attn_barrier();
+    if (blk0 + 1 < blk1) issue(kc, blk0 + 1, kst(blk0 + 1));
+    s_mfma(kst(blk0), sa);
   }
+  int blk = blk0;
+  for (; blk + 1 < blk1; blk += 2) {
+    iteration(blk, sa, sb);
+    iteration(blk + 1, sb, sa);
+  }
+  if (blk < blk1) iteration(blk, sa, sb);
+  attn_wait_loads();  // no direct load may still be writing LDS when the workgroup ends
 
   if (Z > 1) {  // unnormalised partial of this key split
     if (qok) {
