@@ -73,3 +73,29 @@ def test_group_size(torch, st, nq, nkv, hd, qkn):
     print(f"G={nq // nkv} hd={hd} qk_norm={qkn} max row rel err", worst)
     kv.close()
     g.close()
+
+
+@pytest.mark.parametrize("ffn,T", [(16384, 512), (16384, 300), (1408, 512)], ids=["f16384_t512", "f16384_t300", "f1408_t512"])
+def test_prefill_swiglu_tile_widths(torch, st, ffn, T):
+    """The SwiGLU projection's two tile widths, against the float64 oracle.
+
+    Its tiles are 256 rows by 224 or 256 columns (7 or 8 blocks of 16 gate
+    and 16 up rows), whichever fills whole rounds of the chip in fewer
+    tile-times.  The workload shapes all take 224; an FFN of 16384 at a
+    512-token chunk (2 x 128 tiles of 256 columns, exactly one round) takes
+    256, and a 300-token chunk the same with a ragged row tile.  FFN 1408
+    ends in a partial column tile.  One layer, a prefill from hidden rows on
+    an empty cache; every output row is compared.
+    """
+    shape = synth.ModelShape(1, 256, 4, 2, 64, ffn, 300, 1e-5, 1e4)
+    cfg = 60 + ffn % 97
+    model = SeededModel(shape, cfg)
+    g = st.Stage(shape, 0, 1, model.layer, None)
+    kv = g.kv(1, T)
+    h = synth.hidden_states(cfg, synth.STREAM_PREFILL_HIDDEN, 0, T, shape.hidden)
+    y = g.prefill(kv, 0, 0, hidden=torch.from_numpy(h).cuda())
+    o = OracleStage(shape, 0, 1, model.layer, None, max_users=1, max_ctx=T)
+    err = assert_hidden_close(host(y), o.prefill(0, 0, hidden=h), what=f"prefill ffn {ffn} T {T}")
+    print(f"ffn={ffn} T={T} prefill max row rel err", err)
+    kv.close()
+    g.close()
