@@ -481,9 +481,9 @@ def measure_decode(args, torch, g, kv, wl, B: int, ctx) -> dict:
         nonlocal toks
         for i in range(n):
             pos = [ctx[u] + i for u in users]
-            if wl.has_head:
-                g.decode(kv, users, pos, tokens=toks, out=out)
-                toks = g.head_argmax(out)  # closed-loop greedy decode
+            if wl.has_head:  # closed-loop greedy decode; the head reads the rows the decode kept
+                g.decode(kv, users, pos, tokens=toks, keep=True)
+                toks = g.head_argmax(None, rows=B)
             else:
                 g.decode(kv, users, pos, hidden=hid[i], out=out)
 

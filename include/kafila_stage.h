@@ -41,12 +41,14 @@
 extern "C" {
 #endif
 
-#define KF_ABI_VERSION 4  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds;
+#define KF_ABI_VERSION 5  /* 2: kf_model_config.qk_norm and the q/k norm tensor kinds;
                             3: paged KV caches, kf_stage_describe, kf_kv_describe;
                             4: kf_stage_set_flags / kf_stage_get_flags (KF_STAGE_ORDERED), range and
                                NaN-logit errors reported by kf_stage_sync, token -1 for a row of NaN logits,
                                kf_stage_prefill_noalloc; kf_ring_generate's hidden_out_dev (kafila_ring.h);
-                               the kf_shard_* loader (kafila_shard.h) */
+                               the kf_shard_* loader (kafila_shard.h);
+                            5: a head stage's decode may keep its output rows (hidden_out_dev NULL)
+                               for kf_head_logits / kf_head_argmax with hidden_dev NULL */
 #define KF_KV_PAGE 64     /* positions per KV cache page */
 #define KF_MAX_BATCH 4
 
@@ -258,7 +260,14 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
  *                            (append-only; else KF_EINVAL) and be < max_ctx (else KF_ERANGE).
  *   tokens_dev  : int32 [batch] token ids (stage with the head only), or NULL
  *   hidden_in_dev : [batch, H] in `io`, or NULL; exactly one of tokens_dev / hidden_in_dev
- *   hidden_out_dev : [batch, H] in `io`; may alias hidden_in_dev
+ *   hidden_out_dev : [batch, H] in `io`; may alias hidden_in_dev.  NULL (a stage
+ *                    that holds the head only, else KF_EINVAL): the output rows stay
+ *                    in the stage for the head (kf_head_logits / kf_head_argmax with
+ *                    hidden_dev NULL), as when the member that holds the model's
+ *                    last blocks also holds the head and samples the next token.
+ *                    At batch 2-4 they are kept in fp16 (the rounding every layer's
+ *                    input of this stage already takes), which halves the LM head's
+ *                    input traffic; at batch 1 in fp32.
  * Row b's token is at positions[b]: its key and value are written at that slot of
  * the user's cache in every held layer, and it attends slots 0..positions[b].
  * On success every user's length advances by one.  A paged cache lends a page to
@@ -307,6 +316,9 @@ kf_status kf_stage_prefill_noalloc(kf_stage* stage, kf_kv* kv, int32_t user, int
  * embedding and unembedding and samples after the model's last block):
  * logits_dev fp32 [rows, V] = RMSNorm(hidden; final gain) x LM_head^T, for hidden_dev
  * [rows, H] in dtype (KF_F32 or KF_BF16), any rows >= 1.  Head stages only (else KF_ESTATE).
+ * hidden_dev NULL: the rows the stage's last kf_stage_decode kept (its hidden_out_dev
+ * was NULL); rows must equal that decode's batch and dtype is ignored (else KF_ESTATE,
+ * also when the last decode returned its rows or failed).
  */
 kf_status kf_head_logits(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype, float* logits_dev);
 
@@ -317,7 +329,7 @@ kf_status kf_head_logits(kf_stage* stage, int32_t rows, const void* hidden_dev, 
  * (may be NULL) receives the winning logit.  A NaN logit is skipped and raises the
  * stage's NaN-logit error (KF_ERANGE from kf_stage_sync); a row whose logits are all
  * NaN gives token -1 and max logit NaN.  rows in [1, KF_MAX_BATCH] (else KF_EINVAL).
- * Head stages only (else KF_ESTATE).
+ * Head stages only (else KF_ESTATE).  hidden_dev NULL: the kept rows, as for kf_head_logits.
  */
 kf_status kf_head_argmax(kf_stage* stage, int32_t rows, const void* hidden_dev, kf_dtype dtype,
                          int32_t* token_dev, float* max_logit_dev);

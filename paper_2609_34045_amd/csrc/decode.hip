@@ -1177,7 +1177,9 @@ static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiSwiGLU && norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
-  else if (epi == kEpiLMHead && norm)
+  else if (epi == kEpiLMHead && norm && B > 1 && p.in16)
+    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+  else if (epi == kEpiLMHead && norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true>), dim3(grid), dim3(256), 0, s, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();

@@ -106,6 +106,7 @@ struct kf_stage {
   int* part_idx = nullptr;
   int lm_wg = 0;       // capacity of the argmax partials per batch row
   int lm_wg_used = 0;  // partials per row written by the last LM-head launch
+  int kept_rows = 0;   // rows the last decode kept for the head (called without hidden output), else 0
   int* err_flag = nullptr;
   int live_kv = 0;
   PrefillWorkspace pf;
@@ -799,7 +800,8 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   if ((tokens_dev == nullptr) == (hidden_in_dev == nullptr))
     return fail(KF_EINVAL, "exactly one of tokens / hidden input must be given");
   if (tokens_dev && !s->has_head) return fail(KF_ESTATE, "token input needs the head");
-  if (!hidden_out_dev) return fail(KF_EINVAL, "hidden output is NULL");
+  if (!hidden_out_dev && !s->has_head)
+    return fail(KF_EINVAL, "hidden output is NULL (only a stage that holds the head may keep its rows)");
   if (io != KF_F32 && io != KF_BF16) return fail(KF_EINVAL, "io dtype");
   int max_len = 0;
   int64_t total_len = 0;
@@ -824,6 +826,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   for (int b = 0; b < batch; ++b) upto[b] = (int64_t)positions[b] + 1;
   const kf_status gst = kv_grant(kv, batch, users, upto);
   if (gst != KF_OK) return gst;
+  s->kept_rows = 0;  // the residual rows change from here on; set again when the step completes
 
   const Tracer tr = s->tracer();
 
@@ -976,10 +979,10 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     d.N = H;
     d.x = s->x;
     d.err_flag = s->err_flag;
-    if (l == s->hi - 1) {
+    if (l == s->hi - 1 && hidden_out_dev) {
       d.out2 = hidden_out_dev;
       d.out2_type = io == KF_BF16 ? kOut2BF16 : kOut2F32;
-    } else if (batch > 1) {
+    } else if (batch > 1) {  // also the kept rows the head reads (no hidden output)
       d.out2 = s->x16;  // the next layer's QKV input
       d.out2_type = kOut2F16;
     }
@@ -991,6 +994,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
   }
   for (int b = 0; b < batch; ++b) kv->len[users[b]] += 1;
+  s->kept_rows = hidden_out_dev ? 0 : batch;
   return KF_OK;
 }
 
@@ -999,7 +1003,11 @@ static kf_status head_common(kf_stage* s, int rows, const void* hidden, kf_dtype
   if (!s) return fail(KF_EINVAL, "stage is NULL");
   if (!s->has_head) return fail(KF_ESTATE, "the stage does not hold the head");
   if (rows < 1) return fail(KF_EINVAL, "rows must be >= 1");
-  if (!hidden) return fail(KF_EINVAL, "hidden is NULL");
+  if (!hidden) {  // the rows the stage's last decode kept
+    if (s->kept_rows != rows)
+      return fail(KF_ESTATE, "hidden is NULL but the stage's last decode kept %d rows, not %d", s->kept_rows, rows);
+    return KF_OK;
+  }
   if (dtype != KF_F32 && dtype != KF_BF16) return fail(KF_EINVAL, "dtype");
   return KF_OK;
 }
@@ -1014,6 +1022,10 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.gain = s->g_final;
   g.src = hidden;  // the LM head reads the caller's rows directly
   g.src_bf16 = dtype == KF_BF16;
+  if (!hidden) {  // the kept rows: the residual itself at batch 1, its fp16 copy at batch 2-4
+    g.in = rows > 1 ? reinterpret_cast<const float*>(s->x16) : s->x;
+    g.in16 = rows > 1;
+  }
   g.K = c.hidden;
   g.N = c.vocab;
   g.logits = logits;
@@ -1023,7 +1035,8 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.n_wg = gemv_grid(kEpiLMHead, kGemvRows, g);
   s->lm_wg_used = g.n_wg;
   tr.begin(KF_K_LMHEAD);
-  const hipError_t e = launch_gemv_src(kEpiLMHead, kGemvRows, kGemvChunks, true, g, s->stream);
+  const hipError_t e = hidden ? launch_gemv_src(kEpiLMHead, kGemvRows, kGemvChunks, true, g, s->stream)
+                              : launch_gemv(kEpiLMHead, kGemvRows, kGemvChunks, true, g, s->stream);
   tr.end(KF_K_LMHEAD);
   KF_HIP(e, "lm-head launch");
   return KF_OK;
@@ -1033,6 +1046,7 @@ kf_status kf_head_logits(kf_stage* s, int32_t rows, const void* hidden, kf_dtype
   kf_status st = head_common(s, rows, hidden, dtype);
   if (st != KF_OK) return st;
   if (!logits) return fail(KF_EINVAL, "logits is NULL");
+  if (!hidden) return head_launch(s, rows, nullptr, dtype, logits);  // kept rows: at most kMaxBatch
   const size_t esz = dtype == KF_BF16 ? 2 : 4;
   for (int r0 = 0; r0 < rows; r0 += kMaxBatch) {
     const int n = rows - r0 < kMaxBatch ? rows - r0 : kMaxBatch;

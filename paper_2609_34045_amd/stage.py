@@ -267,7 +267,9 @@ class Stage:
         return KV(self, max_users, max_ctx, pages)
 
     # -- compute
-    def decode(self, kv: "KV", users, positions, tokens=None, hidden=None, out=None):
+    def decode(self, kv: "KV", users, positions, tokens=None, hidden=None, out=None, keep: bool = False):
+        """kf_stage_decode; with ``keep`` (a stage that holds the head) the output rows stay in the stage
+        for ``head_logits(None, rows)`` / ``head_argmax(None, rows)`` and None is returned."""
         import torch
         B = len(users)
         u = (ctypes.c_int32 * max(B, 1))(*users)
@@ -285,7 +287,10 @@ class Stage:
             _require_device(tokens, "tokens")
             if tokens.dtype != torch.int32:
                 raise TypeError("tokens must be int32")
-        if out is None:
+        if keep:
+            if out is not None:
+                raise ValueError("keep and out exclude each other")
+        elif out is None:
             out = torch.empty((B, self.shape.hidden), dtype=odt, device=src.device if src is not None else "cuda")
         else:
             _require_device(out, "out")
@@ -317,24 +322,29 @@ class Stage:
         _check(fn(self.handle, kv.handle, user, pos0, n, _ptr(tokens), _ptr(hidden), _ptr(out), io), name)
         return out
 
-    def head_logits(self, hidden, out=None):
-        import torch
+    def _head_rows(self, hidden, rows):
+        """(rows, dtype code, device) of a head call; hidden None means the rows the last decode kept."""
+        if hidden is None:
+            if rows is None:
+                raise ValueError("rows is needed when hidden is None (the rows the last decode kept)")
+            return int(rows), KF_F32, "cuda"
         _require_device(hidden, "hidden")
-        rows = int(hidden.shape[0])
+        return int(hidden.shape[0]), _io_dtype(hidden), hidden.device
+
+    def head_logits(self, hidden, out=None, rows: int | None = None):
+        import torch
+        n, dt, dev = self._head_rows(hidden, rows)
         if out is None:
-            out = torch.empty((rows, self.shape.vocab), dtype=torch.float32, device=hidden.device)
-        _check(self._lib.kf_head_logits(self.handle, rows, _ptr(hidden), _io_dtype(hidden), _ptr(out)),
-               "kf_head_logits")
+            out = torch.empty((n, self.shape.vocab), dtype=torch.float32, device=dev)
+        _check(self._lib.kf_head_logits(self.handle, n, _ptr(hidden), dt, _ptr(out)), "kf_head_logits")
         return out
 
-    def head_argmax(self, hidden, with_max: bool = False):
+    def head_argmax(self, hidden, with_max: bool = False, rows: int | None = None):
         import torch
-        _require_device(hidden, "hidden")
-        rows = int(hidden.shape[0])
-        tok = torch.empty((rows,), dtype=torch.int32, device=hidden.device)
-        mx = torch.empty((rows,), dtype=torch.float32, device=hidden.device) if with_max else None
-        _check(self._lib.kf_head_argmax(self.handle, rows, _ptr(hidden), _io_dtype(hidden), _ptr(tok), _ptr(mx)),
-               "kf_head_argmax")
+        n, dt, dev = self._head_rows(hidden, rows)
+        tok = torch.empty((n,), dtype=torch.int32, device=dev)
+        mx = torch.empty((n,), dtype=torch.float32, device=dev) if with_max else None
+        _check(self._lib.kf_head_argmax(self.handle, n, _ptr(hidden), dt, _ptr(tok), _ptr(mx)), "kf_head_argmax")
         return (tok, mx) if with_max else tok
 
 

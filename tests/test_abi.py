@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.kf_abi_version() == 4
+    assert lib.kf_abi_version() == 5
 
 
 def _comment_before(text: str, name: str) -> str:

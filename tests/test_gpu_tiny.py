@@ -158,6 +158,52 @@ def test_head_tokens_logits_argmax(torch, st, model):
     g.close()
 
 
+def test_head_reads_kept_rows(torch, st, model):
+    """A head stage's decode may keep its output rows for the head instead of returning them (the
+    member that holds the last blocks also samples): the head then reads the fp32 residual at batch 1
+    and its fp16 copy at batch 2-4.  Logits and greedy tokens match the oracle.  The kept rows serve
+    only a head call with the decode's batch, and only until the next decode returns its rows; a stage
+    without the head cannot keep them."""
+    g, kv, o = make(st, model, head=True)
+    for u, n in ((0, 24), (1, 9), (2, 40)):
+        toks = synth.tokens(CFG, 10 + u, n, SHAPE.vocab)
+        assert_hidden_close(host(g.prefill(kv, u, 0, tokens=dev(torch, toks))), o.prefill(u, 0, tokens=toks),
+                            what=f"prefill {u}")
+    rng = np.random.default_rng(5)
+    for step, users in enumerate(([0, 1, 2], [2], [1, 0], [0, 1, 2])):
+        pos = [kv.len(u) for u in users]
+        toks = rng.integers(0, SHAPE.vocab, len(users)).astype(np.int32)
+        assert g.decode(kv, users, pos, tokens=dev(torch, toks), keep=True) is None
+        ref = o.decode(users, pos, tokens=toks)
+        lg = host(g.head_logits(None, rows=len(users)))
+        lr = o.logits(ref)
+        assert_hidden_close(lg, lr, rtol=1e-2, what=f"logits of the kept rows, step {step}")
+        t, mx = g.head_argmax(None, with_max=True, rows=len(users))
+        t = t.cpu().numpy()
+        for b in range(len(users)):
+            assert argmax_agrees(int(t[b]), int(np.argmax(lr[b])), lr[b], lg[b])
+            assert float(mx[b]) == pytest.approx(float(lg[b, int(t[b])]), rel=1e-6)
+        with pytest.raises(st.KFError) as e:  # another row count
+            g.head_argmax(None, rows=len(users) % 4 + 1)
+        assert e.value.status == st.KF_ESTATE
+    pos = [kv.len(0)]
+    y = g.decode(kv, [0], pos, tokens=dev(torch, np.array([7], dtype=np.int32)))  # returns its rows
+    assert_hidden_close(host(y), o.decode([0], pos, tokens=np.array([7])), what="returning decode")
+    with pytest.raises(st.KFError) as e:  # nothing kept any more
+        g.head_logits(None, rows=1)
+    assert e.value.status == st.KF_ESTATE
+    kv.close()
+    g.close()
+    g2, kv2, _ = make(st, model)
+    with pytest.raises(st.KFError) as e:
+        g2.decode(kv2, [0], [0], hidden=dev(torch, synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 0, 1, SHAPE.hidden)),
+                  keep=True)
+    assert e.value.status == st.KF_EINVAL
+    assert kv2.len(0) == 0
+    kv2.close()
+    g2.close()
+
+
 def test_argmax_on_identical_hidden_batch(torch, st, model):
     g, kv, o = make(st, model, head=True)
     h = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 50, 4, SHAPE.hidden)
