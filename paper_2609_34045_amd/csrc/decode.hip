@@ -827,6 +827,286 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
   }
 }
 
+// ------------------------------------------------------------------ attention on the matrix cores
+// The same split-KV partials as attn_decode_kernel, with the products on 16x16
+// MFMAs.  Per block of 16 keys: S^T = K Q^T (16 keys x 16 query slots: the G
+// heads of the group, zero-padded) and O^T += V^T P^T.  Wave w of the
+// workgroup takes the split's blocks w, w + 4, ...; each block's K and V rows
+// come into a two-stage LDS ring of the wave's own by direct global->LDS loads,
+// so the next block is in flight while one is computed, and the waves need no
+// barrier until the final merge of their four states.  K fragments are plain
+// 16-byte LDS reads (lane l: key l % 16, one 16-byte chunk); V^T fragments are
+// transpose reads (lane l: 4 keys of one d).  The score tile's lane layout
+// (lane l: keys 4 (l / 16) .. + 3 of head l % 16) is exactly the P^T operand
+// of the P V MFMA, so the softmax moves no data besides the maximum and the sum
+// over the four 16-lane groups that share a head.  The vector work per key is a
+// few instructions instead of the dot products, lane-group reductions and
+// packed P V of attn_decode_kernel.  Blocks with per-head q/k norms keep that
+// kernel (it also normalises and rotates q and the new key).
+namespace {
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void* dk_lds_ptr;
+
+// Wait until at most N of this wave's vector memory operations are outstanding
+// (direct loads count until their LDS write is done).
+template <int N>
+__device__ __forceinline__ void dk_wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(N | (0x7 << 4) | (0xF << 8));
+}
+
+// Slot of 16-byte chunk c of key row r in a block tile.  A K fragment read
+// takes one chunk of 16 consecutive rows per 16 lanes, a V transpose read two
+// neighbouring chunks of 8 consecutive rows per 32 lanes; f(r) puts both on
+// distinct 16-byte bank groups of the 64-bank LDS (HD 64: two rows per line).
+template <int HD>
+__device__ __forceinline__ int dk_slot(int r, int c) {
+  return HD == 128 ? c ^ (((r & 7) << 1) | ((r >> 3) & 1)) : c ^ ((((r >> 1) & 3) << 1) | ((r >> 3) & 1));
+}
+
+// max / sum of x over lanes l and l ^ 16 (permlane16_swap with x in both
+// operands leaves x[l] and x[l ^ 16] in the two results), and over l and l ^ 32.
+__device__ __forceinline__ float dk_max16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float dk_max32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float dk_sum16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float dk_sum32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ uint32_t dk_pack(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+}
+
+// V^T fragments of one block: transpose reads at LDS byte addresses base + off[t].
+// They are issued as inline assembly, followed by an explicit wait for their
+// results: the compiler would otherwise wait for every direct load in flight
+// (including the next block's) before the first transpose read.  The wait takes
+// the results as operands, so no use of them can be scheduled above it.
+template <int NT>
+__device__ __forceinline__ void dk_read_vt(uint32_t base, const int (&off)[NT], v2u (&vf)[NT]) {
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(vf[t]) : "v"(base + off[t]) : "memory");
+  if constexpr (NT == 8)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(vf[0]), "+v"(vf[1]), "+v"(vf[2]), "+v"(vf[3]), "+v"(vf[4]), "+v"(vf[5]), "+v"(vf[6]),
+                   "+v"(vf[7])::"memory");
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(vf[0]), "+v"(vf[1]), "+v"(vf[2]), "+v"(vf[3])::"memory");
+}
+}  // namespace
+
+#ifndef KF_ATTN_LAZY
+#define KF_ATTN_LAZY 8.0f
+#endif
+
+template <int HD>
+__global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnParams p) {
+  constexpr int KB = 16;             // keys per block
+  constexpr int ROWB = HD * 2;       // bytes per key row
+  constexpr int CPR = ROWB / 16;     // 16-byte chunks per row
+  constexpr int TILEB = KB * ROWB;   // K (or V) of one block
+  constexpr int STAGEB = 2 * TILEB;  // K tile, then V tile
+  constexpr int WAVEB = 2 * STAGEB;  // two stages per wave
+  constexpr int LPT = TILEB / 1024;  // direct loads (1 KB per wave) per tile
+  constexpr int RPL = 1024 / ROWB;   // key rows per direct load
+  constexpr int NS = HD / 32;        // S MFMA steps (32 d each)
+  constexpr int NT = HD / 16;        // O^T tiles (16 d each)
+  constexpr float kLazy = KF_ATTN_LAZY;
+  static_assert(HD == 64 || HD == 128, "head dim");
+  static_assert(kKvPage % KB == 0 && kAttnMaxSplit / kKvPage <= 64, "blocks within pages");
+  static_assert(HD * 16 * 4 + 32 * 4 <= WAVEB, "a wave's final state fits its stages");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * WAVEB];
+
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = p.nq / p.nkv;  // query heads per KV head, at most 16
+  const int len = p.len[b];
+  const int s0 = split * p.split;
+  const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
+  const int nb = nk > 0 ? (nk + KB - 1) / KB : 0;
+  const int cw = nb > wave ? (nb - wave + 3) / 4 : 0;  // this wave's blocks: wave + 4 i, i < cw
+  const int hq0 = g * G, u = p.users[b];
+  const int hn = lane & 15, q4 = lane >> 4;  // MFMA column (query slot) and 16-lane group
+  uint8_t* region = smem + wave * WAVEB;
+
+  // The query slots as fp16 B operands, scaled to log2 units: slot hn, d = 32 s + 8 q4 .. + 7.
+  v4f qlo[NS], qhi[NS];
+  {
+    const bool hv = hn < G;
+    const float* qr = p.q + (int64_t)b * p.nq * HD + (int64_t)(hq0 + (hv ? hn : 0)) * HD;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const v4f* src = reinterpret_cast<const v4f*>(qr + 32 * s + 8 * q4);
+      qlo[s] = src[0];
+      qhi[s] = src[1];
+    }
+  }
+
+  // A paged cache's page ids for the split (at most kAttnMaxSplit / kKvPage;
+  // the split starts on a page boundary), lane i holding the split's page i.
+  int pid = 0;
+  if (p.kv.table && lane * kKvPage < nk) pid = p.kv.table[u * p.kv.ppu + s0 / kKvPage + lane];
+  auto block_off = [&](int blk) -> int64_t {  // element offset of the block's first key row
+    const int k = blk * KB, i = k / kKvPage;
+    const int page = p.kv.table ? __builtin_amdgcn_readlane(pid, i) : u * p.kv.ppu + s0 / kKvPage + i;
+    return (int64_t)page * p.kv.page_stride + ((int64_t)g * kKvPage + k % kKvPage) * HD;
+  };
+  // Direct load j of a tile fills rows RPL j ..; lane l writes row RPL j + l / CPR,
+  // slot l % CPR, so it fetches the chunk that belongs in that slot.  Rows past
+  // the split's last key repeat that key (a written row of the same page): their
+  // scores are masked, and their values stay finite.
+  int drow[LPT], dchunk[LPT];
+#pragma unroll
+  for (int j = 0; j < LPT; ++j) {
+    drow[j] = RPL * j + lane / CPR;
+    dchunk[j] = dk_slot<HD>(drow[j], lane % CPR) * 16;
+  }
+  auto issue = [&](int i) {  // this wave's block i into stage i % 2
+    const int blk = 4 * i + wave;
+    const int64_t off = block_off(blk);
+    const int last = nk - 1 - blk * KB;
+    uint8_t* st = region + (i & 1) * STAGEB;
+    const char* kb = reinterpret_cast<const char*>(p.kc + off);
+    const char* vb = reinterpret_cast<const char*>(p.vc + off);
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int byte = min(drow[j], last) * ROWB + dchunk[j];
+      // (named operands: the host pass drops the kernel's launch stub when a
+      // builtin's pointer argument is a compound expression)
+      const char* ks = kb + byte;
+      const char* vs = vb + byte;
+      uint8_t* kd = st + 1024 * j;
+      uint8_t* vd = st + TILEB + 1024 * j;
+      __builtin_amdgcn_global_load_lds(ks, (dk_lds_ptr)kd, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vs, (dk_lds_ptr)vd, 16, 0, 0);
+    }
+  };
+  if (cw > 0) issue(0);
+  if (cw > 1) issue(1);
+
+  h8 qf[NS];
+  {
+    const float sc = hn < G ? p.scale_log2 : 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qf[s] = h8{(_Float16)(qlo[s].x * sc), (_Float16)(qlo[s].y * sc), (_Float16)(qlo[s].z * sc),
+                 (_Float16)(qlo[s].w * sc), (_Float16)(qhi[s].x * sc), (_Float16)(qhi[s].y * sc),
+                 (_Float16)(qhi[s].z * sc), (_Float16)(qhi[s].w * sc)};
+  }
+  // Fragment offsets within a stage.  K, step s: row hn, chunk 4 s + q4.  V^T,
+  // tile t: key row 4 q4 + (lane / 4) % 4, d = 16 t + 4 (lane % 4) .. + 3.
+  int koff[NS], voff[NT];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) koff[s] = hn * ROWB + dk_slot<HD>(hn, 4 * s + q4) * 16;
+  {
+    const int key = 4 * q4 + ((lane >> 2) & 3), j = lane & 3;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int dd = 16 * t + 4 * j;
+      voff[t] = key * ROWB + dk_slot<HD>(key, dd >> 3) * 16 + (dd & 7) * 2;
+    }
+  }
+  const uint32_t region_lds = (uint32_t)(uintptr_t)(dk_lds_ptr)region;
+
+  v4f o[NT];  // O^T tile t: lane holds d = 16 t + 4 q4 + r of query slot hn
+#pragma unroll
+  for (int t = 0; t < NT; ++t) o[t] = v4f{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+
+  for (int i = 0; i < cw; ++i) {
+    if (i + 1 < cw) dk_wait_vm<2 * LPT>();  // block i has landed; block i + 1 may be in flight
+    else dk_wait_vm<0>();
+    asm volatile("" ::: "memory");  // no LDS read of the block moves above the wait
+    const uint8_t* st = region + (i & 1) * STAGEB;
+    v4f sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const v4u kf = *reinterpret_cast<const v4u*>(st + koff[s]);
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, kf), qf[s], sc, 0, 0, 0);
+    }
+    const int k0 = (4 * i + wave) * KB + 4 * q4;  // this lane's first key, relative to the split
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (k0 + r >= nk) sc[r] = -INFINITY;
+    // Online softmax.  The reference maximum moves only when the block's
+    // maximum exceeds it by more than kLazy (log2 units), so probabilities stay
+    // below 2^kLazy (fp16 holds them as exactly as values below 1) and the
+    // rescale of O is skipped in nearly every block.  A block always holds a
+    // valid key, so its maximum is finite.
+    float mb = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+    mb = dk_max32(dk_max16(mb));
+    const float m_new = mb > m_run + kLazy ? mb : m_run;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 while m_run is -inf
+    const uint32_t w0 = dk_pack(__builtin_amdgcn_exp2f(sc[0] - m_new), __builtin_amdgcn_exp2f(sc[1] - m_new));
+    const uint32_t w1 = dk_pack(__builtin_amdgcn_exp2f(sc[2] - m_new), __builtin_amdgcn_exp2f(sc[3] - m_new));
+    // the sum is taken over the fp16 probabilities that the P V product uses
+    const float ls = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w1), ones,
+                                            __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w0), ones, 0.f, false), false);
+    l_run = l_run * alpha + ls;
+    m_run = m_new;
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) o[t] *= alpha;
+    }
+    v2u vf[NT];
+    dk_read_vt<NT>(region_lds + (uint32_t)((i & 1) * STAGEB + TILEB), voff, vf);
+    const h4 pf = __builtin_bit_cast(h4, v2u{w0, w1});
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(h4, vf[t]), pf, o[t], 0, 0, 0);
+    if (i + 2 < cw) issue(i + 2);  // into the stage just read
+  }
+  l_run = dk_sum32(dk_sum16(l_run));  // over the four key groups of the head
+
+  // The four waves' states (O^T [d][slot], then max and sum per slot) meet in
+  // LDS and are merged into the split's partial (max, sum, unnormalised acc).
+  float* sw = reinterpret_cast<float*>(region);
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sw[(16 * t + 4 * q4 + r) * 16 + hn] = o[t][r];
+  if (q4 == 0) {
+    sw[HD * 16 + hn] = m_run;
+    sw[HD * 16 + 16 + hn] = l_run;
+  }
+  __syncthreads();
+  for (int e = tid; e < G * HD; e += 256) {
+    const int h = e / HD, d = e % HD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, reinterpret_cast<const float*>(smem + w * WAVEB)[HD * 16 + h]);
+    float v = 0.f, l = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float* s = reinterpret_cast<const float*>(smem + w * WAVEB);
+        const float f = exp2f(s[HD * 16 + h] - M);  // 0 for a wave without keys (its max is -inf)
+        v += f * s[d * 16 + h];
+        l += f * s[HD * 16 + 16 + h];
+      }
+    }
+    const int64_t row = ((int64_t)b * p.nq + hq0 + h) * p.max_split + split;
+    p.part_acc[row * HD + d] = v;
+    if (d == 0) {
+      p.part_ml[row * 2] = M;
+      p.part_ml[row * 2 + 1] = l;
+    }
+  }
+}
+
 // Merge of the split-KV partials of one (head h, row b): weights 2^(m_s - M)
 // over the splits that saw keys (M their largest max), the weighted partial
 // vectors summed and divided by the weighted partial sums.  The split weights are
@@ -1252,9 +1532,16 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   return hipErrorInvalidValue;
 }
 
+#ifndef KF_ATTN_MFMA
+#define KF_ATTN_MFMA 1
+#endif
 template <int HD, int G>
 static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
   const dim3 grid(p.n_split, p.nkv, batch);
+  if (KF_ATTN_MFMA && p.kraw == nullptr) {
+    hipLaunchKernelGGL(attn_decode_mfma_kernel<HD>, grid, dim3(256), 0, s, p);
+    return hipGetLastError();
+  }
   // Two chunks in flight per wave pay off only where few workgroups stream long
   // splits (batch 1, 512 keys or more: 8B-shaped 32K context 33.9 -> 29.8 us);
   // elsewhere the 36 extra VGPRs cost more in occupancy than they gain.
