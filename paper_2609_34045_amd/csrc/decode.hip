@@ -830,11 +830,11 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 // ------------------------------------------------------------------ attention on the matrix cores
 // The same split-KV partials as attn_decode_kernel, with the products on 16x16
 // MFMAs.  Per block of 16 keys: S^T = K Q^T (16 keys x 16 query slots: the G
-// heads of the group, zero-padded) and O^T += V^T P^T.  Wave w of the
-// workgroup takes the split's blocks w, w + 4, ...; each block's K and V rows
+// heads of the group, zero-padded) and O^T += V^T P^T.  Wave w of the NW-wave
+// workgroup takes the split's blocks w, w + NW, ...; each block's K and V rows
 // come into a two-stage LDS ring of the wave's own by direct global->LDS loads,
 // so the next block is in flight while one is computed, and the waves need no
-// barrier until the final merge of their four states.  K fragments are plain
+// barrier until the final merge of their states.  K fragments are plain
 // 16-byte LDS reads (lane l: key l % 16, one 16-byte chunk); V^T fragments are
 // transpose reads (lane l: 4 keys of one d).  The score tile's lane layout
 // (lane l: keys 4 (l / 16) .. + 3 of head l % 16) is exactly the P^T operand
@@ -842,7 +842,12 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 // over the four 16-lane groups that share a head.  The vector work per key is a
 // few instructions instead of the dot products, lane-group reductions and
 // packed P V of attn_decode_kernel.  Blocks with per-head q/k norms keep that
-// kernel (it also normalises and rotates q and the new key).
+// kernel (it also normalises and rotates q and the new key).  Splits may start
+// anywhere on a 16-key boundary; from batch 2 the host sizes them for about one
+// workgroup per CU.  Measured against a deeper ring with K fragments read
+// straight from memory (16 rows x 64 bytes per load: slower), eight-wave
+// workgroups one per CU, and a split score chain with early V^T reads (both
+// no faster).
 namespace {
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef unsigned v2u __attribute__((ext_vector_type(2)));
@@ -911,8 +916,8 @@ __device__ __forceinline__ void dk_read_vt(uint32_t base, const int (&off)[NT], 
 #define KF_ATTN_LAZY 8.0f
 #endif
 
-template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnParams p) {
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_decode_mfma_kernel(const AttnParams p) {
   constexpr int KB = 16;             // keys per block
   constexpr int ROWB = HD * 2;       // bytes per key row
   constexpr int CPR = ROWB / 16;     // 16-byte chunks per row
@@ -927,21 +932,17 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnPara
   static_assert(HD == 64 || HD == 128, "head dim");
   static_assert(kKvPage % KB == 0 && kAttnMaxSplit / kKvPage <= 64, "blocks within pages");
   static_assert(HD * 16 * 4 + 32 * 4 <= WAVEB, "a wave's final state fits its stages");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * WAVEB];
+  static_assert(NW * WAVEB <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NW * WAVEB];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = p.nq / p.nkv;  // query heads per KV head, at most 16
-  const int len = p.len[b];
-  const int s0 = split * p.split;
-  const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
-  const int nb = nk > 0 ? (nk + KB - 1) / KB : 0;
-  const int cw = nb > wave ? (nb - wave + 3) / 4 : 0;  // this wave's blocks: wave + 4 i, i < cw
-  const int hq0 = g * G, u = p.users[b];
+  const int hq0 = g * G;
   const int hn = lane & 15, q4 = lane >> 4;  // MFMA column (query slot) and 16-lane group
-  uint8_t* region = smem + wave * WAVEB;
 
-  // The query slots as fp16 B operands, scaled to log2 units: slot hn, d = 32 s + 8 q4 .. + 7.
+  // The query slots as fp16 B operands, scaled to log2 units: slot hn, d = 32 s + 8 q4 .. + 7
+  // (requested first: the previous kernel has just written them).
   v4f qlo[NS], qhi[NS];
   {
     const bool hv = hn < G;
@@ -953,14 +954,36 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnPara
       qhi[s] = src[1];
     }
   }
+  asm volatile("" ::: "memory");  // the query loads go out before the exit test below
+  const int len = p.len[b];
+  const int s0 = split * p.split;
+  const int nk = min(s0 + p.split, len) - s0;
+  if (nk <= 0) {  // a trailing split of a shorter row: its partial is empty, (max, sum, acc) = (-inf, 0, 0)
+    for (int e = tid; e < G * HD; e += 64 * NW) {
+      const int h = e / HD, d = e % HD;
+      const int64_t row = ((int64_t)b * p.nq + hq0 + h) * p.max_split + split;
+      p.part_acc[row * HD + d] = 0.f;
+      if (d == 0) {
+        p.part_ml[row * 2] = -INFINITY;
+        p.part_ml[row * 2 + 1] = 0.f;
+      }
+    }
+    return;
+  }
+  const int nb = (nk + KB - 1) / KB;
+  const int cw = nb > wave ? (nb - wave + NW - 1) / NW : 0;  // this wave's blocks: wave + NW i, i < cw
+  const int u = p.users[b];
+  uint8_t* region = smem + wave * WAVEB;
 
-  // A paged cache's page ids for the split (at most kAttnMaxSplit / kKvPage;
-  // the split starts on a page boundary), lane i holding the split's page i.
+  // A paged cache's page ids for the split (at most kAttnMaxSplit / kKvPage + 1:
+  // the split starts at key kp0 of its first page), lane i holding the split's
+  // page i.  A block (16 keys, 16-aligned) lies in one page.
+  const int kp0 = s0 % kKvPage, pg0 = s0 / kKvPage;
   int pid = 0;
-  if (p.kv.table && lane * kKvPage < nk) pid = p.kv.table[u * p.kv.ppu + s0 / kKvPage + lane];
+  if (p.kv.table && lane * kKvPage < kp0 + nk) pid = p.kv.table[u * p.kv.ppu + pg0 + lane];
   auto block_off = [&](int blk) -> int64_t {  // element offset of the block's first key row
-    const int k = blk * KB, i = k / kKvPage;
-    const int page = p.kv.table ? __builtin_amdgcn_readlane(pid, i) : u * p.kv.ppu + s0 / kKvPage + i;
+    const int k = kp0 + blk * KB, i = k / kKvPage;
+    const int page = p.kv.table ? __builtin_amdgcn_readlane(pid, i) : u * p.kv.ppu + pg0 + i;
     return (int64_t)page * p.kv.page_stride + ((int64_t)g * kKvPage + k % kKvPage) * HD;
   };
   // Direct load j of a tile fills rows RPL j ..; lane l writes row RPL j + l / CPR,
@@ -974,7 +997,7 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnPara
     dchunk[j] = dk_slot<HD>(drow[j], lane % CPR) * 16;
   }
   auto issue = [&](int i) {  // this wave's block i into stage i % 2
-    const int blk = 4 * i + wave;
+    const int blk = NW * i + wave;
     const int64_t off = block_off(blk);
     const int last = nk - 1 - blk * KB;
     uint8_t* st = region + (i & 1) * STAGEB;
@@ -1037,7 +1060,7 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnPara
       const v4u kf = *reinterpret_cast<const v4u*>(st + koff[s]);
       sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, kf), qf[s], sc, 0, 0, 0);
     }
-    const int k0 = (4 * i + wave) * KB + 4 * q4;  // this lane's first key, relative to the split
+    const int k0 = (NW * i + wave) * KB + 4 * q4;  // this lane's first key, relative to the split
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       if (k0 + r >= nk) sc[r] = -INFINITY;
@@ -1071,8 +1094,8 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnPara
   }
   l_run = dk_sum32(dk_sum16(l_run));  // over the four key groups of the head
 
-  // The four waves' states (O^T [d][slot], then max and sum per slot) meet in
-  // LDS and are merged into the split's partial (max, sum, unnormalised acc).
+  // The waves' states (O^T [d][slot], then max and sum per slot) meet in LDS
+  // and are merged into the split's partial (max, sum, unnormalised acc).
   float* sw = reinterpret_cast<float*>(region);
 #pragma unroll
   for (int t = 0; t < NT; ++t)
@@ -1083,15 +1106,15 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(const AttnPara
     sw[HD * 16 + 16 + hn] = l_run;
   }
   __syncthreads();
-  for (int e = tid; e < G * HD; e += 256) {
+  for (int e = tid; e < G * HD; e += 64 * NW) {
     const int h = e / HD, d = e % HD;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, reinterpret_cast<const float*>(smem + w * WAVEB)[HD * 16 + h]);
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, reinterpret_cast<const float*>(smem + w * WAVEB)[HD * 16 + h]);
     float v = 0.f, l = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < NW; ++w) {
         const float* s = reinterpret_cast<const float*>(smem + w * WAVEB);
         const float f = exp2f(s[HD * 16 + h] - M);  // 0 for a wave without keys (its max is -inf)
         v += f * s[d * 16 + h];
@@ -1539,7 +1562,7 @@ template <int HD, int G>
 static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
   const dim3 grid(p.n_split, p.nkv, batch);
   if (KF_ATTN_MFMA && p.kraw == nullptr) {
-    hipLaunchKernelGGL(attn_decode_mfma_kernel<HD>, grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((attn_decode_mfma_kernel<HD, kAttnMfmaWaves>), grid, dim3(64 * kAttnMfmaWaves), 0, s, p);
     return hipGetLastError();
   }
   // Two chunks in flight per wave pay off only where few workgroups stream long
@@ -1564,6 +1587,8 @@ static hipError_t attn_dispatch_g(const AttnParams& p, int batch, hipStream_t s)
     default: return hipErrorInvalidValue;
   }
 }
+
+bool attn_mfma_enabled() { return KF_ATTN_MFMA != 0; }
 
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s) {
   if (p.hd == 128) return attn_dispatch_g<128>(p, batch, s);

@@ -791,6 +791,35 @@ static void attn_split(int nkv, int batch, int64_t total_len, int max_len, int m
   *n_split = (max_len + sp - 1) / sp;
 }
 
+// Keys per split for the matrix-core attention kernel from batch 2: one
+// workgroup per CU over the keys of the whole batch (16-key granularity), but
+// at least one block per wave and at most KF_ATTN_MFMA_MAX_KEYS (five blocks
+// per wave), past which more workgroups in more rounds beat longer chains of
+// blocks.  Against the batch-1 rule (about twice the workgroups, page-aligned):
+// the 8B-shaped head stage's ragged rows (256 to 4096 keys) 11.1 -> 9.5 us,
+// four 8B-shaped rows of up to 32K keys 53.5 -> 48.7 us, 32B-shaped batch 4
+// unchanged (320-key splits either way).  At batch 1 the rule of attn_split
+// measured best.
+#ifndef KF_ATTN_MFMA_MAX_KEYS
+#define KF_ATTN_MFMA_MAX_KEYS 320
+#endif
+#ifndef KF_ATTN_MFMA_WG_PER_CU
+#define KF_ATTN_MFMA_WG_PER_CU 1
+#endif
+static void attn_split_mfma(int nkv, int64_t total_len, int max_len, int max_split, int n_cu, int* split,
+                            int* n_split) {
+  auto up = [](int64_t v) { return (int)((v + kAttnMfmaAlign - 1) / kAttnMfmaAlign * kAttnMfmaAlign); };
+  const int64_t wgs = (int64_t)KF_ATTN_MFMA_WG_PER_CU * n_cu;
+  int sp = up((total_len * nkv + wgs - 1) / wgs);
+  if (sp < 16 * kAttnMfmaWaves) sp = 16 * kAttnMfmaWaves;
+  if (sp > KF_ATTN_MFMA_MAX_KEYS) sp = KF_ATTN_MFMA_MAX_KEYS;
+  const int need = up((max_len + max_split - 1) / max_split);
+  if (sp < need) sp = need;
+  if (sp > kAttnMaxSplit) sp = kAttnMaxSplit;
+  *split = sp;
+  *n_split = (max_len + sp - 1) / sp;
+}
+
 kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* users, const int32_t* positions,
                           const int32_t* tokens_dev, const void* hidden_in_dev, void* hidden_out_dev, kf_dtype io) {
   if (!s || !kv) return fail(KF_EINVAL, "stage or kv is NULL");
@@ -820,8 +849,12 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   hipStream_t st = s->stream;
 
   int split, n_split;
-  attn_split(c.n_kv_heads, batch, total_len, max_len, kv->max_split, &split, &n_split);
-  if (split % kKvPage) return fail(KF_EINVAL, "split of %d keys is not a whole number of pages", split);
+  const bool attn_mfma = attn_mfma_enabled() && !c.qk_norm;
+  if (attn_mfma && batch > 1)
+    attn_split_mfma(c.n_kv_heads, total_len, max_len, kv->max_split, s->n_cu, &split, &n_split);
+  else attn_split(c.n_kv_heads, batch, total_len, max_len, kv->max_split, &split, &n_split);
+  if (split % (attn_mfma ? kAttnMfmaAlign : kKvPage))
+    return fail(KF_EINVAL, "split of %d keys breaks the attention kernel's alignment", split);
   int64_t upto[kMaxBatch];
   for (int b = 0; b < batch; ++b) upto[b] = (int64_t)positions[b] + 1;
   const kf_status gst = kv_grant(kv, batch, users, upto);

@@ -166,3 +166,48 @@ def test_8b_shape_paged_decode_with_injected_contexts(torch, st):
     print("paged 8B max row rel err", worst)
     kv.close()
     g.close()
+
+
+@pytest.mark.parametrize("which", ["tiny", "8b"])
+def test_batch4_decode_with_splits_inside_pages(torch, st, which):
+    """Batch-4 decode whose split-KV workgroups start inside cache pages.
+
+    From batch 2 the matrix-core attention takes splits of any multiple of 16
+    keys: about one workgroup per CU over the batch's keys.  These contexts make
+    that 80 keys (tiny shape, 2 KV heads) or 96 keys (8B shape, 8 KV heads), so
+    splits start at keys 16, 32 or 48 of a page, over scattered pages.
+    """
+    if which == "tiny":
+        shape, cfg_id, lays, ctx = TINY, 35, (0, 1), (3000, 2000, 2500, 900)
+    else:
+        shape, cfg_id, lays, ctx = synth.SHAPE_8B, 36, (6, 7), (1200, 500, 900, 60)
+    layers = {l: synth.layer_weights(shape, cfg_id, l) for l in lays}
+    max_ctx = max(ctx) + 8
+    npages = sum(pages_held(n + 3) for n in ctx)
+    g = st.Stage(shape, lays[0], lays[-1] + 1, layers, None)
+    kv = g.kv(4, max_ctx, pages=npages)
+    o = OracleStage(shape, lays[0], lays[-1] + 1, lambda l: layers[l], None, max_users=4, max_ctx=max_ctx)
+    full = {(l, u): synth.injected_kv(shape, cfg_id, l, u, n) for l in lays for u, n in enumerate(ctx)}
+    for p0 in range(0, max(ctx), PAGE):  # page by page, users in turn: every user's pages scattered
+        for u, n in enumerate(ctx):
+            if p0 >= n:
+                continue
+            m = min(PAGE, n - p0)
+            for l in lays:
+                kb, vb = full[(l, u)]
+                kv.write(l, u, p0, dev(torch, kb[p0:p0 + m].view(np.int16)), dev(torch, vb[p0:p0 + m].view(np.int16)))
+            kv.set_len(u, p0 + m)
+    for (l, u), (kb, vb) in full.items():
+        o.kv.inject(l, u, 0, kb, vb)
+    for u, n in enumerate(ctx):
+        o.kv.set_len(u, n)
+    worst = 0.0
+    users = [2, 0, 3, 1]
+    for step in range(3):
+        pos = [kv.len(u) for u in users]
+        x = synth.hidden_states(cfg_id, synth.STREAM_DECODE_HIDDEN, step, 4, shape.hidden)
+        y = g.decode(kv, users, pos, hidden=dev(torch, x))
+        worst = max(worst, assert_hidden_close(host(y), o.decode(users, pos, hidden=x), what=f"decode {step}"))
+    print(f"splits inside pages ({which}) max row rel err", worst)
+    kv.close()
+    g.close()
