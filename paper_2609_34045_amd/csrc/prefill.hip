@@ -276,9 +276,19 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   const int Z = gridDim.z, z = bz;
   const int blk0 = (int)((int64_t)nblk_all * z / Z), blk1 = (int)((int64_t)nblk_all * (z + 1) / Z);
   // A block of KB keys lies in one cache page (KB divides kKvPage, blocks start at multiples of KB).
-  auto block_off = [&](int blk) -> int64_t {
-    const int k0 = blk * KB;
-    return (int64_t)kv_page(kp, user, k0 / kKvPage) * kp.page_stride + ((int64_t)g * kKvPage + k0 % kKvPage) * HD;
+  // Page ids of a paged cache for blocks [pb, pb + 64) of the range, lane i
+  // holding block pb + i's (a block is one page), loaded outside the loop's
+  // issue points: a table load there would put a wait for every direct load
+  // in flight in front of the next block's loads.
+  static_assert(KB == kKvPage, "one page per key block");
+  int pb = blk0, pid = 0;
+  auto load_pids = [&]() {
+    pid = (kp.table && pb + lane < kp.ppu) ? kp.table[user * kp.ppu + pb + lane] : 0;
+  };
+  load_pids();
+  auto block_off = [&](int blk) -> int64_t {  // wave-uniform: the block's loads take a scalar base
+    const int page = kp.table ? __builtin_amdgcn_readlane(pid, blk - pb) : user * kp.ppu + blk;
+    return (int64_t)page * kp.page_stride + (int64_t)g * kKvPage * HD;
   };
 
   // Q^T fragments: lane holds query qi, d = 16 s + 8 half_sel .. +7.
@@ -308,11 +318,12 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   // every query of the workgroup, so the causal mask gives them weight 0; in
   // the block that holds nkeys - 1 they are loaded from that key instead, a
   // written row of the same page.
-  int dma_row[LPW], dma_chunk[LPW];
+  int dma_row[LPW], dma_chunk[LPW], dma_off[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
     dma_row[j] = RPI * (4 * j + wave) + lane / CPR;
     dma_chunk[j] = kv_slot<HD>(dma_row[j], lane % CPR) * 16;
+    dma_off[j] = dma_row[j] * ROWB + dma_chunk[j];
   }
   auto issue = [&](const uint16_t* cache, int blk, uint8_t* dst) {
     const int last = nkeys - 1 - blk * KB;
@@ -320,7 +331,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     if (last >= KB - 1) {
 #pragma unroll
       for (int j = 0; j < LPW; ++j) {
-        const char* src = base + (dma_row[j] * ROWB + dma_chunk[j]);
+        const char* src = base + dma_off[j];
         uint8_t* d = dst + 1024 * (4 * j + wave);
         __builtin_amdgcn_global_load_lds(src, (lds_ptr)d, 16, 0, 0);
       }
@@ -440,9 +451,9 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     for (int i = 0; i < kRing; ++i) ring[i] = vread(i);
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const v4u cur = ring[i % kRing];
+      // the MFMA takes the slot before its refill is issued (no register copy)
+      o[i / NP] = mfma32(ring[i % kRing], pf[(i % NP) / 2][i % 2], o[i / NP]);
       if (i + kRing < NI) ring[i % kRing] = vread(i + kRing);
-      o[i / NP] = mfma32(cur, pf[(i % NP) / 2][i % 2], o[i / NP]);
     }
   };
 
@@ -459,9 +470,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     for (int i = 0; i < kRing; ++i) ring[i] = kread(ks, i);
 #pragma unroll
     for (int i = 0; i < NI_S; ++i) {
-      const v4u cur = ring[i % kRing];
+      st[i / NS] = mfma32(ring[i % kRing], qf[i % NS], st[i / NS]);
       if (i + kRing < NI_S) ring[i % kRing] = kread(ks, i + kRing);
-      st[i / NS] = mfma32(cur, qf[i % NS], st[i / NS]);
     }
   };
 
@@ -488,9 +498,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     for (int i = 0; i < kRing; ++i) ring[i] = kread(ks, i);
 #pragma unroll
     for (int i = 0; i < NI_S; ++i) {
-      const v4u cur = ring[i % kRing];
+      st[i / NS] = mfma32(ring[i % kRing], qf[i % NS], st[i / NS]);
       if (i + kRing < NI_S) ring[i % kRing] = kread(ks, i + kRing);
-      st[i / NS] = mfma32(cur, qf[i % NS], st[i / NS]);
       if (i < MAXS) {
 #pragma unroll
         for (int u = i * MPS; u < (i + 1) * MPS; ++u) mb = fmaxf(mb, sc[u / 16][u % 16]);
@@ -532,6 +541,10 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   auto iteration = [&](int blk, f32x16 (&sc)[NT], f32x16 (&sn)[NT]) {
     attn_wait_loads();
     attn_barrier();
+    if (kp.table && blk + 2 >= pb + 64) {  // the window moves on (every 62 blocks)
+      pb = blk + 1;
+      load_pids();
+    }
     if (blk + 2 < blk1) issue(kc, blk + 2, kst(blk + 2));
     if (blk + 1 < blk1) issue(vc, blk + 1, vst(blk + 1));
     if (blk * KB + KB - 1 > pos0 + i0 + wave * 32) mask(blk, sc);
