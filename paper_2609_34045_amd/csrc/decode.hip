@@ -1150,6 +1150,18 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams a, uin
   __shared__ float red[4][HD];
   __shared__ float sM[4], sL[4];
 
+  // Wave w's first PRE splits (w, w + 4, ...) are requested with the (max, sum)
+  // pairs, so the weighted sum needs no second memory round trip; splits past
+  // ns re-read split ns - 1 (in bounds, finite) and get weight 0 below.
+  constexpr int PRE = 8;
+  float pre[PRE][DPL];
+#pragma unroll
+  for (int k = 0; k < PRE; ++k) {
+    const int sp = min(wave + 4 * k, ns - 1);
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) pre[k][i] = acc[(int64_t)sp * HD + i];
+  }
+
   float M = -INFINITY;
   for (int s = tid; s < ns; s += 256)
     if (ml[2 * s + 1] > 0.f) M = fmaxf(M, ml[2 * s]);
@@ -1171,8 +1183,15 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const AttnParams a, uin
   float o[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) o[i] = 0.f;
+#pragma unroll
+  for (int k = 0; k < PRE; ++k) {
+    const int sp = wave + 4 * k;
+    const float w = sp < ns ? wsm[sp] : 0.f;
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) o[i] += w * pre[k][i];
+  }
 #pragma unroll 8
-  for (int s = wave; s < ns; s += 4) {
+  for (int s = wave + 4 * PRE; s < ns; s += 4) {
     const float w = wsm[s];
 #pragma unroll
     for (int i = 0; i < DPL; ++i) o[i] += w * acc[(int64_t)s * HD + i];
