@@ -841,8 +841,8 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 // of the P V MFMA, so the softmax moves no data besides the maximum and the sum
 // over the four 16-lane groups that share a head.  The vector work per key is a
 // few instructions instead of the dot products, lane-group reductions and
-// packed P V of attn_decode_kernel.  Blocks with per-head q/k norms keep that
-// kernel (it also normalises and rotates q and the new key).  Splits may start
+// packed P V of attn_decode_kernel.  For blocks with per-head q/k norms it
+// also normalises and rotates the queries and the new key.  Splits may start
 // anywhere on a 16-key boundary; from batch 2 the host sizes them for about one
 // workgroup per CU.  Measured against a deeper ring with K fragments read
 // straight from memory (16 rows x 64 bytes per load: slower), eight-wave
@@ -1019,6 +1019,94 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_decode_mfma_ker
   if (cw > 0) issue(0);
   if (cw > 1) issue(1);
 
+  // Blocks with per-head q/k norms: q comes raw from the QKV GEMV.  Each query
+  // slot is RMS-normalised (gains gq; its squares summed over the four lanes
+  // that hold it) and rotated at the row's new position: the RoPE partner of
+  // d = 32 s + 8 q4 + j, d +- HD/2, is step s +- NS/2 of the same lane.
+  const bool qkn = p.kraw != nullptr;
+  const int npos = len - 1;  // row b's new position
+  if (qkn) {
+    float x[NS][8];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      x[s][0] = qlo[s].x; x[s][1] = qlo[s].y; x[s][2] = qlo[s].z; x[s][3] = qlo[s].w;
+      x[s][4] = qhi[s].x; x[s][5] = qhi[s].y; x[s][6] = qhi[s].z; x[s][7] = qhi[s].w;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ss += x[s][j] * x[s][j];
+    const float rs = 1.0f / sqrtf(dk_sum32(dk_sum16(ss)) / (float)HD + p.eps);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      float gf[8];
+      bf16x8(*reinterpret_cast<const v4u*>(p.gq + 32 * s + 8 * q4), gf);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[s][j] *= rs * gf[j];
+    }
+#pragma unroll
+    for (int s = 0; s < NS / 2; ++s) {
+      const v4f* cp = reinterpret_cast<const v4f*>(p.rope_cos + (int64_t)npos * (HD / 2) + 32 * s + 8 * q4);
+      const v4f* sp = reinterpret_cast<const v4f*>(p.rope_sin + (int64_t)npos * (HD / 2) + 32 * s + 8 * q4);
+      const v4f c0 = cp[0], c1 = cp[1], n0 = sp[0], n1 = sp[1];
+      const float c[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+      const float sn[8] = {n0.x, n0.y, n0.z, n0.w, n1.x, n1.y, n1.z, n1.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float a = x[s][j], bb = x[s + NS / 2][j];
+        x[s][j] = a * c[j] - bb * sn[j];
+        x[s + NS / 2][j] = bb * c[j] + a * sn[j];
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      qlo[s] = v4f{x[s][0], x[s][1], x[s][2], x[s][3]};
+      qhi[s] = v4f{x[s][4], x[s][5], x[s][6], x[s][7]};
+    }
+  }
+  // The new key of such a block: the wave whose block holds position npos
+  // normalises (gains gk) and rotates it from its raw projection, lane c < CPR
+  // taking 16-byte chunk c (partner chunk c +- CPR/2); it stores it to the cache
+  // for later steps and writes it over that row of its LDS tile once the
+  // block's direct loads have landed (the cache row they read was stale).
+  const int rel_new = npos - s0;
+  const bool own_new = qkn && rel_new >= 0 && rel_new < nk && (rel_new / KB) % NW == wave;
+  const int i_new = own_new ? (rel_new / KB) / NW : -1;
+  v4u knew = {0u, 0u, 0u, 0u};
+  if (own_new) {
+    const int c = lane % CPR, d0 = 8 * c;
+    const v4f* src = reinterpret_cast<const v4f*>(p.kraw + ((int64_t)b * p.nkv + g) * HD + d0);
+    const v4f lo = src[0], hi = src[1];
+    float x[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    float gf[8];
+    bf16x8(*reinterpret_cast<const v4u*>(p.gk + d0), gf);
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ss += x[j] * x[j];
+    const float rs = 1.0f / sqrtf(group_sum<CPR>(ss) / (float)HD + p.eps);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] *= rs * gf[j];
+    const int i0 = d0 % (HD / 2);
+    const float sgn = d0 < HD / 2 ? -1.f : 1.f;
+    float y[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) y[j] = CPR == 16 ? dpp<kDppRor8>(x[j]) : __shfl_xor(x[j], CPR / 2);
+    bool bad = false;
+    uint16_t k16[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float cs = p.rope_cos[(int64_t)npos * (HD / 2) + i0 + j], sn = p.rope_sin[(int64_t)npos * (HD / 2) + i0 + j];
+      k16[j] = f16_checked(x[j] * cs + sgn * y[j] * sn, bad);
+    }
+    knew = v4u{k16[0] | ((uint32_t)k16[1] << 16), k16[2] | ((uint32_t)k16[3] << 16),
+               k16[4] | ((uint32_t)k16[5] << 16), k16[6] | ((uint32_t)k16[7] << 16)};
+    if (lane < CPR) {
+      *reinterpret_cast<v4u*>(p.kc + kv_offset(p.kv, u, g, npos, HD) + d0) = knew;
+      raise_err(p.err_flag, bad, kErrF16Range);
+    }
+  }
+
   h8 qf[NS];
   {
     const float sc = hn < G ? p.scale_log2 : 0.f;
@@ -1054,6 +1142,8 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_decode_mfma_ker
     else dk_wait_vm<0>();
     asm volatile("" ::: "memory");  // no LDS read of the block moves above the wait
     const uint8_t* st = region + (i & 1) * STAGEB;
+    if (i == i_new && lane < CPR)  // the new key over its stale row (this wave's reads follow in order)
+      *reinterpret_cast<v4u*>(region + (i & 1) * STAGEB + (rel_new % KB) * ROWB + dk_slot<HD>(rel_new % KB, lane) * 16) = knew;
     v4f sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -1580,7 +1670,7 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
 template <int HD, int G>
 static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
   const dim3 grid(p.n_split, p.nkv, batch);
-  if (KF_ATTN_MFMA && p.kraw == nullptr) {
+  if (KF_ATTN_MFMA) {
     hipLaunchKernelGGL((attn_decode_mfma_kernel<HD, kAttnMfmaWaves>), grid, dim3(64 * kAttnMfmaWaves), 0, s, p);
     return hipGetLastError();
   }

@@ -14,9 +14,9 @@ constexpr int kAttnMaxSplit = 1024; // keys per split-KV workgroup, upper bound
 // slower: every workgroup repeats its head's merge of the split partials).
 constexpr int kOprojRows = 256;
 constexpr int kAttnMaxSplitCount = 1024;  // split-KV workgroups per (row, KV head), upper bound
-// Decode attention on the matrix cores (blocks without per-head q/k norms):
-// workgroups of kAttnMfmaWaves waves over splits of any multiple of
-// kAttnMfmaAlign keys (16-key blocks, one page or less each).
+// Decode attention on the matrix cores: workgroups of kAttnMfmaWaves waves over
+// splits of any multiple of kAttnMfmaAlign keys (16-key blocks, one page or
+// less each).
 #ifndef KF_ATTN_WAVES
 #define KF_ATTN_WAVES 4
 #endif
@@ -171,8 +171,8 @@ hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
-// Whether launch_attn_decode takes the matrix-core kernel for blocks without
-// per-head q/k norms (their splits may then be any multiple of kAttnMfmaAlign).
+// Whether launch_attn_decode takes the matrix-core kernel (its splits may then
+// be any multiple of kAttnMfmaAlign) rather than the vector-ALU one.
 bool attn_mfma_enabled();
 // Head h of row b merged from the attention partials in p, to o16[b][h*hd:(h+1)*hd]
 // (fp16) or, with o16 NULL, to o32[b][h*hd:(h+1)*hd] (fp32).

@@ -849,7 +849,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   hipStream_t st = s->stream;
 
   int split, n_split;
-  const bool attn_mfma = attn_mfma_enabled() && !c.qk_norm;
+  const bool attn_mfma = attn_mfma_enabled();
   if (attn_mfma && batch > 1)
     attn_split_mfma(c.n_kv_heads, total_len, max_len, kv->max_split, s->n_cu, &split, &n_split);
   else attn_split(c.n_kv_heads, batch, total_len, max_len, kv->max_split, &split, &n_split);
