@@ -531,305 +531,10 @@ void gemv_kernel(const GemvParams p) {
 }
 
 // ------------------------------------------------------------------ attention
-// Workgroup (split s, KV head g, row b) covers keys [s*split, min((s+1)*split, len_b)).
-// A key's hd elements are read by hd/8 lanes, 16 bytes each; all G query heads of
-// the group are scored against it, so each K/V byte is read once per KV head.
-// Each wave runs its own online softmax over chunks of 4 keys per lane group (K
-// and V of a chunk are loaded together, so one memory latency covers both, and
-// DEPTH chunks are in flight); the four waves' (max, sum, acc) states are merged
-// through LDS and written as the split's partial.  For blocks with per-head q/k
-// norms the kernel also normalises and rotates the queries, and the new key in
-// the workgroup that holds it.
-#ifndef KF_ATTN_J
-#define KF_ATTN_J 4
-#endif
-
-template <int HD, int G, int DEPTH>
-__global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
-  constexpr int LPK = HD / 8;      // lanes per key (one 16-byte slice each)
-  constexpr int KPW = 64 / LPK;    // key groups per wave
-  constexpr int J = KF_ATTN_J;     // keys per key group per chunk
-  constexpr int CH = KPW * J;      // keys per wave chunk
-  constexpr int SUB = 4 * KPW;     // (wave, key group) partial states per workgroup
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int len = p.len[b];
-  const int s0 = split * p.split;
-  const int nk = min(s0 + p.split, len) - s0;  // may be <= 0 for trailing splits
-  const int hq0 = g * G;
-
-  __shared__ float sacc[SUB][G][HD];
-  __shared__ float sl[SUB][G];
-  __shared__ float sm[4][G];
-
-  const int d0 = (lane % LPK) * 8;
-  const int kgrp = lane / LPK;
-  // The split starts on a page boundary (split sizes are multiples of kKvPage)
-  // and a wave's chunk of CH keys, which starts at a multiple of CH, lies in one
-  // page.  A paged cache's page ids for the split (at most kAttnMaxSplit /
-  // kKvPage) are loaded once, lane i holding the split's page i.
-  static_assert(kKvPage % CH == 0 && kAttnMaxSplit / kKvPage <= 64, "chunks within pages");
-  const int u = p.users[b], pg0 = s0 / kKvPage;
-  int pid = 0;
-  if (p.kv.table && lane * kKvPage < nk) pid = p.kv.table[u * p.kv.ppu + pg0 + lane];
-  const int64_t goff = (int64_t)g * kKvPage * HD + d0;
-  auto chunk_base = [&](int c) -> int64_t {  // c: the wave's chunk start, relative to s0
-    const int i = c / kKvPage;
-    const int page = p.kv.table ? __builtin_amdgcn_readlane(pid, i) : u * p.kv.ppu + pg0 + i;
-    return (int64_t)page * p.kv.page_stride + goff + (int64_t)(c % kKvPage) * HD;
-  };
-
-  float acc[G][8], m_run[G], l_run[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_run[h] = -INFINITY;
-    l_run[h] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[h][i] = 0.f;
-  }
-
-  // The first chunks' K and V are requested before the query, which the
-  // previous kernel has just written.  DEPTH chunks per wave are in flight:
-  // slot s holds the chunk processed at steps s, s + DEPTH, ... and is reloaded
-  // with the chunk DEPTH steps ahead once its values are in registers.
-  static_assert(DEPTH == 1 || DEPTH == 2, "one or two chunks in flight");
-  int c0 = wave * CH;
-  v4u kw[DEPTH][J], vw[DEPTH][J];
-  bool ok[DEPTH][J];
-  auto load_chunk = [&](int c, auto slot) {  // keys past nk re-read the chunk's first key (c < nk)
-    constexpr int sl = decltype(slot)::value;
-    const int64_t base = chunk_base(c);
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      const int r = j * KPW + kgrp;
-      ok[sl][j] = c + r < nk;
-      const int64_t at = base + (int64_t)(ok[sl][j] ? r : 0) * HD;
-      kw[sl][j] = *reinterpret_cast<const v4u*>(p.kc + at);
-      vw[sl][j] = *reinterpret_cast<const v4u*>(p.vc + at);
-    }
-  };
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, DEPTH - 1>;
-  if (c0 < nk) load_chunk(c0, S0{});
-  if (DEPTH > 1 && c0 + 4 * CH < nk) load_chunk(c0 + 4 * CH, S1{});
-
-  // Blocks with q/k norms: the workgroup whose split holds row b's new key
-  // requests that key's raw projection now, so that its latency overlaps the
-  // query's rather than following it.
-  const bool qkn = p.kraw != nullptr;
-  const int npos = len - 1;  // row b's new position
-  const bool own_new = qkn && nk > 0 && npos >= s0 && npos < s0 + nk;
-  v4f kr_lo = {0.f, 0.f, 0.f, 0.f}, kr_hi = kr_lo;
-  v4u kgain = {0u, 0u, 0u, 0u};
-  if (own_new && wave == 0) {
-    const v4f* src = reinterpret_cast<const v4f*>(p.kraw + ((int64_t)b * p.nkv + g) * HD + d0);
-    kr_lo = src[0];
-    kr_hi = src[1];
-    kgain = *reinterpret_cast<const v4u*>(p.gk + d0);
-  }
-
-  // Per-head norm + RoPE (blocks with q/k norms) of a head vector held as 8
-  // values per lane by the LPK lanes of a key group: the squares are summed over
-  // the group, and the rotation partner of dim d (d +- HD/2) sits LPK/2 lanes away.
-  // This lane's rotation factors (dims d0..d0+7 at the new position, sign folded
-  // into the sine) and the query gains: the same for every head of the group.
-  float rc[8], rsn[8], gqf[8];
-  if (qkn) {
-    const int i0 = d0 % (HD / 2);
-    const float sgn = d0 < HD / 2 ? -1.f : 1.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      rc[i] = p.rope_cos[(int64_t)npos * (HD / 2) + i0 + i];
-      rsn[i] = sgn * p.rope_sin[(int64_t)npos * (HD / 2) + i0 + i];
-    }
-    bf16x8(*reinterpret_cast<const v4u*>(p.gq + d0), gqf);
-  }
-  auto norm_rope = [&](float (&x)[8], const float (&gf)[8]) {
-    float ss = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
-    const float rs = 1.0f / sqrtf(group_sum<LPK>(ss) / (float)HD + p.eps);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] *= rs * gf[i];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {  // the partner dim (d +- HD/2) is LPK/2 lanes away
-      const float y = LPK == 16 ? dpp<kDppRor8>(x[i]) : __shfl_xor(x[i], LPK / 2);
-      x[i] = x[i] * rc[i] + y * rsn[i];
-    }
-  };
-
-  // The scaled query as fp16 pairs: a score is then 4 packed fp16 dot products
-  // (fp32 accumulation) against the key's fp16 values as stored in the cache.
-  h2 qh[G][4];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const v4f* src = reinterpret_cast<const v4f*>(p.q + (int64_t)b * p.nq * HD + (hq0 + h) * HD + d0);
-    const v4f lo0 = src[0], hi0 = src[1];
-    float x[8] = {lo0.x, lo0.y, lo0.z, lo0.w, hi0.x, hi0.y, hi0.z, hi0.w};
-    if (qkn) norm_rope(x, gqf);
-    const float sc = p.scale_log2;
-    qh[h][0] = __builtin_convertvector(f2{x[0] * sc, x[1] * sc}, h2);
-    qh[h][1] = __builtin_convertvector(f2{x[2] * sc, x[3] * sc}, h2);
-    qh[h][2] = __builtin_convertvector(f2{x[4] * sc, x[5] * sc}, h2);
-    qh[h][3] = __builtin_convertvector(f2{x[6] * sc, x[7] * sc}, h2);
-  }
-
-  // The new key (blocks with q/k norms): the workgroup whose split holds it
-  // normalises and rotates it once (wave 0), stores it to the cache for later
-  // steps and to LDS, and the lanes that loaded that slot from the cache take
-  // it from LDS instead.
-  __shared__ __attribute__((aligned(16))) uint16_t knew[HD];
-  if (own_new) {
-    if (wave == 0) {
-      float x[8] = {kr_lo.x, kr_lo.y, kr_lo.z, kr_lo.w, kr_hi.x, kr_hi.y, kr_hi.z, kr_hi.w};
-      float gkf[8];
-      bf16x8(kgain, gkf);
-      norm_rope(x, gkf);
-      if (kgrp == 0) {
-        bool bad = false;
-        uint16_t k16[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) k16[i] = f16_checked(x[i], bad);
-        const v4u kv16 = v4u{k16[0] | ((uint32_t)k16[1] << 16), k16[2] | ((uint32_t)k16[3] << 16),
-                             k16[4] | ((uint32_t)k16[5] << 16), k16[6] | ((uint32_t)k16[7] << 16)};
-        *reinterpret_cast<v4u*>(p.kc + kv_offset(p.kv, u, g, npos, HD) + d0) = kv16;
-        *reinterpret_cast<v4u*>(&knew[d0]) = kv16;
-        raise_err(p.err_flag, bad, kErrF16Range);
-      }
-    }
-    __syncthreads();
-  }
-
-  // One step: the chunk at c0, held in slot `slot`.
-  auto step = [&](auto slot) {
-    constexpr int sl = decltype(slot)::value;
-    if (own_new) {
-#pragma unroll
-      for (int j = 0; j < J; ++j)
-        if (s0 + c0 + j * KPW + kgrp == npos) kw[sl][j] = *reinterpret_cast<const v4u*>(&knew[d0]);
-    }
-    float sc[J][G];
-#pragma unroll
-    for (int j = 0; j < J; ++j) {
-      // Pairs are taken from the whole 8-half vector by shuffles (a bit cast of a
-      // single dword element of the loaded vector is lowered to element 0).
-      const h8 k8 = __builtin_bit_cast(h8, kw[sl][j]);
-      const h2 k0 = __builtin_shufflevector(k8, k8, 0, 1), k1 = __builtin_shufflevector(k8, k8, 2, 3),
-               k2 = __builtin_shufflevector(k8, k8, 4, 5), k3 = __builtin_shufflevector(k8, k8, 6, 7);
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float a = __builtin_amdgcn_fdot2(k0, qh[h][0], 0.f, false);
-        a = __builtin_amdgcn_fdot2(k1, qh[h][1], a, false);
-        a = __builtin_amdgcn_fdot2(k2, qh[h][2], a, false);
-        a = __builtin_amdgcn_fdot2(k3, qh[h][3], a, false);
-        sc[j][h] = group_sum<LPK>(a);
-      }
-    }
-    // V of key pairs (2m, 2m+1) regrouped per dimension: vp[m][i] = (v_2m[i], v_2m+1[i]),
-    // so P.V is a packed fp16 dot product per dimension and key pair.
-    static_assert(J % 2 == 0, "keys come in pairs");
-    h2 vp[J / 2][8];
-#pragma unroll
-    for (int m = 0; m < J / 2; ++m) {
-      const h8 a = __builtin_bit_cast(h8, vw[sl][2 * m]), c = __builtin_bit_cast(h8, vw[sl][2 * m + 1]);
-      vp[m][0] = __builtin_shufflevector(a, c, 0, 8);
-      vp[m][1] = __builtin_shufflevector(a, c, 1, 9);
-      vp[m][2] = __builtin_shufflevector(a, c, 2, 10);
-      vp[m][3] = __builtin_shufflevector(a, c, 3, 11);
-      vp[m][4] = __builtin_shufflevector(a, c, 4, 12);
-      vp[m][5] = __builtin_shufflevector(a, c, 5, 13);
-      vp[m][6] = __builtin_shufflevector(a, c, 6, 14);
-      vp[m][7] = __builtin_shufflevector(a, c, 7, 15);
-    }
-    bool okc[J];
-#pragma unroll
-    for (int j = 0; j < J; ++j) okc[j] = ok[sl][j];
-    // the chunk DEPTH steps ahead is in flight during this one's math
-    if (c0 + DEPTH * 4 * CH < nk) load_chunk(c0 + DEPTH * 4 * CH, slot);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float mc = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < J; ++j) mc = okc[j] ? fmaxf(mc, sc[j][h]) : mc;
-      // max over the wave's key groups (a chunk has at least one valid key, so mc is finite)
-      if (LPK == 8) mc = fmaxf(mc, dpp<kDppMirror>(mc));
-      mc = fmaxf(mc, __shfl_xor(mc, 16));
-      mc = fmaxf(mc, __shfl_xor(mc, 32));
-      const float m_new = fmaxf(m_run[h], mc);
-      const float alpha = __builtin_amdgcn_exp2f(m_run[h] - m_new);  // 0 while m_run is -inf
-      m_run[h] = m_new;
-      l_run[h] *= alpha;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[h][i] *= alpha;
-      float pj[J];
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        pj[j] = okc[j] ? __builtin_amdgcn_exp2f(sc[j][h] - m_new) : 0.f;
-        l_run[h] += pj[j];
-      }
-#pragma unroll
-      for (int m = 0; m < J / 2; ++m) {
-        const h2 pp = __builtin_convertvector(f2{pj[2 * m], pj[2 * m + 1]}, h2);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[h][i] = __builtin_amdgcn_fdot2(vp[m][i], pp, acc[h][i], false);
-      }
-    }
-  };
-  while (c0 < nk) {
-    step(S0{});
-    c0 += 4 * CH;
-    if (DEPTH > 1 && c0 < nk) {
-      step(S1{});
-      c0 += 4 * CH;
-    }
-  }
-
-  // Every lane's (key group, 8 dims) state goes to LDS; the running max is wave-uniform.
-  const int sub = wave * KPW + kgrp;
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) sacc[sub][h][d0 + i] = acc[h][i];
-  if ((lane % LPK) == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) sl[sub][h] = l_run[h];
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) sm[wave][h] = m_run[h];
-  }
-  __syncthreads();
-
-  // Merge the workgroup's states into this split's partial (max, sum, unnormalised acc).
-  for (int e = tid; e < G * HD; e += 256) {
-    const int h = e / HD, d = e % HD;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][h]);
-    float v = 0.f, l = 0.f;
-    if (M != -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float sw = exp2f(sm[w][h] - M);  // 0 for a wave without keys (its max is -inf)
-#pragma unroll
-        for (int k = 0; k < KPW; ++k) {
-          v += sw * sacc[w * KPW + k][h][d];
-          l += sw * sl[w * KPW + k][h];
-        }
-      }
-    }
-    const int64_t row = ((int64_t)b * p.nq + hq0 + h) * p.max_split + split;
-    p.part_acc[row * HD + d] = v;
-    if (d == 0) {
-      p.part_ml[row * 2] = M;
-      p.part_ml[row * 2 + 1] = l;
-    }
-  }
-}
-
-// ------------------------------------------------------------------ attention on the matrix cores
-// The same split-KV partials as attn_decode_kernel, with the products on 16x16
-// MFMAs.  Per block of 16 keys: S^T = K Q^T (16 keys x 16 query slots: the G
+// Split-KV decode attention with the products on 16x16 MFMAs.  A workgroup
+// (split s, KV head g, row b) covers keys [s*split, min((s+1)*split, len_b))
+// for all G query heads of the group, so each K/V byte is read once per KV
+// head, and writes the split's partial (max, sum, unnormalised acc).  Per block of 16 keys: S^T = K Q^T (16 keys x 16 query slots: the G
 // heads of the group, zero-padded) and O^T += V^T P^T.  Wave w of the NW-wave
 // workgroup takes the split's blocks w, w + NW, ...; each block's K and V rows
 // come into a two-stage LDS ring of the wave's own by direct global->LDS loads,
@@ -839,10 +544,10 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const AttnParams p) {
 // transpose reads (lane l: 4 keys of one d).  The score tile's lane layout
 // (lane l: keys 4 (l / 16) .. + 3 of head l % 16) is exactly the P^T operand
 // of the P V MFMA, so the softmax moves no data besides the maximum and the sum
-// over the four 16-lane groups that share a head.  The vector work per key is a
-// few instructions instead of the dot products, lane-group reductions and
-// packed P V of attn_decode_kernel.  For blocks with per-head q/k norms it
-// also normalises and rotates the queries and the new key.  Splits may start
+// over the four 16-lane groups that share a head: a few vector instructions
+// per key, where a vector-ALU kernel spent ~30 on dot products, 16-lane
+// reductions and packed P V.  For blocks with per-head q/k norms it also
+// normalises and rotates the queries and the new key.  Splits may start
 // anywhere on a 16-key boundary; from batch 2 the host sizes them for about one
 // workgroup per CU.  Measured against a deeper ring with K fragments read
 // straight from memory (16 rows x 64 bytes per load: slower), eight-wave
@@ -1664,45 +1369,16 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   return hipErrorInvalidValue;
 }
 
-#ifndef KF_ATTN_MFMA
-#define KF_ATTN_MFMA 1
-#endif
-template <int HD, int G>
-static hipError_t attn_launch(const AttnParams& p, int batch, hipStream_t s) {
-  const dim3 grid(p.n_split, p.nkv, batch);
-  if (KF_ATTN_MFMA) {
-    hipLaunchKernelGGL((attn_decode_mfma_kernel<HD, kAttnMfmaWaves>), grid, dim3(64 * kAttnMfmaWaves), 0, s, p);
-    return hipGetLastError();
-  }
-  // Two chunks in flight per wave pay off only where few workgroups stream long
-  // splits (batch 1, 512 keys or more: 8B-shaped 32K context 33.9 -> 29.8 us);
-  // elsewhere the 36 extra VGPRs cost more in occupancy than they gain.
-  if (batch == 1 && p.split >= 512) hipLaunchKernelGGL((attn_decode_kernel<HD, G, 2>), grid, dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((attn_decode_kernel<HD, G, 1>), grid, dim3(256), 0, s, p);
-  return hipGetLastError();
-}
-
-template <int HD>
-static hipError_t attn_dispatch_g(const AttnParams& p, int batch, hipStream_t s) {
-  switch (p.nq / p.nkv) {
-    case 1: return attn_launch<HD, 1>(p, batch, s);
-    case 2: return attn_launch<HD, 2>(p, batch, s);
-    case 3: return attn_launch<HD, 3>(p, batch, s);
-    case 4: return attn_launch<HD, 4>(p, batch, s);
-    case 5: return attn_launch<HD, 5>(p, batch, s);
-    case 6: return attn_launch<HD, 6>(p, batch, s);
-    case 7: return attn_launch<HD, 7>(p, batch, s);
-    case 8: return attn_launch<HD, 8>(p, batch, s);
-    default: return hipErrorInvalidValue;
-  }
-}
-
-bool attn_mfma_enabled() { return KF_ATTN_MFMA != 0; }
-
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s) {
-  if (p.hd == 128) return attn_dispatch_g<128>(p, batch, s);
-  if (p.hd == 64) return attn_dispatch_g<64>(p, batch, s);
-  return hipErrorInvalidValue;
+  if (p.nq % p.nkv || p.nq / p.nkv > 16) return hipErrorInvalidValue;  // query slots of one MFMA column block
+  const dim3 grid(p.n_split, p.nkv, batch);
+  if (p.hd == 128)
+    hipLaunchKernelGGL((attn_decode_mfma_kernel<128, kAttnMfmaWaves>), grid, dim3(64 * kAttnMfmaWaves), 0, s, p);
+  else if (p.hd == 64)
+    hipLaunchKernelGGL((attn_decode_mfma_kernel<64, kAttnMfmaWaves>), grid, dim3(64 * kAttnMfmaWaves), 0, s, p);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 template <int HD>

@@ -171,9 +171,6 @@ hipError_t launch_gemv(int epi, int rows_per_wg, int chunks_in_flight, bool norm
 hipError_t launch_gemv_src(int epi, int rows_per_wg, int chunks_in_flight, bool norm, const GemvParams& p,
                            hipStream_t s);
 hipError_t launch_attn_decode(const AttnParams& p, int batch, hipStream_t s);
-// Whether launch_attn_decode takes the matrix-core kernel (its splits may then
-// be any multiple of kAttnMfmaAlign) rather than the vector-ALU one.
-bool attn_mfma_enabled();
 // Head h of row b merged from the attention partials in p, to o16[b][h*hd:(h+1)*hd]
 // (fp16) or, with o16 NULL, to o32[b][h*hd:(h+1)*hd] (fp32).
 hipError_t launch_attn_merge(const AttnParams& p, uint16_t* o16, float* o32, int batch, hipStream_t s);

@@ -764,23 +764,19 @@ kf_status kf_kv_read(const kf_kv* kv, int32_t layer, int32_t user, int32_t pos0,
 }
 
 // ------------------------------------------------------------------ decode
-// Keys per split-KV workgroup: sized from the keys of the whole batch, so that
-// about KF_ATTN_TARGET_WGS workgroups carry keys however ragged the contexts are
-// (a row shorter than the longest has idle trailing splits, which exit at once;
-// few, long splits keep the merge cheap at short contexts), but no more than
-// KF_ATTN_KEYS_PER_WG keys each, so that long contexts spread over more
-// workgroups (a workgroup streams its keys with one chunk in flight per wave).
-// From batch 2 the target doubles: the rows' keys then keep two workgroups per
-// CU busy (32B-shaped batch 4 at 4096 keys: 24.7 -> 19.2 us), while at batch 1
-// the extra partials cost the merge in the output projection more than they
-// save.  The split never exceeds the partial-buffer capacity per row.
+// Keys per split-KV workgroup at batch 1: about KF_ATTN_TARGET_WGS workgroups
+// over the row's keys, whole pages, at most KF_ATTN_KEYS_PER_WG keys (long
+// contexts spread over more workgroups).  Fewer, longer splits than one
+// workgroup per CU, since every extra partial costs the merge in the output
+// projection (8B-shaped: 17 splits of 128 keys for 2049 keys).  The split
+// never exceeds the partial-buffer capacity per row.
 #ifndef KF_ATTN_KEYS_PER_WG
 #define KF_ATTN_KEYS_PER_WG 512
 #endif
-static_assert(KF_ATTN_ALIGN % kKvPage == 0, "splits start on page boundaries");
-static void attn_split(int nkv, int batch, int64_t total_len, int max_len, int max_split, int* split, int* n_split) {
+static_assert(KF_ATTN_ALIGN % kKvPage == 0, "batch-1 splits start on page boundaries");
+static void attn_split(int nkv, int64_t total_len, int max_len, int max_split, int* split, int* n_split) {
   auto up = [](int64_t v) { return (int)((v + KF_ATTN_ALIGN - 1) / KF_ATTN_ALIGN * KF_ATTN_ALIGN); };
-  const int64_t target = batch > 1 ? 2 * KF_ATTN_TARGET_WGS : KF_ATTN_TARGET_WGS;
+  const int64_t target = KF_ATTN_TARGET_WGS;
   int sp = up((total_len * nkv + target - 1) / target);
   if (sp > KF_ATTN_KEYS_PER_WG) sp = KF_ATTN_KEYS_PER_WG;
   const int need = up((max_len + max_split - 1) / max_split);
@@ -849,12 +845,9 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
   hipStream_t st = s->stream;
 
   int split, n_split;
-  const bool attn_mfma = attn_mfma_enabled();
-  if (attn_mfma && batch > 1)
-    attn_split_mfma(c.n_kv_heads, total_len, max_len, kv->max_split, s->n_cu, &split, &n_split);
-  else attn_split(c.n_kv_heads, batch, total_len, max_len, kv->max_split, &split, &n_split);
-  if (split % (attn_mfma ? kAttnMfmaAlign : kKvPage))
-    return fail(KF_EINVAL, "split of %d keys breaks the attention kernel's alignment", split);
+  if (batch > 1) attn_split_mfma(c.n_kv_heads, total_len, max_len, kv->max_split, s->n_cu, &split, &n_split);
+  else attn_split(c.n_kv_heads, total_len, max_len, kv->max_split, &split, &n_split);
+  if (split % kAttnMfmaAlign) return fail(KF_EINVAL, "split of %d keys breaks the attention kernel's alignment", split);
   int64_t upto[kMaxBatch];
   for (int b = 0; b < batch; ++b) upto[b] = (int64_t)positions[b] + 1;
   const kf_status gst = kv_grant(kv, batch, users, upto);
