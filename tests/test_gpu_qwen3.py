@@ -129,3 +129,46 @@ def test_qwen3_32b_prefill_chunk_as_benched(torch, st):
     print("qwen3-32b chunk max row rel err", worst)
     kv.close()
     g.close()
+
+
+def test_tiny_paged_batch4_new_keys_inside_pages(torch, st):
+    """Batch-4 decode of q/k-norm blocks over a paged cache whose pages are scattered.
+
+    The contexts (3000 / 2000 / 2500 / 900 keys, injected one 64-position page
+    per user in turn) make the batch's split-KV workgroups 80 keys long, so
+    splits start inside pages, and over the steps each row's new key falls at
+    different offsets of its 16-key block: the workgroup holding it normalises,
+    rotates and stores it, and scores it in place of the stale cache row.
+    """
+    page = 64
+    model = SeededModel(TINY, CFG)
+    ctx = (3000, 2000, 2500, 900)
+    max_ctx = max(ctx) + 8
+    npages = sum((n + 5 + page - 1) // page for n in ctx)
+    g = st.Stage(TINY, 0, 2, model.layer, None)
+    kv = g.kv(4, max_ctx, pages=npages)
+    o = OracleStage(TINY, 0, 2, model.layer, None, max_users=4, max_ctx=max_ctx)
+    full = {(l, u): synth.injected_kv(TINY, CFG, l, u, n) for l in (0, 1) for u, n in enumerate(ctx)}
+    for p0 in range(0, max(ctx), page):
+        for u, n in enumerate(ctx):
+            if p0 >= n:
+                continue
+            m = min(page, n - p0)
+            for l in (0, 1):
+                kb, vb = full[(l, u)]
+                kv.write(l, u, p0, dev(torch, kb[p0:p0 + m].view(np.int16)), dev(torch, vb[p0:p0 + m].view(np.int16)))
+            kv.set_len(u, p0 + m)
+    for (l, u), (kb, vb) in full.items():
+        o.kv.inject(l, u, 0, kb, vb)
+    for u, n in enumerate(ctx):
+        o.kv.set_len(u, n)
+    worst = 0.0
+    users = [1, 3, 0, 2]
+    for step in range(5):
+        pos = [kv.len(u) for u in users]
+        x = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, step, 4, TINY.hidden)
+        y = g.decode(kv, users, pos, hidden=dev(torch, x))
+        worst = max(worst, assert_hidden_close(host(y), o.decode(users, pos, hidden=x), what=f"decode {step}"))
+    print("qwen3 tiny paged batch-4 max row rel err", worst)
+    kv.close()
+    g.close()
