@@ -169,8 +169,11 @@ __device__ __forceinline__ const uint16_t* gemv_row(const GemvParams& p, int wg,
     const int row = head * p.hd + (r < R / 2 ? i0 + r : p.hd / 2 + i0 + r - R / 2);
     return p.w0 + (int64_t)row * p.K;
   } else if (EPI == kEpiSwiGLU) {
+    // R / 2 outputs per workgroup; unless R / 2 divides 64 (and so every
+    // supported ffn), the last workgroup has rows past the end
     const int row = wg * (R / 2) + (r < R / 2 ? r : r - R / 2);
-    return (r < R / 2 ? p.w0 : p.w1) + (int64_t)row * p.K;
+    ok = 64 % (R / 2) == 0 || row < p.N;
+    return (r < R / 2 ? p.w0 : p.w1) + (int64_t)(ok ? row : 0) * p.K;
   } else {
     const int row = wg * R + r;
     ok = row < p.N;
@@ -264,7 +267,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams& p, int wg, const
       }
     }
   } else if (EPI == kEpiSwiGLU) {
-    if (tid < (R / 2) * B) {
+    if (tid < (R / 2) * B && (64 % (R / 2) == 0 || wg * (R / 2) + tid / B < p.N)) {
       const int r = tid / B, b = tid % B;
       const float gt = fin[r * B + b] * rs[b];
       const float up = fin[(r + R / 2) * B + b] * rs[b];
@@ -340,9 +343,12 @@ __device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, in
 // The weight bytes in flight per CU scale with resident waves; at batch 3-4 the
 // input rows and partial sums put the kernel just past 128 VGPRs (3 waves per
 // SIMD), so the register budget is held to 4 waves there.  Smaller batches are
-// left to the compiler (a cap costs the batch-1 gate/up kernel a wave).
+// left to the compiler (a cap costs the batch-1 gate/up kernel a wave).  The
+// 12-row workgroups of batch 4 need about 160 VGPRs and are held to 3 waves
+// (at 4 they spill, and ran slower than 8 rows).
 template <int B, int R, int U, int EPI, bool NORM, bool SRC = false, bool IN16 = false>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(B >= 3 ? KF_GEMV_MIN_WAVES : 1)))
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(B >= 3 ? (R > 10 ? 3 : KF_GEMV_MIN_WAVES) : 1)))
 void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
   constexpr int NV = R * B + (NORM ? B : 0);
@@ -1326,7 +1332,7 @@ static hipError_t gemv_dispatch_b(int epi, bool norm, const GemvParams& p, int g
 int gemv_grid(int epi, int R, const GemvParams& p) {
   switch (epi) {
     case kEpiQKV: return (p.nq + 2 * p.nkv) * (p.hd / R);
-    case kEpiSwiGLU: return p.N / (R / 2);
+    case kEpiSwiGLU: return (p.N + R / 2 - 1) / (R / 2);
     default: return (p.N + R - 1) / R;
   }
 }
@@ -1338,27 +1344,35 @@ hipError_t launch_gemv_src(int epi, int R, int U, bool norm, const GemvParams& p
   return hipErrorInvalidValue;
 }
 
-// Residual GEMV in workgroups of 4 rows (fp16 inputs from batch 2, as at 8 rows).
-template <int B>
-static hipError_t resid4_launch(const GemvParams& p, int grid, hipStream_t s) {
+// Residual GEMV in workgroups of 4 or 10 rows (fp16 inputs from batch 2, as at 8 rows).
+template <int B, int R>
+static hipError_t resid_launch(const GemvParams& p, int grid, hipStream_t s) {
   if (B > 1 && p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, 4, 1, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemv_kernel<B, R, 1, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((gemv_kernel<B, 4, 1, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((gemv_kernel<B, R, 1, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
   return hipGetLastError();
+}
+template <int R>
+static hipError_t resid_dispatch_b(const GemvParams& p, int grid, hipStream_t s) {
+  switch (p.batch) {
+    case 1: return resid_launch<1, R>(p, grid, s);
+    case 2: return resid_launch<2, R>(p, grid, s);
+    case 3: return resid_launch<3, R>(p, grid, s);
+    case 4: return resid_launch<4, R>(p, grid, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hipStream_t s) {
   const int grid = gemv_grid(epi, R, p);
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
-  if (R == 4 && U == 1 && epi == kEpiResid && !norm) {
-    switch (p.batch) {
-      case 1: return resid4_launch<1>(p, grid, s);
-      case 2: return resid4_launch<2>(p, grid, s);
-      case 3: return resid4_launch<3>(p, grid, s);
-      case 4: return resid4_launch<4>(p, grid, s);
-      default: return hipErrorInvalidValue;
-    }
+  if (R == 4 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<4>(p, grid, s);
+  if (R == 10 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<10>(p, grid, s);
+  // Batch-4 gate/up in workgroups of 12 rows (fp16 inputs)
+  if (R == 12 && U == 1 && p.batch == 4 && p.in16 && norm && epi == kEpiSwiGLU) {
+    hipLaunchKernelGGL((gemv_kernel<4, 12, 1, kEpiSwiGLU, true, false, true>), dim3(grid), dim3(256), 0, s, p);
+    return hipGetLastError();
   }
   // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
   // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.

@@ -32,6 +32,29 @@ static int resid_rows(int n, int n_cu) {
   if ((n / 8) % n_cu != 0 && n % 4 == 0 && (n / 4) % n_cu == 0) return 4;
   return 8;
 }
+// Rows per workgroup of the down projection (K = ffn, the longest rows): 10 when
+// that grid is a whole number of rounds over the compute units, else the
+// residual rule.  Each workgroup reads its input rows once for all its weight
+// rows, so more rows per workgroup move fewer input bytes through the vector
+// caches (at batch 4 a 4-row workgroup reads as many input bytes as weight
+// bytes).  H = 5120: 512 workgroups of 10 rows, 2 per CU; the 32B-shaped down
+// projection went from 45.4 to 44.4 us at batch 1 and 51.5 to 46.5 us at batch 4.
+// 16 rows at H = 8192 were slower (70B-shaped batch 1: 69.7 -> 70.8 us), and so
+// were 10 rows for the output projection (K = heads x hd, 16.5 -> 17.0 us).
+static int down_rows(int n, int n_cu) {
+  if (n % 10 == 0 && (n / 10) % n_cu == 0) return 10;
+  return resid_rows(n, n_cu);
+}
+// Rows per workgroup of the gate/up launch: at batch 4, 12 (6 gate and 6 up
+// rows: two thirds of the fp16 input-row reads per weight byte of 8 rows, at 3
+// waves per SIMD) when that grid is a whole number of rounds over the compute
+// units, else 8.  32B-shaped (ffn 27648, 4608 workgroups): 88.6 -> 87.1 us; at
+// the 8B shape (ffn 14336, a partial last round) 12 rows were slower (39.4 ->
+// 40.3 us), and so were 12-row LM-head launches within noise (154.4 -> 153.5 us).
+static int gateup_rows(int batch, int ffn, int n_cu) {
+  if (batch == 4 && ffn % 6 == 0 && (ffn / 6) % n_cu == 0) return 12;
+  return kGemvRows;
+}
 #ifndef KF_ATTN_TARGET_WGS
 #define KF_ATTN_TARGET_WGS 256
 #endif
@@ -991,7 +1014,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.err_flag = s->err_flag;
     {
       tr.begin(KF_K_GATEUP);
-      const hipError_t le = launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
+      const hipError_t le = launch_gemv(kEpiSwiGLU, gateup_rows(batch, c.ffn, s->n_cu), kGemvChunks, true, gu, st);
       tr.end(KF_K_GATEUP);
       KF_HIP(le, "gate/up launch");
     }
@@ -1014,7 +1037,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     }
     {
       tr.begin(KF_K_DOWN);
-      const hipError_t le = launch_gemv(kEpiResid, resid_rows(H, s->n_cu), kGemvChunks, false, d, st);
+      const hipError_t le = launch_gemv(kEpiResid, down_rows(H, s->n_cu), kGemvChunks, false, d, st);
       tr.end(KF_K_DOWN);
       KF_HIP(le, "down launch");
     }
