@@ -186,6 +186,18 @@ def test_32b_stage_decode_batch_1_and_4(torch, kf):
     g.close()
 
 
+def test_32b_two_layers_batch_2_and_3_ragged(torch, kf):
+    """Layers [16,18) of the 32B shape with ragged contexts {4096, 1500, 333}: one step at batch 2 and
+    one at batch 3 (the down projection's 10-row workgroups at these batches, fp16 inputs, and
+    attention splits that end inside the shorter rows)."""
+    wl = synth.WORKLOADS["32b_b4"]
+    g, kv, o, _ = build(torch, kf, wl, 16, 18, 3, 4096 + 8, (4096, 1500, 333))
+    print("max row rel err", decode_steps(torch, g, kv, o, wl, [2, 0], 1),
+          decode_steps(torch, g, kv, o, wl, [1, 2, 0], 1, first_step=20))
+    kv.close()
+    g.close()
+
+
 def test_70b_prefill_chunk_one_layer(torch, kf):
     """Layer 40 of the 70B shape: a 512-token prefill chunk at positions [3584, 4096) on top of an
     injected cache for [0, 3584) (all 512 output rows compared), then 2 decode steps."""
