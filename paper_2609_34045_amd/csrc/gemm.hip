@@ -276,15 +276,17 @@ __device__ __forceinline__ void gemm_wave(const Params& p, uint8_t* smem, const 
   }
 }
 
-// Tiles of 256 rows x 32 NB columns (NB = 8, or 7 for the SwiGLU launch when
-// 224-column tiles fill whole rounds of the chip: see gemm_tile_blocks).  With
-// NB = 8 the eight waves are 2 x 4 of 128 x 64; with NB = 7 they are 4 x 2 of
-// 64 x 128 and 64 x 96, so that with waves dealt to the SIMDs round-robin each
-// SIMD holds one of each (7 blocks).  The W tile is loaded as 256 rows either
-// way; rows past 32 NB repeat the tile's last row and are not used.
+// Tiles of 256 rows x 32 NB columns (NB = 8; 7, 5 or 4 where narrower tiles
+// fill the chip in fewer tile-times: see gemm_tile_blocks).  With NB = 8 the
+// eight waves are 2 x 4 of 128 x 64; with NB = 7 (5) they are 4 x 2 of 64 x 128
+// (96) and 64 x 96 (64), so that with waves dealt to the SIMDs round-robin each
+// SIMD holds one of each; with NB = 4, 4 x 2 of 64 x 64.  The W tile is loaded
+// as 256 rows for NB = 8 and 7 (rows past 32 NB repeat the tile's last row and
+// are not used); for NB = 5 and 4 only the loads that hold the tile's rows are
+// issued.
 template <int EPI, int NB>
 __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
-  static_assert(NB == 8 || NB == 7, "tile widths");
+  static_assert(NB == 8 || NB == 7 || NB == 5 || NB == 4, "tile widths");
   // SA A tiles, then SW W tiles, each [256 rows][CH swizzled 16-byte chunks]; both fp16.
   __shared__ __attribute__((aligned(1024))) uint8_t smem[(SA + SW) * TILE_BYTES];
 
@@ -335,6 +337,14 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
   }
   if (NB == 8) {
     gemm_wave<EPI, 4, 2, LOADS>(p, smem, asrc, wsrc, nk, wave, lane, m0, n0, 128 * (wave / 4), 2 * (wave % 4), ks);
+  } else if (NB == 5) {
+    // W tile load j of wave w fills rows 8 (8 j + w) ..: rows 0..127 take
+    // loads 0 and 1 of every wave, rows 128..159 load 2 of waves 0..3
+    static_assert(LOADS == 4, "1 KB loads of 8 rows");
+    if (wave < 4) gemm_wave<EPI, 2, 3, 3>(p, smem, asrc, wsrc, nk, wave, lane, m0, n0, 64 * wave, 0, ks);
+    else gemm_wave<EPI, 2, 2, 2>(p, smem, asrc, wsrc, nk, wave, lane, m0, n0, 64 * (wave - 4), 3, ks);
+  } else if (NB == 4) {
+    gemm_wave<EPI, 2, 2, 2>(p, smem, asrc, wsrc, nk, wave, lane, m0, n0, 64 * (wave & 3), 2 * (wave >> 2), ks);
   } else {
 #ifndef KF_GEMM_NB7_PAIRS
 #define KF_GEMM_NB7_PAIRS 0
@@ -356,8 +366,9 @@ __global__ __launch_bounds__(kGemmThreads) void gemm256_kernel(const Params p) {
 #define KF_GEMM_MAX_SPLIT 8  // upper bound on K slices per output tile
 #endif
 
-int gemm_splitk(int M, int N, int K) {
-  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+// K slices for tiles of 32 nb columns.
+static int splitk_for(int M, int N, int K, int nb) {
+  const int tiles = ((M + BM - 1) / BM) * ((N + 32 * nb - 1) / (32 * nb));
   const int k32 = K / 32;
   if (tiles >= 192 || k32 < 128) return 1;  // enough tiles, or a short (cheap) reduction
   int s = KF_GEMM_SPLIT_FLOOR ? 256 / tiles : (256 + tiles - 1) / tiles;
@@ -366,11 +377,46 @@ int gemm_splitk(int M, int N, int K) {
   return s < 1 ? 1 : s;
 }
 
+#ifndef KF_GEMM_NARROW
+#define KF_GEMM_NARROW 1  // split-K tiles of 160 or 128 columns where they take fewer tile-times
+#endif
+#ifndef KF_GEMM_NARROW_COST
+#define KF_GEMM_NARROW_COST 13  // cost of a narrow tile's column-step, in tenths of a 256-column tile's
+#endif
+// Tile width of the split-K (partial-sum) launch: the number of 32-column
+// blocks (8, 5 or 4) whose grid, tiles x K slices, takes the fewest
+// tile-times over the 256 CUs.  A tile-time is its columns times its K steps,
+// weighted 1.3x for the narrow tiles: per column-step they measured 1.12-1.34x
+// the 256-column tile's (fewer MFMAs per fragment read, and a fuller chip runs
+// at a lower clock).  The Qwen3-32B-shaped QKV and output projections (160 of
+// the 256 CUs busy with 256-column tiles) gain: 69.0 -> 57.0 and 57.3 -> 47.8 us
+// with 160-column tiles, where its down projection (240 workgroups either way)
+// lost 122 -> 140 us and the 70B-shaped QKV projection 83.6 -> 87.3 us.
+static int partial_tile_blocks(int M, int N, int K) {
+  if (!KF_GEMM_NARROW) return 8;
+  const int mt = (M + BM - 1) / BM, nk = K / BK;
+  int best = 8;
+  int64_t best_cost = 0;
+  for (int nb : {8, 5, 4}) {
+    const int s = splitk_for(M, N, K, nb);
+    const int64_t wgs = (int64_t)mt * ((N + 32 * nb - 1) / (32 * nb)) * s;
+    const int64_t cost = (wgs + 255) / 256 * nb * ((nk + s - 1) / s) * (nb == 8 ? 10 : KF_GEMM_NARROW_COST);
+    if (nb == 8 || cost < best_cost) {
+      best = nb;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+int gemm_splitk(int M, int N, int K) { return splitk_for(M, N, K, partial_tile_blocks(M, N, K)); }
+
 // 32-column blocks per tile: 7 for the SwiGLU launch when 224-column tiles take
 // fewer tile-times than 256-column ones over whole rounds of the 256 CUs
 // (70B gate/up: 512 tiles of 7 blocks in 2 rounds against 448 of 8, the second
 // round three quarters full), else 8.
-int gemm_tile_blocks(int epi, int M, int N) {
+int gemm_tile_blocks(int epi, int M, int N, int K) {
+  if (epi == kGemmPartialF32) return partial_tile_blocks(M, N, K);
   if (epi != kGemmSwiGLU) return 8;
   const int mt = (M + BM - 1) / BM;
   auto cost = [&](int nb) { return ((mt * ((N + 32 * nb - 1) / (32 * nb)) + 255) / 256) * nb; };
@@ -383,7 +429,7 @@ hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint
   if (epi == kGemmSwiGLU && N % 32) return hipErrorInvalidValue;  // whole 16-output gate/up blocks
   // the nonlinearity and the residual update need complete sums: only the partial epilogue splits K
   Params p{A, W, W2, M, N, K, epi == kGemmPartialF32 ? gemm_splitk(M, N, K) : 1, C, Cb, err_flag};
-  const int nb = gemm_tile_blocks(epi, M, N);
+  const int nb = gemm_tile_blocks(epi, M, N, K);
   const int grid = ((M + BM - 1) / BM) * ((N + 32 * nb - 1) / (32 * nb)) * p.splitk;
   switch (epi) {
     case kGemmResidF32:
@@ -394,7 +440,9 @@ hipError_t launch_gemm(int epi, const uint16_t* A, const uint16_t* W, const uint
       else hipLaunchKernelGGL((gemm256_kernel<kGemmSwiGLU, 8>), dim3(grid), dim3(kGemmThreads), 0, s, p);
       break;
     case kGemmPartialF32:
-      hipLaunchKernelGGL((gemm256_kernel<kGemmPartialF32, 8>), dim3(grid), dim3(kGemmThreads), 0, s, p);
+      if (nb == 5) hipLaunchKernelGGL((gemm256_kernel<kGemmPartialF32, 5>), dim3(grid), dim3(kGemmThreads), 0, s, p);
+      else if (nb == 4) hipLaunchKernelGGL((gemm256_kernel<kGemmPartialF32, 4>), dim3(grid), dim3(kGemmThreads), 0, s, p);
+      else hipLaunchKernelGGL((gemm256_kernel<kGemmPartialF32, 8>), dim3(grid), dim3(kGemmThreads), 0, s, p);
       break;
     default: return hipErrorInvalidValue;
   }
