@@ -99,3 +99,30 @@ def test_prefill_swiglu_tile_widths(torch, st, ffn, T):
     print(f"ffn={ffn} T={T} prefill max row rel err", err)
     kv.close()
     g.close()
+
+
+@pytest.mark.parametrize("T", [300, 512], ids=["t300", "t512"])
+def test_prefill_splitk_tile_widths(torch, st, T):
+    """The split-K projections' three tile widths, against the float64 oracle.
+
+    A split-K launch takes tiles of 256 rows by 256, 160 or 128 columns,
+    whichever covers its grid in the fewest weighted tile-times.  At H 6144,
+    32 query heads and 8 KV heads of 128, FFN 8192, the QKV projection (6144
+    columns: the last 160-column tile is partial) takes 160 columns in 3 K
+    slices, the output projection 128 columns in 2, the down projection 256
+    in 4; their slices meet in the RoPE and row-norm kernels and in the
+    output store.  300 tokens end in a partial row tile.  One layer, a
+    prefill from hidden rows on an empty cache; every output row is compared.
+    """
+    shape = synth.ModelShape(1, 6144, 32, 8, 128, 8192, 300, 1e-5, 1e4)
+    cfg = 77
+    model = SeededModel(shape, cfg)
+    g = st.Stage(shape, 0, 1, model.layer, None)
+    kv = g.kv(1, T)
+    h = synth.hidden_states(cfg, synth.STREAM_PREFILL_HIDDEN, 0, T, shape.hidden)
+    y = g.prefill(kv, 0, 0, hidden=torch.from_numpy(h).cuda())
+    o = OracleStage(shape, 0, 1, model.layer, None, max_users=1, max_ctx=T)
+    err = assert_hidden_close(host(y), o.prefill(0, 0, hidden=h), what=f"prefill T {T}")
+    print(f"split-K tile widths T={T} prefill max row rel err", err)
+    kv.close()
+    g.close()
