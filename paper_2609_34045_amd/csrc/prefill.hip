@@ -18,6 +18,7 @@
 
 #include "kernels.h"
 #include <algorithm>
+#include <type_traits>
 
 #include "prefill.h"
 
@@ -537,20 +538,28 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   // Iteration blk: on entry K(blk + 1) and V(blk) were loaded (by this wave)
   // an iteration ago, and S(blk) is in sc.  After the barrier every wave's
   // loads have landed and every wave is done with K(blk) (read for S(blk))
-  // and V(blk - 1), so their stages take K(blk + 2) and V(blk + 1).
-  auto iteration = [&](int blk, f32x16 (&sc)[NT], f32x16 (&sn)[NT]) {
+  // and V(blk - 1), so their stages take K(blk + 2) and V(blk + 1).  The
+  // parity P of blk - blk0 is a compile-time constant, so every stage
+  // address is a constant and the fragment reads take it as their immediate
+  // offset (a stage chosen at run time cost a vector add per read).
+  auto iteration = [&](auto parity, int blk, f32x16 (&sc)[NT], f32x16 (&sn)[NT]) {
+    constexpr int P = decltype(parity)::value;
+    uint8_t* const k_this = smem + P * TILEB;  // K(blk), then K(blk + 2)
+    uint8_t* const k_next = smem + (1 - P) * TILEB;
+    uint8_t* const v_this = smem + (2 + P) * TILEB;
+    uint8_t* const v_next = smem + (3 - P) * TILEB;
     attn_wait_loads();
     attn_barrier();
     if (kp.table && blk + 2 >= pb + 64) {  // the window moves on (every 62 blocks)
       pb = blk + 1;
       load_pids();
     }
-    if (blk + 2 < blk1) issue(kc, blk + 2, kst(blk + 2));
-    if (blk + 1 < blk1) issue(vc, blk + 1, vst(blk + 1));
+    if (blk + 2 < blk1) issue(kc, blk + 2, k_this);
+    if (blk + 1 < blk1) issue(vc, blk + 1, v_next);
     if (blk * KB + KB - 1 > pos0 + i0 + wave * 32) mask(blk, sc);
     v4u pf[NT][2];
     float alpha;
-    if (blk + 1 < blk1) alpha = s_mfma_softmax(kst(blk + 1), sn, sc, pf);
+    if (blk + 1 < blk1) alpha = s_mfma_softmax(k_next, sn, sc, pf);
     else alpha = softmax(sc, pf);
     if (__ballot(alpha != 1.0f)) {  // no lane's reference moved: nothing to rescale
 #pragma unroll
@@ -558,7 +567,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
 #pragma unroll
         for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
     }
-    pv_mfma(vst(blk), pf);
+    pv_mfma(v_this, pf);
   };
 
   f32x16 sa[NT], sb[NT];
@@ -572,10 +581,10 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   }
   int blk = blk0;
   for (; blk + 1 < blk1; blk += 2) {
-    iteration(blk, sa, sb);
-    iteration(blk + 1, sb, sa);
+    iteration(std::integral_constant<int, 0>(), blk, sa, sb);
+    iteration(std::integral_constant<int, 1>(), blk + 1, sb, sa);
   }
-  if (blk < blk1) iteration(blk, sa, sb);
+  if (blk < blk1) iteration(std::integral_constant<int, 0>(), blk, sa, sb);
   attn_wait_loads();  // no direct load may still be writing LDS when the workgroup ends
 
   if (Z > 1) {  // unnormalised partial of this key split
