@@ -319,7 +319,10 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
   // every query of the workgroup, so the causal mask gives them weight 0; in
   // the block that holds nkeys - 1 they are loaded from that key instead, a
   // written row of the same page.
-  int dma_row[LPW], dma_chunk[LPW], dma_off[LPW];
+  // (unsigned lane offsets from the block's wave-uniform base: the loads take
+  // the base in scalar registers and the offset as their 32-bit vector operand)
+  int dma_row[LPW];
+  uint32_t dma_chunk[LPW], dma_off[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
     dma_row[j] = RPI * (4 * j + wave) + lane / CPR;
@@ -339,7 +342,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* q,
     } else {
 #pragma unroll
       for (int j = 0; j < LPW; ++j) {
-        const char* src = base + (min(dma_row[j], last) * ROWB + dma_chunk[j]);
+        const char* src = base + (uint32_t)(min(dma_row[j], last) * ROWB + dma_chunk[j]);
         uint8_t* d = dst + 1024 * (4 * j + wave);
         __builtin_amdgcn_global_load_lds(src, (lds_ptr)d, 16, 0, 0);
       }
