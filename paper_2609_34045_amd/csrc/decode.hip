@@ -716,7 +716,7 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 1 : 2) void attn_decode_mfma_ker
     const char* vb = reinterpret_cast<const char*>(p.vc + off);
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
-      const int byte = min(drow[j], last) * ROWB + dchunk[j];
+      const uint32_t byte = min(drow[j], last) * ROWB + dchunk[j];  // unsigned: a scalar base plus a 32-bit lane offset
       // (named operands: the host pass drops the kernel's launch stub when a
       // builtin's pointer argument is a compound expression)
       const char* ks = kb + byte;
