@@ -389,9 +389,10 @@ static int splitk_for(int M, int N, int K, int nb) {
 // weighted 1.3x for the narrow tiles: per column-step they measured 1.12-1.34x
 // the 256-column tile's (fewer MFMAs per fragment read, and a fuller chip runs
 // at a lower clock).  The Qwen3-32B-shaped QKV and output projections (160 of
-// the 256 CUs busy with 256-column tiles) gain: 69.0 -> 57.0 and 57.3 -> 47.8 us
-// with 160-column tiles, where its down projection (240 workgroups either way)
-// lost 122 -> 140 us and the 70B-shaped QKV projection 83.6 -> 87.3 us.
+// the 256 CUs busy with 256-column tiles) gain: 69.4 -> 59.4 and 57.9 -> 48.5 us
+// with 160-column tiles, where the unweighted rule's 160-column tiles for its
+// down projection (240 workgroups either way) lost 122 -> 140 us and for the
+// 70B-shaped QKV projection 83.6 -> 87.3 us.
 static int partial_tile_blocks(int M, int N, int K) {
   if (!KF_GEMM_NARROW) return 8;
   const int mt = (M + BM - 1) / BM, nk = K / BK;
@@ -411,10 +412,11 @@ static int partial_tile_blocks(int M, int N, int K) {
 
 int gemm_splitk(int M, int N, int K) { return splitk_for(M, N, K, partial_tile_blocks(M, N, K)); }
 
-// 32-column blocks per tile: 7 for the SwiGLU launch when 224-column tiles take
-// fewer tile-times than 256-column ones over whole rounds of the 256 CUs
-// (70B gate/up: 512 tiles of 7 blocks in 2 rounds against 448 of 8, the second
-// round three quarters full), else 8.
+// 32-column blocks per tile: for the split-K launch see partial_tile_blocks;
+// 7 for the SwiGLU launch when 224-column tiles take fewer tile-times than
+// 256-column ones over whole rounds of the 256 CUs (70B gate/up: 512 tiles of 7
+// blocks in 2 rounds against 448 of 8, the second round three quarters full);
+// else 8.
 int gemm_tile_blocks(int epi, int M, int N, int K) {
   if (epi == kGemmPartialF32) return partial_tile_blocks(M, N, K);
   if (epi != kGemmSwiGLU) return 8;
