@@ -19,8 +19,9 @@
 using namespace kf;
 
 // Launch shapes (compile-time; the defaults are the measured best on MI355X).
-// Decode GEMVs take 8 output rows per workgroup and one 16-byte chunk per row in
-// flight per thread (other shapes were measured slower at every batch).
+// Decode GEMVs take 8 output rows per workgroup by default (the rules below pick
+// 4, 10 or 12 where the grid then fills whole rounds of the CUs) and one
+// 16-byte chunk per row in flight per thread (two were slower at every batch).
 constexpr int kGemvRows = 8, kGemvChunks = 1;
 constexpr int kQkvRowsBatch1 = 4;  // the batch-1 QKV launch (after the first layer) takes 4-row workgroups
 
