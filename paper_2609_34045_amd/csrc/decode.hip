@@ -346,7 +346,11 @@ __device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, in
 // left to the compiler (a cap costs the batch-1 gate/up kernel a wave).  The
 // 12-row workgroups of batch 4 need about 160 VGPRs and are held to 3 waves
 // (at 4 they spill, and ran slower than 8 rows).
-template <int B, int R, int U, int EPI, bool NORM, bool SRC = false, bool IN16 = false>
+// With NORM and GAIN false the norm's gain has been folded into the weight
+// matrix's columns at stage init (W diag(g), rounded once to fp16): the input
+// rows meet the weights as they are, and only the sum of squares is taken
+// (from batch 2 by packed dot products of the fp16 inputs with themselves).
+template <int B, int R, int U, int EPI, bool NORM, bool SRC = false, bool IN16 = false, bool GAIN = true>
 __global__ __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(B >= 3 ? (R > 10 ? 3 : KF_GEMV_MIN_WAVES) : 1)))
 void gemv_kernel(const GemvParams p) {
@@ -412,7 +416,7 @@ void gemv_kernel(const GemvParams p) {
             xh[u][b] = src[1];
           }
         }
-        if (NORM) gv[u] = *reinterpret_cast<const v4u*>(p.gain + c * 8);
+        if (NORM && GAIN) gv[u] = *reinterpret_cast<const v4u*>(p.gain + c * 8);
       }
     };
     if (kInputFirst) load_input();
@@ -445,7 +449,7 @@ void gemv_kernel(const GemvParams p) {
           // input pairs in fp16; with the norm, x * gain rounded to fp16 (sum(x^2) in fp32)
           h2 xp[B][4];
           float gf[8];
-          if (NORM) bf16x8(gv[u], gf);
+          if (NORM && GAIN) bf16x8(gv[u], gf);
           if constexpr (kDotSrc) {
 #pragma unroll
             for (int b = 0; b < B; ++b) {
@@ -460,7 +464,7 @@ void gemv_kernel(const GemvParams p) {
           }
 #pragma unroll
           for (int b = 0; b < B; ++b) {
-            if (NORM) {
+            if (NORM && GAIN) {
               float f[8];
               f16x8_apart(xr[u][b], f);
 #pragma unroll
@@ -473,6 +477,12 @@ void gemv_kernel(const GemvParams p) {
               xp[b][1] = __builtin_shufflevector(x8, x8, 2, 3);
               xp[b][2] = __builtin_shufflevector(x8, x8, 4, 5);
               xp[b][3] = __builtin_shufflevector(x8, x8, 6, 7);
+              if (NORM) {  // the gain is in the weights: the squares of the fp16 inputs, summed in fp32
+                float q = acc[R * B + b];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) q = __builtin_amdgcn_fdot2(xp[b][j], xp[b][j], q, false);
+                acc[R * B + b] = q;
+              }
             }
           }
 #pragma unroll
@@ -500,13 +510,13 @@ void gemv_kernel(const GemvParams p) {
         }
         if (NORM) {
           float gf[8];
-          bf16x8(gv[u], gf);
+          if (GAIN) bf16x8(gv[u], gf);
 #pragma unroll
           for (int b = 0; b < B; ++b) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
               acc[R * B + b] += xf[b][i] * xf[b][i];
-              xf[b][i] *= gf[i];
+              if (GAIN) xf[b][i] *= gf[i];
             }
           }
         }
@@ -1238,6 +1248,31 @@ __global__ void weights_to_f16_kernel(uint16_t* w, int64_t n, int* bad) {
   if (flag) atomicOr(bad, 1);
 }
 
+// Whether every fp16 rounding of w[r][k] g[k] (bf16 w [rows][K] and g [K]) is
+// finite: flag set when one is not (its gain then stays out of the matrix).
+__global__ void gain_fold_check_kernel(const uint16_t* w, int64_t n, int K, const uint16_t* g, int* flag) {
+  int over = 0;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const float v = bf16_to_f32(w[i]) * bf16_to_f32(g[i % K]);  // exact in fp32 (8-bit significands)
+    over |= __builtin_isinf((float)(_Float16)v) && !__builtin_isnan(v);
+  }
+  if (over) atomicOr(flag, 1);
+}
+
+// In place: bf16 w[r][k] -> fp16 bits of w[r][k] g[k], rounded to nearest even
+// (the norm's gain folded into the matrix's columns).  Raises *bad when a
+// product lies beyond the fp16 range.
+__global__ void weights_to_f16_gain_kernel(uint16_t* w, int64_t n, int K, const uint16_t* g, int* bad) {
+  int flag = 0;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const float v = bf16_to_f32(w[i]) * bf16_to_f32(g[i % K]);
+    const _Float16 h = (_Float16)v;
+    flag |= __builtin_isinf((float)h) && !__builtin_isinf(v) && !__builtin_isnan(v);
+    w[i] = __builtin_bit_cast(uint16_t, h);
+  }
+  if (flag) atomicOr(bad, 1);
+}
+
 __global__ void store_hidden_kernel(const float* x, void* out, int out_bf16, int64_t n) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= n) return;
@@ -1286,24 +1321,32 @@ __global__ void kv_table_update_kernel(int* table, const KvTableUpdate u) {
 }
 
 // ------------------------------------------------------------------ launchers
+// A launch that folds RMSNorm into its product: with the gain (p.gain) applied
+// to the input rows, or, with p.gain NULL, already folded into the weights.
+template <int B, int R, int U, int EPI, bool SRC, bool IN16>
+static void gemv_norm_launch(const GemvParams& p, int grid, hipStream_t s) {
+  if (p.gain) hipLaunchKernelGGL((gemv_kernel<B, R, U, EPI, true, SRC, IN16, true>), dim3(grid), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((gemv_kernel<B, R, U, EPI, true, SRC, IN16, false>), dim3(grid), dim3(256), 0, s, p);
+}
+
 template <int B, int R, int U>
 static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
   if (epi == kEpiQKV && norm && B > 1 && p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiQKV, false, (B > 1)>(p, grid, s);
   else if (epi == kEpiQKV && norm && !p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiQKV, false, false>(p, grid, s);
   else if (epi == kEpiResid && !norm && B > 1 && p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiResid && !norm && !p.in16)
     hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiResid, false>), dim3(grid), dim3(256), 0, s, p);
   else if (epi == kEpiSwiGLU && norm && B > 1 && p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiSwiGLU, false, (B > 1)>(p, grid, s);
   else if (epi == kEpiSwiGLU && norm && !p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiSwiGLU, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiSwiGLU, false, false>(p, grid, s);
   else if (epi == kEpiLMHead && norm && B > 1 && p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true, false, (B > 1)>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiLMHead, false, (B > 1)>(p, grid, s);
   else if (epi == kEpiLMHead && norm && !p.in16)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiLMHead, false, false>(p, grid, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -1311,9 +1354,9 @@ static hipError_t gemv_dispatch_epi(int epi, bool norm, const GemvParams& p, int
 template <int B, int R, int U>
 static hipError_t gemv_dispatch_src(int epi, bool norm, const GemvParams& p, int grid, hipStream_t s) {
   if (epi == kEpiQKV && norm)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiQKV, true, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiQKV, true, false>(p, grid, s);
   else if (epi == kEpiLMHead && norm)
-    hipLaunchKernelGGL((gemv_kernel<B, R, U, kEpiLMHead, true, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<B, R, U, kEpiLMHead, true, false>(p, grid, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -1371,13 +1414,13 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   if (R == 10 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<10>(p, grid, s);
   // Batch-4 gate/up in workgroups of 12 rows (fp16 inputs)
   if (R == 12 && U == 1 && p.batch == 4 && p.in16 && norm && epi == kEpiSwiGLU) {
-    hipLaunchKernelGGL((gemv_kernel<4, 12, 1, kEpiSwiGLU, true, false, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<4, 12, 1, kEpiSwiGLU, false, true>(p, grid, s);
     return hipGetLastError();
   }
   // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
   // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.
   if (R == 4 && U == 1 && epi == kEpiQKV && p.batch == 1 && norm && !p.in16) {
-    hipLaunchKernelGGL((gemv_kernel<1, 4, 1, kEpiQKV, true>), dim3(grid), dim3(256), 0, s, p);
+    gemv_norm_launch<1, 4, 1, kEpiQKV, false, false>(p, grid, s);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;
@@ -1441,6 +1484,22 @@ hipError_t launch_weights_to_f16(uint16_t* w, int64_t n, int* bad, hipStream_t s
   if (n <= 0) return hipSuccess;
   const int64_t blocks = (n + 255) / 256;
   hipLaunchKernelGGL(weights_to_f16_kernel, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0, s, w, n, bad);
+  return hipGetLastError();
+}
+
+hipError_t launch_gain_fold_check(const uint16_t* w, int64_t n, int K, const uint16_t* g, int* flag, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(gain_fold_check_kernel, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0, s, w, n, K, g,
+                     flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_weights_to_f16_gain(uint16_t* w, int64_t n, int K, const uint16_t* g, int* bad, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(weights_to_f16_gain_kernel, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0, s, w, n, K,
+                     g, bad);
   return hipGetLastError();
 }
 

@@ -183,6 +183,10 @@ hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int n
 // In place over n elements: bf16 weights to fp16 (round to nearest even); *bad |= 1
 // if a finite weight is beyond the fp16 range.
 hipError_t launch_weights_to_f16(uint16_t* w, int64_t n, int* bad, hipStream_t s);
+// Sets *flag when some w[r][k] g[k] (bf16 w [n / K][K], bf16 g [K]) has no finite fp16 rounding.
+hipError_t launch_gain_fold_check(const uint16_t* w, int64_t n, int K, const uint16_t* g, int* flag, hipStream_t s);
+// In place: bf16 w[r][k] -> fp16 w[r][k] g[k] (the gain folded into the columns); *bad on an fp16 overflow.
+hipError_t launch_weights_to_f16_gain(uint16_t* w, int64_t n, int K, const uint16_t* g, int* bad, hipStream_t s);
 hipError_t launch_store_hidden(const float* x, void* out, int out_bf16, int64_t n, hipStream_t s);
 // Positions [pos0, pos0 + n) of one user in one layer (k, v: the layer's base)
 // from / to [n][nkv][hd] rows.  src_type: 0 fp32, 1 bf16, 2 fp16 (the kf_dtype values).

@@ -56,7 +56,8 @@ __device__ __forceinline__ f32x16 mfma32(v4u a, v4u b, f32x16 c) {
 }
 
 // ------------------------------------------------------------------ row RMSNorm -> fp16
-// Row RMSNorm of the residual stream to fp16.  With nsplit > 0 the row first
+// Row RMSNorm of the residual stream to fp16 (gain g, or none when g is NULL:
+// the gain is then folded into the next projection's weights).  With nsplit > 0 the row first
 // takes the nsplit split-K slices of the projection that just ran (part, slice
 // stride `stride`), added in slice order, and the sum is written back to x.
 // Threads move 16 bytes at a time and request every slice before adding; the
@@ -102,7 +103,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rows_f16_kernel(float* __restrict
 #pragma unroll 4
   for (int k = tid; k < H4; k += 256) {
     const v4f v = xr[k] * rs;
-    const uint2 gw = g4[k];
+    const uint2 gw = g4 ? g4[k] : uint2{0x3F803F80u, 0x3F803F80u};  // g NULL: folded into the next matrix (gain 1)
     o[k] = uint2{pack_f16_checked(v.x * __uint_as_float(gw.x << 16), v.y * __uint_as_float(gw.x & 0xffff0000u), bad),
                  pack_f16_checked(v.z * __uint_as_float(gw.y << 16), v.w * __uint_as_float(gw.y & 0xffff0000u), bad)};
   }
