@@ -343,16 +343,14 @@ __device__ __forceinline__ void stage_input_chunk(const GemvParams& p, int b, in
 // The weight bytes in flight per CU scale with resident waves; at batch 3-4 the
 // input rows and partial sums put the kernel just past 128 VGPRs (3 waves per
 // SIMD), so the register budget is held to 4 waves there.  Smaller batches are
-// left to the compiler (a cap costs the batch-1 gate/up kernel a wave).  The
-// 12-row workgroups of batch 4 need about 160 VGPRs and are held to 3 waves
-// (at 4 they spill, and ran slower than 8 rows).
+// left to the compiler (a cap costs the batch-1 gate/up kernel a wave).
 // With NORM and GAIN false the norm's gain has been folded into the weight
 // matrix's columns at stage init (W diag(g), rounded once to fp16): the input
 // rows meet the weights as they are, and only the sum of squares is taken
 // (from batch 2 by packed dot products of the fp16 inputs with themselves).
 template <int B, int R, int U, int EPI, bool NORM, bool SRC = false, bool IN16 = false, bool GAIN = true>
 __global__ __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(B >= 3 ? (R > 10 ? 3 : KF_GEMV_MIN_WAVES) : 1)))
+__attribute__((amdgpu_waves_per_eu(B >= 3 ? KF_GEMV_MIN_WAVES : 1)))
 void gemv_kernel(const GemvParams p) {
   constexpr int T = 256;
   constexpr int NV = R * B + (NORM ? B : 0);
@@ -1412,11 +1410,6 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
   if (R == 4 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<4>(p, grid, s);
   if (R == 10 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<10>(p, grid, s);
-  // Batch-4 gate/up in workgroups of 12 rows (fp16 inputs)
-  if (R == 12 && U == 1 && p.batch == 4 && p.in16 && norm && epi == kEpiSwiGLU) {
-    gemv_norm_launch<4, 12, 1, kEpiSwiGLU, false, true>(p, grid, s);
-    return hipGetLastError();
-  }
   // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
   // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.
   if (R == 4 && U == 1 && epi == kEpiQKV && p.batch == 1 && norm && !p.in16) {

@@ -20,7 +20,7 @@ using namespace kf;
 
 // Launch shapes (compile-time; the defaults are the measured best on MI355X).
 // Decode GEMVs take 8 output rows per workgroup by default (the rules below pick
-// 4, 10 or 12 where the grid then fills whole rounds of the CUs) and one
+// 4 or 10 for the residual launches where the grid then fills whole rounds of the CUs) and one
 // 16-byte chunk per row in flight per thread (two were slower at every batch).
 constexpr int kGemvRows = 8, kGemvChunks = 1;
 constexpr int kQkvRowsBatch1 = 4;  // the batch-1 QKV launch (after the first layer) takes 4-row workgroups
@@ -45,16 +45,6 @@ static int resid_rows(int n, int n_cu) {
 static int down_rows(int n, int n_cu) {
   if (n % 10 == 0 && (n / 10) % n_cu == 0) return 10;
   return resid_rows(n, n_cu);
-}
-// Rows per workgroup of the gate/up launch: at batch 4, 12 (6 gate and 6 up
-// rows: two thirds of the fp16 input-row reads per weight byte of 8 rows, at 3
-// waves per SIMD) when that grid is a whole number of rounds over the compute
-// units, else 8.  32B-shaped (ffn 27648, 4608 workgroups): 88.6 -> 87.1 us; at
-// the 8B shape (ffn 14336, a partial last round) 12 rows were slower (39.4 ->
-// 40.3 us), and so were 12-row LM-head launches within noise (154.4 -> 153.5 us).
-static int gateup_rows(int batch, int ffn, int n_cu) {
-  if (batch == 4 && ffn % 6 == 0 && (ffn / 6) % n_cu == 0) return 12;
-  return kGemvRows;
 }
 #ifndef KF_ATTN_TARGET_WGS
 #define KF_ATTN_TARGET_WGS 256
@@ -1053,7 +1043,7 @@ kf_status kf_stage_decode(kf_stage* s, kf_kv* kv, int32_t batch, const int32_t* 
     gu.err_flag = s->err_flag;
     {
       tr.begin(KF_K_GATEUP);
-      const hipError_t le = launch_gemv(kEpiSwiGLU, gateup_rows(batch, c.ffn, s->n_cu), kGemvChunks, true, gu, st);
+      const hipError_t le = launch_gemv(kEpiSwiGLU, kGemvRows, kGemvChunks, true, gu, st);
       tr.end(KF_K_GATEUP);
       KF_HIP(le, "gate/up launch");
     }
