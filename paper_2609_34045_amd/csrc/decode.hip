@@ -1259,13 +1259,15 @@ __global__ void gain_fold_check_kernel(const uint16_t* w, int64_t n, int K, cons
 
 // In place: bf16 w[r][k] -> fp16 bits of w[r][k] g[k], rounded to nearest even
 // (the norm's gain folded into the matrix's columns).  Raises *bad when a
-// product lies beyond the fp16 range.
+// product lies beyond the fp16 range, and, as for a matrix stored without its
+// gain, when a finite weight itself does (whatever its gain).
 __global__ void weights_to_f16_gain_kernel(uint16_t* w, int64_t n, int K, const uint16_t* g, int* bad) {
   int flag = 0;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const float v = bf16_to_f32(w[i]) * bf16_to_f32(g[i % K]);
+    const float x = bf16_to_f32(w[i]), v = x * bf16_to_f32(g[i % K]);
     const _Float16 h = (_Float16)v;
     flag |= __builtin_isinf((float)h) && !__builtin_isinf(v) && !__builtin_isnan(v);
+    flag |= __builtin_isinf((float)(_Float16)x) && !__builtin_isinf(x);
     w[i] = __builtin_bit_cast(uint16_t, h);
   }
   if (flag) atomicOr(bad, 1);
