@@ -1411,6 +1411,16 @@ hipError_t launch_gemv(int epi, int R, int U, bool norm, const GemvParams& p, hi
   const int grid = gemv_grid(epi, R, p);
   if (R == 8 && U == 1) return gemv_dispatch_b<8, 1, false>(epi, norm, p, grid, s);
   if (R == 4 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<4>(p, grid, s);
+  // The LM head on fp16 input rows (batch 2-4) in workgroups of 12 rows.
+  if (R == 12 && U == 1 && epi == kEpiLMHead && norm && p.in16) {
+    switch (p.batch) {
+      case 2: gemv_norm_launch<2, 12, 1, kEpiLMHead, false, true>(p, grid, s); break;
+      case 3: gemv_norm_launch<3, 12, 1, kEpiLMHead, false, true>(p, grid, s); break;
+      case 4: gemv_norm_launch<4, 12, 1, kEpiLMHead, false, true>(p, grid, s); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   if (R == 10 && U == 1 && epi == kEpiResid && !norm) return resid_dispatch_b<10>(p, grid, s);
   // Batch-1 QKV in workgroups of 4 rows (2 rotation pairs): twice the workgroups
   // of the 8-row launch, which measured 0.1 us faster per layer at the 8B shape.

@@ -24,6 +24,12 @@ using namespace kf;
 // 16-byte chunk per row in flight per thread (two were slower at every batch).
 constexpr int kGemvRows = 8, kGemvChunks = 1;
 constexpr int kQkvRowsBatch1 = 4;  // the batch-1 QKV launch (after the first layer) takes 4-row workgroups
+// The LM head on the rows a decode kept (fp16, batch 2-4) takes 12-row
+// workgroups: each reads its input rows once for all its weight rows, so these
+// move two thirds of the 8-row launch's input bytes per weight byte (8B-shaped
+// head stage at batch 4: 153.5 -> 152.2 us, V = 128256 = 12 x 10688).  The
+// caller's fp32 or bf16 rows keep 8-row workgroups.
+constexpr int kHeadRowsKept = 12;
 
 // Rows per workgroup of a residual GEMV with n output rows: 8, unless that
 // leaves the grid a fraction of a round over the compute units and 4 rows do
@@ -507,7 +513,7 @@ kf_status kf_stage_init(const kf_model_config* cfg, int32_t lo, int32_t hi, int3
   s->x16 = (uint16_t*)take(B * H * 2);
   if (c.qk_norm) s->kraw = (float*)take(B * c.n_kv_heads * hd * 4);
   if (has_head) {
-    s->lm_wg = (int)((V + kGemvRows - 1) / kGemvRows);
+    s->lm_wg = (int)((V + kGemvRows - 1) / kGemvRows);  // the 8-row grid, the larger of the LM head's two
     s->part_val = (float*)take(B * s->lm_wg * 4);
     s->part_idx = (int*)take(B * s->lm_wg * 4);
   }
@@ -1110,11 +1116,13 @@ static kf_status head_launch(kf_stage* s, int rows, const void* hidden, kf_dtype
   g.part_val = s->part_val;
   g.part_idx = s->part_idx;
   g.err_flag = s->err_flag;
-  g.n_wg = gemv_grid(kEpiLMHead, kGemvRows, g);
+  const int rows_per_wg = !hidden && rows > 1 ? kHeadRowsKept : kGemvRows;
+  g.n_wg = gemv_grid(kEpiLMHead, rows_per_wg, g);
+  if (g.n_wg > s->lm_wg) return fail(KF_EINVAL, "LM-head grid of %d workgroups above the partials' %d", g.n_wg, s->lm_wg);
   s->lm_wg_used = g.n_wg;
   tr.begin(KF_K_LMHEAD);
   const hipError_t e = hidden ? launch_gemv_src(kEpiLMHead, kGemvRows, kGemvChunks, true, g, s->stream)
-                              : launch_gemv(kEpiLMHead, kGemvRows, kGemvChunks, true, g, s->stream);
+                              : launch_gemv(kEpiLMHead, rows_per_wg, kGemvChunks, true, g, s->stream);
   tr.end(KF_K_LMHEAD);
   KF_HIP(e, "lm-head launch");
   return KF_OK;

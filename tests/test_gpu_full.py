@@ -124,6 +124,37 @@ def test_8b_head_planted_ties_at_full_vocab(torch, kf):
     g.close()
 
 
+def test_8b_head_planted_ties_on_kept_rows(torch, kf):
+    """V = 128256 on the rows a batch-4 decode kept (the head stage's path, 12-row workgroups): the
+    decode's output rows of one layer are taken from the oracle, and the LM head gets for row 0 an exact
+    tie across workgroups (2000 and 90001), for row 1 a tie inside one 12-row workgroup (60002 and
+    60010), for row 2 a planted maximum in the last row (128255); row 3 is unplanted.  GPU tokens equal
+    the oracle's, which are the lowest planted indices."""
+    wl = synth.WORKLOADS["8b_head"]
+    s = wl.shape
+    lw = synth.layer_weights(s, wl.cfg_id, 0, wl.seed)
+    hw = synth.head_weights(s, wl.cfg_id, wl.seed)
+    users, pos = [0, 1, 2, 3], [0, 0, 0, 0]
+    toks = synth.tokens(wl.cfg_id, 7, 4, s.vocab, wl.seed)
+    o = OracleStage(s, 0, 1, {0: lw}.__getitem__, hw, max_users=4, max_ctx=4)
+    y_ref = o.decode(users, pos, tokens=toks)
+    xh = rms_norm(y_ref, bf16_to_f64(hw["final_norm"]), s.rms_eps)
+    plants = {0: [90001, 2000], 1: [60010, 60002], 2: [128255]}
+    for b, rows in plants.items():
+        hw = plant_lm_rows(hw, xh[b], rows)
+    o = OracleStage(s, 0, 1, {0: lw}.__getitem__, hw, max_users=4, max_ctx=4)
+    want = o.argmax(o.decode(users, pos, tokens=toks))
+    assert [int(want[b]) for b in plants] == [2000, 60002, 128255]
+    g = kf.Stage(s, 0, 1, {0: lw}, hw)
+    kv = g.kv(4, 4)
+    assert g.decode(kv, users, pos, tokens=dev(torch, toks), keep=True) is None
+    t = g.head_argmax(None, rows=4).cpu().numpy()
+    assert np.array_equal(t, want), (t, want)
+    g.sync()
+    kv.close()
+    g.close()
+
+
 def test_8b_head_prefill_then_teacher_forced_decode(torch, head_stage):
     """Embedding + layers [0,4) + head; token prefill of 16/64/128/256 tokens (one chunk per user),
     then 8 greedy steps at batch 4 where both sides consume the oracle's token."""

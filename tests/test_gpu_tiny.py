@@ -161,16 +161,17 @@ def test_head_tokens_logits_argmax(torch, st, model):
 def test_head_reads_kept_rows(torch, st, model):
     """A head stage's decode may keep its output rows for the head instead of returning them (the
     member that holds the last blocks also samples): the head then reads the fp32 residual at batch 1
-    and its fp16 copy at batch 2-4.  Logits and greedy tokens match the oracle.  The kept rows serve
+    and its fp16 copy at batch 2-4 (in 12-row workgroups, V = 1000 leaving a 4-row tail).  Logits and
+    greedy tokens match the oracle.  The kept rows serve
     only a head call with the decode's batch, and only until the next decode returns its rows; a stage
     without the head cannot keep them."""
     g, kv, o = make(st, model, head=True)
-    for u, n in ((0, 24), (1, 9), (2, 40)):
+    for u, n in ((0, 24), (1, 9), (2, 40), (3, 17)):
         toks = synth.tokens(CFG, 10 + u, n, SHAPE.vocab)
         assert_hidden_close(host(g.prefill(kv, u, 0, tokens=dev(torch, toks))), o.prefill(u, 0, tokens=toks),
                             what=f"prefill {u}")
     rng = np.random.default_rng(5)
-    for step, users in enumerate(([0, 1, 2], [2], [1, 0], [0, 1, 2])):
+    for step, users in enumerate(([0, 1, 2], [2], [1, 0], [3, 0, 2, 1], [0, 1, 2])):
         pos = [kv.len(u) for u in users]
         toks = rng.integers(0, SHAPE.vocab, len(users)).astype(np.int32)
         assert g.decode(kv, users, pos, tokens=dev(torch, toks), keep=True) is None
