@@ -1184,7 +1184,8 @@ __global__ void prep_hidden_kernel(const void* __restrict__ in, int in_bf16, con
 
 // Second level of the greedy argmax: the per-workgroup (max, lowest row) pairs
 // of one batch row reduced by one 1024-thread workgroup.  Each thread requests
-// U pairs before comparing any, so the pass costs a few memory round trips.
+// U = 16 pairs before comparing any, so up to 16,384 pairs per row (every LM
+// head grid up to V = 131,072 at 8 rows per workgroup) take one memory round trip.
 __device__ __forceinline__ void argmax_take(float v, int ix, float& best, int& bidx) {
   if (v > best || (v == best && ix < bidx)) {
     best = v;
@@ -1194,7 +1195,7 @@ __device__ __forceinline__ void argmax_take(float v, int ix, float& best, int& b
 
 __global__ __launch_bounds__(1024) void argmax_final_kernel(const float* part_val, const int* part_idx, int n_wg,
                                                             int32_t* token, float* max_logit) {
-  constexpr int T = 1024, U = 8;
+  constexpr int T = 1024, U = 16;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* pv = part_val + (int64_t)b * n_wg;
   const int* pi = part_idx + (int64_t)b * n_wg;
