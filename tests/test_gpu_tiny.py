@@ -450,3 +450,27 @@ def test_kernel_profiling_records_every_launch(torch, st, model):
     assert g.profile_read() == {}
     kv.close()
     g.close()
+
+
+def test_argmax_partials_beyond_one_pass(torch, st):
+    """V = 140000 on the caller's rows (8-row workgroups): 17,500 per-workgroup partials per row, more
+    than the 16,384 the final argmax reads in one pass, so its second pass runs.  Row 0 gets an exact
+    tie between LM-head rows 8 and 139992 (partials 1 and 17499, one in each pass), row 1 a planted
+    maximum in the last row.  GPU tokens equal the oracle's, which are the lowest planted indices."""
+    import dataclasses
+    s = dataclasses.replace(SHAPE, vocab=140000)
+    layers = {0: synth.layer_weights(s, CFG, 0)}
+    hw = synth.head_weights(s, CFG)
+    h = synth.hidden_states(CFG, synth.STREAM_DECODE_HIDDEN, 77, 2, s.hidden)
+    xh = rms_norm(h.astype(np.float64), bf16_to_f64(hw["final_norm"]), s.rms_eps)
+    plants = {0: [139992, 8], 1: [139999]}
+    for b, rows in plants.items():
+        hw = plant_lm_rows(hw, xh[b], rows)
+    o = OracleStage(s, 0, 1, layers.__getitem__, hw, max_users=1, max_ctx=4)
+    want = o.argmax(h)
+    assert [int(w) for w in want] == [8, 139999]
+    g = st.Stage(s, 0, 1, layers, hw)
+    t = g.head_argmax(dev(torch, h)).cpu().numpy()
+    assert np.array_equal(t, want), (t, want)
+    g.sync()
+    g.close()
